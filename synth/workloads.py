@@ -1,0 +1,304 @@
+"""Seeded model weights and row tables shaped like the paper's LLMMap workloads.
+
+The paper runs its LM functions over database rows: one prompt per row
+(LLMMap, Sec. 2.3.2 "Refined LLMMap Prompting Pattern"), the rows sharing
+the instruction text of the prompt template (Appendix "Prompts"), with
+duplicate inputs removed first (Sec. 2.4 "Early Deduplication") and joins
+evaluated as LLMMap over DB-built pairs (Sec. 4.1, the ecomm self-join CTE).
+It publishes neither its datasets nor its checkpoints, so every input here is
+synthetic: uniform random token ids, a Llama-shaped decoder with N(0, 0.02)
+weights quantised to symmetric int4 with one fp16 scale per 32 consecutive
+input features (W4A16, Sec. 3.2 Table "tab:models"), and suffix lengths drawn
+to match the workload recipes below.
+
+Weight tensors are drawn with torch on a chosen device (the 8B shape has
+7e9 parameters; drawing them on the host would take minutes), so a given
+seed yields the same weights on the same device type.  Row tables are drawn
+with numpy PCG64 and are identical everywhere.
+
+Layout of a quantised matrix W [N][K] (y = x W^T):
+  qweight uint8 [N][Kp/2], Kp = K rounded up to 32; feature k sits in the
+  low nibble of byte k//2 when k is even, the high nibble when odd; each
+  nibble is a two's-complement int4 in [-8, 7]; pad features have q = 0.
+  scales float16 [N][Kp/32]: one scale per (row, group of 32 features).
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import List, Optional
+
+import numpy as np
+import torch
+
+GROUP = 32
+
+
+@dataclasses.dataclass(frozen=True)
+class ModelShape:
+    name: str
+    n_layers: int
+    d_model: int
+    n_heads: int
+    n_kv_heads: int
+    head_dim: int
+    d_ff: int
+    vocab: int
+    rope_theta: float
+    rms_eps: float = 1e-5
+    group_size: int = GROUP
+    shape_id: int = 0
+
+
+SHAPES = {
+    "tiny": ModelShape("tiny", 2, 256, 4, 4, 64, 688, 2048, 1e4, shape_id=1),
+    "1b": ModelShape("1b", 16, 2048, 32, 8, 64, 8192, 128256, 5e5, shape_id=2),
+    "8b": ModelShape("8b", 32, 4096, 32, 8, 128, 14336, 128256, 5e5, shape_id=3),
+}
+
+
+@dataclasses.dataclass
+class QMat:
+    qweight: torch.Tensor  # uint8 [N][Kp/2]
+    scales: torch.Tensor   # float16 [N][Kp/32]
+    n: int
+    k: int
+
+
+@dataclasses.dataclass
+class Layer:
+    attn_norm: torch.Tensor  # float32 [d]
+    mlp_norm: torch.Tensor   # float32 [d]
+    wq: QMat
+    wk: QMat
+    wv: QMat
+    wo: QMat
+    w_gate: QMat
+    w_up: QMat
+    w_down: QMat
+
+
+@dataclasses.dataclass
+class Weights:
+    shape: ModelShape
+    tok_embedding: torch.Tensor  # float16 [V][d]
+    lm_head: torch.Tensor        # float16 [V][d]
+    final_norm: torch.Tensor     # float32 [d]
+    layers: List[Layer]
+
+    def to(self, device) -> "Weights":
+        def qm(m: QMat) -> QMat:
+            return QMat(m.qweight.to(device), m.scales.to(device), m.n, m.k)
+        layers = [Layer(l.attn_norm.to(device), l.mlp_norm.to(device), qm(l.wq), qm(l.wk),
+                        qm(l.wv), qm(l.wo), qm(l.w_gate), qm(l.w_up), qm(l.w_down))
+                  for l in self.layers]
+        return Weights(self.shape, self.tok_embedding.to(device), self.lm_head.to(device),
+                       self.final_norm.to(device), layers)
+
+
+def _seed(*parts: int) -> int:
+    state = np.random.SeedSequence([int(p) for p in parts]).generate_state(2, np.uint32)
+    return int((int(state[0]) << 31) ^ int(state[1])) & ((1 << 62) - 1)
+
+
+def _normal(shape, std: float, seed: int, device) -> torch.Tensor:
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    return torch.randn(shape, generator=g, device=device, dtype=torch.float32) * std
+
+
+def quantize_int4_g32(w: torch.Tensor):
+    """Symmetric int4 with one fp16 scale per 32 consecutive input features.
+
+    Input generation, not part of the operator: s = fp16(max|w| / 7) per
+    group (1 if that is 0), q = clip(round_half_even(w / s), -8, 7).  Returns
+    (qweight uint8 [N][Kp/2], scales float16 [N][Kp/32]).
+    """
+    n, k = w.shape
+    kp = (k + GROUP - 1) // GROUP * GROUP
+    if kp != k:
+        w = torch.nn.functional.pad(w, (0, kp - k))
+    g = w.reshape(n, kp // GROUP, GROUP)
+    s = (g.abs().amax(-1) / 7.0).to(torch.float16)
+    s = torch.where(s == 0, torch.ones_like(s), s)
+    q = torch.round(g / s.float().unsqueeze(-1)).clamp_(-8, 7).to(torch.int16).reshape(n, kp)
+    lo = q[:, 0::2] & 0xF
+    hi = q[:, 1::2] & 0xF
+    packed = (lo | (hi << 4)).to(torch.uint8)
+    return packed.contiguous(), s.contiguous()
+
+
+def make_weights(shape: ModelShape, seed: int = 1234, device="cpu", std: float = 0.02,
+                 n_layers: Optional[int] = None) -> Weights:
+    """Random-init weights of `shape`, linear layers quantised to int4 g32.
+
+    Each tensor has its own stream keyed by (seed, shape, layer, tensor), so a
+    model with fewer layers is a prefix of the full one.
+    """
+    dev = torch.device(device)
+    sid = shape.shape_id
+    d, hd = shape.d_model, shape.head_dim
+    nq, nkv, f = shape.n_heads * hd, shape.n_kv_heads * hd, shape.d_ff
+    L = shape.n_layers if n_layers is None else n_layers
+
+    def qmat(layer: int, tid: int, n: int, k: int) -> QMat:
+        w = _normal((n, k), std, _seed(seed, sid, layer, tid), dev)
+        qw, sc = quantize_int4_g32(w)
+        del w
+        return QMat(qw, sc, n, k)
+
+    emb = _normal((shape.vocab, d), std, _seed(seed, sid, 10_000, 0), dev).to(torch.float16)
+    head = _normal((shape.vocab, d), std, _seed(seed, sid, 10_000, 1), dev).to(torch.float16)
+    ones = torch.ones(d, dtype=torch.float32, device=dev)
+    layers = []
+    for l in range(L):
+        layers.append(Layer(
+            attn_norm=ones.clone(), mlp_norm=ones.clone(),
+            wq=qmat(l, 0, nq, d), wk=qmat(l, 1, nkv, d), wv=qmat(l, 2, nkv, d),
+            wo=qmat(l, 3, d, nq), w_gate=qmat(l, 4, f, d), w_up=qmat(l, 5, f, d),
+            w_down=qmat(l, 6, d, f)))
+    return Weights(shape, emb, head, ones.clone(), layers)
+
+
+# --------------------------------------------------------------------------
+# Row tables
+# --------------------------------------------------------------------------
+
+KIND_BOOL, KIND_ENUM, KIND_INT = 0, 1, 2
+
+
+@dataclasses.dataclass
+class Workload:
+    """A table of rows for one LM-operator call.
+
+    Every row's sequence is prefix ++ child[row_child[r]] (if any) ++ suffix_r.
+    `tokens`/`offsets` is the CSR of the row suffixes.
+    """
+    name: str
+    shape: ModelShape
+    prefix: np.ndarray                  # int32 [P]
+    tokens: np.ndarray                  # int32 [sum S_r]
+    offsets: np.ndarray                 # int64 [n_rows + 1]
+    kind: int
+    allowed: np.ndarray                 # int32 [n_allowed]; INT: the 10 digit tokens
+    eos: int = -1
+    max_tokens: int = 1
+    children: Optional[List[np.ndarray]] = None   # second-level prefixes (joins)
+    row_child: Optional[np.ndarray] = None         # int32 [n_rows]
+
+    @property
+    def n_rows(self) -> int:
+        return len(self.offsets) - 1
+
+    def suffix(self, r: int) -> np.ndarray:
+        return self.tokens[self.offsets[r]:self.offsets[r + 1]]
+
+    def row_prefix(self, r: int) -> np.ndarray:
+        if self.row_child is None:
+            return self.prefix
+        return np.concatenate([self.prefix, self.children[int(self.row_child[r])]])
+
+    def subset(self, rows) -> "Workload":
+        rows = np.asarray(rows, dtype=np.int64)
+        parts = [self.suffix(int(r)) for r in rows]
+        lens = np.array([len(p) for p in parts], dtype=np.int64)
+        offs = np.zeros(len(rows) + 1, dtype=np.int64)
+        np.cumsum(lens, out=offs[1:])
+        toks = np.concatenate(parts).astype(np.int32) if parts else np.zeros(0, np.int32)
+        rc = None if self.row_child is None else self.row_child[rows].astype(np.int32)
+        return dataclasses.replace(self, name=f"{self.name}[subset {len(rows)}]", tokens=toks,
+                                   offsets=offs, row_child=rc)
+
+    @property
+    def n_suffix_tokens(self) -> int:
+        return int(self.offsets[-1])
+
+
+def _csr(parts):
+    lens = np.array([len(p) for p in parts], dtype=np.int64)
+    offs = np.zeros(len(parts) + 1, dtype=np.int64)
+    np.cumsum(lens, out=offs[1:])
+    toks = np.concatenate(parts).astype(np.int32) if parts else np.zeros(0, np.int32)
+    return toks, offs
+
+
+def _lognormal_lengths(rng, n, mean, lo, hi, sigma=0.75):
+    mu = math.log(mean) - sigma * sigma / 2.0
+    return np.clip(np.rint(rng.lognormal(mu, sigma, size=n)), lo, hi).astype(np.int64)
+
+
+def make_workload(name: str, seed: int = 7, n_rows: Optional[int] = None) -> Workload:
+    """Synthetic LM-operator table.  `name` is one of WORKLOADS.
+
+    filter_tiny   tiny decoder, 64 rows, prefix 96, suffix U{16..48}, bool
+    filter_1b     1B shape, 4,096 rows, prefix 384, suffix lognormal mean 40 in [8,256], bool
+    filter_8b     8B shape, 10,000 rows, prefix 512, suffix lognormal mean 60 in [8,512],
+                  enum over 24 tokens
+    map_int_8b    8B shape, prefix 256, 20,000 rows drawn Zipf(1.1) from 5,000 distinct
+                  suffixes of U{24..64} tokens; integer output over 10 digits + EOS, <= 4 tokens
+    join_8b       8B shape, instruction 320, 200 left x 200 right values of U{8..32} tokens,
+                  all 40,000 pairs left-major; bool; one child prefix per left value
+    `n_rows` truncates the table to its first rows (same draws otherwise).
+    """
+    cfg = WORKLOADS[name]
+    rng = np.random.default_rng([seed, cfg["id"]])
+    shape = SHAPES[cfg["shape"]]
+    V = shape.vocab
+    prefix = rng.integers(0, V, size=cfg["prefix"], dtype=np.int64).astype(np.int32)
+    n_allowed = cfg["n_allowed"]
+    allowed = rng.choice(V, size=n_allowed, replace=False).astype(np.int32)
+    eos = -1
+    if cfg["kind"] == KIND_INT:
+        while True:
+            e = int(rng.integers(0, V))
+            if e not in set(allowed.tolist()):
+                eos = e
+                break
+    children = row_child = None
+    if name == "map_int_8b":
+        n_distinct, n_total = 5000, 20000
+        lens = rng.integers(24, 65, size=n_distinct)
+        distinct = [rng.integers(0, V, size=int(s)).astype(np.int32) for s in lens]
+        ranks = np.arange(1, n_distinct + 1, dtype=np.float64)
+        p = ranks ** -1.1
+        p /= p.sum()
+        perm = rng.permutation(n_distinct)
+        draws = rng.choice(n_distinct, size=n_total, p=p)
+        parts = [distinct[perm[k]] for k in draws]
+    elif name == "join_8b":
+        n_left = n_right = 200
+        llen = rng.integers(8, 33, size=n_left)
+        rlen = rng.integers(8, 33, size=n_right)
+        children = [rng.integers(0, V, size=int(s)).astype(np.int32) for s in llen]
+        rights = [rng.integers(0, V, size=int(s)).astype(np.int32) for s in rlen]
+        parts = [rights[j] for i in range(n_left) for j in range(n_right)]
+        row_child = np.repeat(np.arange(n_left, dtype=np.int32), n_right)
+    else:
+        n = cfg["rows"]
+        if cfg["len"][0] == "uniform":
+            lens = rng.integers(cfg["len"][1], cfg["len"][2] + 1, size=n)
+        else:
+            lens = _lognormal_lengths(rng, n, cfg["len"][1], cfg["len"][2], cfg["len"][3])
+        parts = [rng.integers(0, V, size=int(s)).astype(np.int32) for s in lens]
+    if n_rows is not None:
+        parts = parts[:n_rows]
+        if row_child is not None:
+            row_child = row_child[:n_rows]
+    toks, offs = _csr(parts)
+    return Workload(name=name, shape=shape, prefix=prefix, tokens=toks, offsets=offs,
+                    kind=cfg["kind"], allowed=allowed, eos=eos, max_tokens=cfg["max_tokens"],
+                    children=children, row_child=row_child)
+
+
+WORKLOADS = {
+    "filter_tiny": dict(id=1, shape="tiny", rows=64, prefix=96, len=("uniform", 16, 48),
+                        kind=KIND_BOOL, n_allowed=2, max_tokens=1),
+    "filter_1b": dict(id=2, shape="1b", rows=4096, prefix=384, len=("lognormal", 40, 8, 256),
+                      kind=KIND_BOOL, n_allowed=2, max_tokens=1),
+    "filter_8b": dict(id=3, shape="8b", rows=10000, prefix=512, len=("lognormal", 60, 8, 512),
+                      kind=KIND_ENUM, n_allowed=24, max_tokens=1),
+    "map_int_8b": dict(id=4, shape="8b", rows=20000, prefix=256, len=None,
+                       kind=KIND_INT, n_allowed=10, max_tokens=4),
+    "join_8b": dict(id=5, shape="8b", rows=40000, prefix=320, len=None,
+                    kind=KIND_BOOL, n_allowed=2, max_tokens=1),
+}
