@@ -1,0 +1,195 @@
+/*
+ * lmop.h - C ABI of the LM-operator row-evaluation library (gfx950 / MI355X).
+ *
+ * The library evaluates one quantised decoder LM over every row of a table,
+ * the row-wise LM function of the paper (Sec. 2.3.2 "llmmap": for each row,
+ * the row's values v1..vk and the question Q form one prompt and the LM
+ * returns f(Q, v1..vk)), with the return type enforced by constrained
+ * decoding (Sec. 2.3 "Constrained Decoding": a declared return_type or an
+ * `options` set restricts what may be generated).  The prompt's shared part
+ * (instruction, type instructions, one-shot example, question: Appendix
+ * "Prompts") is a *prefix* whose keys/values are computed once and reused by
+ * every row (the serving setup enables prefix caching, Appendix "vLLM
+ * Config"); each row contributes only its own suffix tokens.  Identical rows
+ * are evaluated once (Sec. 2.4 "Early Deduplication of Database Values").
+ * Joins are LLMMap over DB-built pairs (Sec. 4.1, ecomm self-join example):
+ * a child prefix extends a root prefix with the left value, rows hold the
+ * right value.  Weights are W4A16 (Sec. 3.2, Table "tab:models"): int4 with
+ * one fp16 scale per 32 input features; embeddings and LM head are fp16.
+ *
+ * Conventions for every call:
+ *  - Every call returns lmop_status; nothing throws across the ABI.  On
+ *    error, lmop_last_error(ctx) describes the cause until the next call on
+ *    that ctx, and output buffers are left unspecified.
+ *  - A ctx is not thread-safe; use one ctx per host thread and stream.
+ *  - The caller owns every pointer it passes and may free it when the call
+ *    returns.  The library owns its device memory (weights, prefix KV,
+ *    activations) and frees it in lmop_release_prefix / lmop_destroy.
+ *  - LMOP_ERR_DEVICE is sticky: after a HIP error the ctx refuses further
+ *    work and must be destroyed.
+ *  - All calls are synchronous with respect to the host: when they return,
+ *    their device work on the ctx stream has completed.
+ */
+#ifndef LMOP_H
+#define LMOP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LMOP_OK = 0,
+  LMOP_ERR_INVALID_ARG = -1, /* a bad pointer, size, token id, layout or handle      */
+  LMOP_ERR_STATE = -2,       /* call out of order (e.g. eval before load_weights)     */
+  LMOP_ERR_OOM = -3,         /* a device or host allocation failed                    */
+  LMOP_ERR_DEVICE = -4,      /* a HIP call failed; sticky, the ctx must be destroyed  */
+  LMOP_ERR_UNSUPPORTED = -5  /* a model shape or option this build does not handle    */
+} lmop_status;
+
+typedef struct lmop_ctx lmop_ctx;       /* opaque */
+typedef struct lmop_prefix lmop_prefix; /* opaque; owned by its ctx */
+
+/* Decoder shape (Llama-style: RMSNorm, rotate-half RoPE, grouped-query
+ * attention, SwiGLU MLP; no biases).  Supported: head_dim 64 or 128,
+ * n_heads % n_kv_heads == 0, d_model % 64 == 0, group_size 32. */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff, vocab, group_size;
+  float rms_eps, rope_theta;
+  int32_t max_seq; /* longest prefix + suffix + generated tokens; 0 = 4096 */
+} lmop_config;
+
+/* Creates a ctx on HIP device `device` whose work runs on `hip_stream`
+ * (a hipStream_t; NULL = the library creates its own).  device = -1 creates
+ * a host-only ctx: every argument check runs, but calls that would touch a
+ * GPU return LMOP_ERR_UNSUPPORTED after validation.  On failure *out is NULL
+ * and lmop_last_error(NULL) describes the cause (per host thread). */
+lmop_status lmop_create(const lmop_config* cfg, int32_t device, void* hip_stream, lmop_ctx** out);
+void lmop_destroy(lmop_ctx* ctx); /* frees everything, including live prefixes; NULL is a no-op */
+const char* lmop_last_error(const lmop_ctx* ctx);
+const char* lmop_status_string(lmop_status s);
+
+/* One W4A16 linear map y = x W^T with W [n][k]:
+ *   qweight uint8 [n][kp/2], kp = k rounded up to 32: feature j is the low
+ *     nibble of byte j/2 when j is even, the high nibble when j is odd; each
+ *     nibble is a two's-complement int4 in [-8, 7]; pad features hold 0.
+ *   scales  fp16 bit patterns [n][kp/32]: W[r][j] = q[r][j] * scales[r][j/32]. */
+typedef struct {
+  const uint8_t* qweight;
+  const uint16_t* scales;
+  int32_t n, k;
+} lmop_qmat;
+
+typedef struct {
+  const float* attn_norm; /* fp32 [d_model] RMSNorm gain before attention */
+  const float* mlp_norm;  /* fp32 [d_model] RMSNorm gain before the MLP   */
+  lmop_qmat wq;           /* [n_heads*head_dim][d_model]    */
+  lmop_qmat wk, wv;       /* [n_kv_heads*head_dim][d_model] */
+  lmop_qmat wo;           /* [d_model][n_heads*head_dim]    */
+  lmop_qmat w_gate, w_up; /* [d_ff][d_model]                */
+  lmop_qmat w_down;       /* [d_model][d_ff]                */
+} lmop_layer;
+
+typedef struct {
+  const uint16_t* tok_embedding; /* fp16 [vocab][d_model] */
+  const uint16_t* lm_head;       /* fp16 [vocab][d_model] */
+  const float* final_norm;       /* fp32 [d_model]        */
+  const lmop_layer* layers;      /* host array [n_layers] (always host memory) */
+  int32_t n_layers;
+  int32_t on_device; /* 0: the tensor pointers are host memory; 1: device memory on the ctx's device */
+} lmop_weights;
+
+/* Copies the weights to the device and repacks them into the kernels'
+ * tiled layout (fusing q/k/v and gate/up).  May be called again to replace
+ * the weights; existing prefixes are then invalid and are released. */
+lmop_status lmop_load_weights(lmop_ctx* ctx, const lmop_weights* w);
+
+/* Computes and keeps the keys/values of a shared prompt prefix (the
+ * instruction part of the LLMMap prompt, Appendix "Prompts").  parent ==
+ * NULL makes a root; otherwise the prefix continues its parent's sequence
+ * (positions continue, attention sees the parent's tokens) - the two-level
+ * reuse of a join, root = instruction, child = instruction + left value.
+ * A child's parent must be a root.  tokens: host int32 [n_tokens], n_tokens
+ * >= 1, ids in [0, vocab).  The parent must stay alive while children or
+ * rows use it (release order is free; a released parent lives on until its
+ * last child is released). */
+lmop_status lmop_set_prefix(lmop_ctx* ctx, const lmop_prefix* parent, const int32_t* tokens,
+                            int32_t n_tokens, lmop_prefix** out);
+lmop_status lmop_release_prefix(lmop_ctx* ctx, lmop_prefix* prefix);
+/* Total sequence length of a prefix (ancestors included); -1 for NULL. */
+int32_t lmop_prefix_length(const lmop_prefix* prefix);
+
+/* Return types (Sec. 2.3 "Constrained Decoding"; `options`, Sec. 2.3.2 Example 4). */
+typedef enum {
+  LMOP_BOOL = 0, /* tokens = {false_token, true_token}; value 0/1                        */
+  LMOP_ENUM = 1, /* tokens[i] = single-token option i; value = option index              */
+  LMOP_INT = 2   /* tokens[d] = token of digit d (n_tokens = 10), eos_token ends the
+                    number; a digit string of at most max_tokens tokens (EOS included),
+                    no EOS at the first step; value = decimal value of the digits       */
+} lmop_kind;
+
+typedef struct {
+  int32_t kind;          /* lmop_kind */
+  const int32_t* tokens; /* host [n_tokens], distinct ids in [0, vocab) */
+  int32_t n_tokens;      /* BOOL: 2; ENUM: 1..4096; INT: 10 */
+  int32_t eos_token;     /* INT only: not one of the digit tokens */
+  int32_t max_tokens;    /* INT: 1..8; BOOL/ENUM: ignored (1) */
+} lmop_type;
+
+typedef struct {
+  int64_t value;      /* BOOL 0/1; ENUM option index; INT decimal value                     */
+  float logprob;      /* sum over steps of log-softmax over that step's allowed tokens       */
+  float logprob_full; /* sum over steps of log-softmax over the whole vocabulary            */
+  int32_t n_tokens;   /* tokens generated (INT: EOS included)                               */
+  int32_t tokens[8];  /* generated token ids; unused entries are -1                         */
+} lmop_result;
+
+#define LMOP_NO_DEDUP 1u /* evaluate duplicate rows separately (results are identical) */
+
+typedef struct {
+  uint32_t flags;           /* LMOP_NO_DEDUP                                              */
+  int32_t max_batch_tokens; /* suffix tokens per device batch; 0 = library default        */
+  float* debug_logits;      /* NULL or host fp32 [n_rows][max_steps][vocab]: the logits of
+                               each step (max_steps = max_tokens for INT, else 1); steps a
+                               row did not take are NaN                                   */
+} lmop_eval_opts;
+
+/* Evaluates the LM function on every row: row r's sequence is
+ * prefix(r) ++ tokens[offsets[r] .. offsets[r+1]), where prefix(r) =
+ * row_prefix[r] if row_prefix != NULL else `prefix` (either may be NULL =
+ * no prefix).  tokens/offsets: host CSR, offsets[0] = 0, non-decreasing,
+ * offsets[n_rows] = total.  A row with an empty suffix takes its answer from
+ * the prefix's last position; a row with neither is INVALID_ARG.  Writes
+ * out[r] (host) for every row.  n_rows = 0 is a no-op. */
+lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
+                           const lmop_prefix* const* row_prefix, const int32_t* tokens,
+                           const int64_t* offsets, int32_t n_rows, const lmop_type* type,
+                           lmop_result* out, const lmop_eval_opts* opts);
+
+/* Early deduplication (Sec. 2.4): rows with equal (key, suffix) get the
+ * same representative, the first such row.  keys: NULL or host [n_rows]
+ * (e.g. a prefix id per row).  rep[r] = index of r's representative;
+ * *n_unique = number of distinct rows.  Host only; needs no ctx. */
+lmop_status lmop_dedup_rows(const int32_t* tokens, const int64_t* offsets, int32_t n_rows,
+                            const int64_t* keys, int32_t* rep, int32_t* n_unique);
+
+/* Per-kernel timing of the ctx's launches, measured with HIP events on the
+ * ctx stream while profiling is on (off by default). */
+typedef struct {
+  char name[48];
+  int64_t launches;
+  double total_ms;
+  double flops; /* algorithmic FLOPs of those launches */
+  double bytes; /* algorithmic HBM bytes of those launches */
+} lmop_kernel_stat;
+
+lmop_status lmop_set_profiling(lmop_ctx* ctx, int32_t enable); /* also clears the counters */
+lmop_status lmop_get_kernel_stats(lmop_ctx* ctx, lmop_kernel_stat* out, int32_t max_entries,
+                                  int32_t* n_entries);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LMOP_H */

@@ -1,0 +1,249 @@
+// HBM-bound kernels of the row-evaluation path: embedding gather, RMSNorm
+// (fp32 residual -> fp16 GEMM operand), rotary embedding with the key/value
+// write into the KV store, the load-time int4 repack, and the per-row
+// finish of the constrained LM head.
+#include "common.h"
+#include "kernels.h"
+
+namespace lmop {
+
+namespace {
+
+// --------------------------------------------------------------- embedding
+// x[t][:] = fp32(E[tok[t]][:]); one workgroup per token, 8 halves per thread-iteration
+__global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ tok,
+                                                    const f16* __restrict__ emb, int d,
+                                                    float* __restrict__ x) {
+  const int t = blockIdx.x;
+  const f16* src = emb + (size_t)tok[t] * d;
+  float* dst = x + (size_t)t * d;
+  for (int j = threadIdx.x * 8; j < d; j += 256 * 8) {
+    const f16x8 v = *(const f16x8*)(src + j);
+    float4 lo = make_float4((float)v[0], (float)v[1], (float)v[2], (float)v[3]);
+    float4 hi = make_float4((float)v[4], (float)v[5], (float)v[6], (float)v[7]);
+    *(float4*)(dst + j) = lo;
+    *(float4*)(dst + j + 4) = hi;
+  }
+}
+
+// --------------------------------------------------------------- RMSNorm
+// out[i] = fp16(x_i / sqrt(mean(x_i^2) + eps) * gamma); one workgroup per row.
+// The sum of squares is reduced in a fixed order, so a row's result does not
+// depend on which other rows share the launch.
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x, int ldx,
+                                                      const float* const* __restrict__ rowptr,
+                                                      const float* __restrict__ gamma, int d,
+                                                      float eps, f16* __restrict__ out, int ldo) {
+  const int i = blockIdx.x;
+  const float* row = rowptr ? rowptr[i] : x + (size_t)i * ldx;
+  __shared__ float red[4];
+  float ss = 0.f;
+  for (int j = threadIdx.x * 4; j < d; j += 256 * 4) {
+    const float4 v = *(const float4*)(row + j);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) ss += shfl_xor(ss, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+  const float rstd = 1.0f / sqrtf(tot / (float)d + eps);
+  f16* o = out + (size_t)i * ldo;
+  for (int j = threadIdx.x * 4; j < d; j += 256 * 4) {
+    const float4 v = *(const float4*)(row + j);
+    const float4 gm = *(const float4*)(gamma + j);
+    f16x4 h = {(f16)(v.x * rstd * gm.x), (f16)(v.y * rstd * gm.y), (f16)(v.z * rstd * gm.z),
+               (f16)(v.w * rstd * gm.w)};
+    *(f16x4*)(o + j) = h;
+  }
+}
+
+// --------------------------------------------------------------- RoPE + KV write
+// qkv row layout: [q heads | k heads | v heads], each head hd wide.  Pair
+// (i, i + hd/2) of every q and k head turns by the angle of position pos[t]
+// (cos/sin table built on the host in double precision).  q goes to qout,
+// k and v to slot[t] of the KV store ([slot][nkv][hd]).
+__global__ __launch_bounds__(256) void rope_kv_kernel(const f16* __restrict__ qkv, int ldqkv,
+                                                      const int32_t* __restrict__ pos,
+                                                      const int32_t* __restrict__ slot,
+                                                      const float2* __restrict__ tab, int nq,
+                                                      int nkv, int hd, f16* __restrict__ qout,
+                                                      f16* __restrict__ kc, f16* __restrict__ vc) {
+  const int t = blockIdx.x;
+  const int half = hd / 2;
+  const f16* src = qkv + (size_t)t * ldqkv;
+  const float2* cs = tab + (size_t)pos[t] * half;
+  const size_t kvoff = (size_t)slot[t] * nkv * hd;
+  const int n_rot = (nq + nkv) * half;
+  for (int e = threadIdx.x; e < n_rot; e += 256) {
+    const int h = e / half, i = e - h * half;
+    const float x1 = (float)src[h * hd + i], x2 = (float)src[h * hd + i + half];
+    const float2 a = cs[i];
+    const f16 y1 = (f16)(x1 * a.x - x2 * a.y), y2 = (f16)(x1 * a.y + x2 * a.x);
+    if (h < nq) {
+      f16* dq = qout + (size_t)t * nq * hd + h * hd;
+      dq[i] = y1;
+      dq[i + half] = y2;
+    } else {
+      f16* dk = kc + kvoff + (h - nq) * hd;
+      dk[i] = y1;
+      dk[i + half] = y2;
+    }
+  }
+  const f16* vsrc = src + (nq + nkv) * hd;
+  for (int e = threadIdx.x; e < nkv * hd; e += 256) vc[kvoff + e] = vsrc[e];
+}
+
+// --------------------------------------------------------------- int4 repack
+// One thread per (64-column block, group, lane, word): gathers the 8 codes of
+// column nb*64 + 16f + c, features kg*32 + 8g .. +7, from its source row and
+// writes them biased by +8 in the nibble order the GEMM's dequant expects.
+__global__ void repack_kernel(RepackSrc src, const int32_t* __restrict__ colsrc, int np, int kg_n,
+                              uint32_t* __restrict__ qpack, f16* __restrict__ spack) {
+  const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t total = (size_t)(np / 64) * kg_n * 256;
+  if (item >= total) return;
+  const int f = item & 3;
+  const int lane = (item >> 2) & 63;
+  const size_t blk = item >> 8;  // nb * kg_n + kg
+  const int kg = (int)(blk % kg_n);
+  const int nb = (int)(blk / kg_n);
+  const int g = lane >> 4, c = lane & 15;
+  const int col = nb * 64 + 16 * f + c;
+  const int cs = colsrc[col];
+  uint32_t word = 0x88888888u;  // code 0 everywhere
+  f16 scale = (f16)0.0f;
+  if (cs >= 0) {
+    const int si = cs >> 24, r = cs & 0xFFFFFF;
+    const int kp = src.kp_src[si];
+    if (kg * 32 < kp) {
+      const uint8_t* qb = src.q[si] + (size_t)r * (kp / 2) + kg * 16 + g * 4;
+      uint32_t codes = 0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t nib = (qb[j >> 1] >> ((j & 1) * 4)) & 0xF;
+        const uint32_t u = nib ^ 8u;  // two's complement -> biased
+        const int p = (j & 1) ? 4 + (j >> 1) : (j >> 1);
+        codes |= u << (4 * p);
+      }
+      word = codes;
+      scale = ((const f16*)src.s[si])[(size_t)r * (kp / 32) + kg];
+    }
+  }
+  qpack[item] = word;
+  if (g == 0) spack[blk * 64 + c * 4 + f] = scale;
+}
+
+// --------------------------------------------------------------- head finish
+// One wave per row: LSE over the vocabulary from the per-slice partials, then
+// the first maximum among the allowed tokens and the allowed-set LSE.
+__global__ __launch_bounds__(64) void head_finalize_kernel(const float2* __restrict__ part,
+                                                           int n_chunks,
+                                                           const float* __restrict__ zsel,
+                                                           int n_sel, int n_allowed,
+                                                           const int32_t* __restrict__ allowed_tok,
+                                                           HeadPick* __restrict__ out) {
+  const int r = blockIdx.x, lane = threadIdx.x;
+  const float2* pr = part + (size_t)r * n_chunks;
+  float mx = -INFINITY;
+  for (int j = lane; j < n_chunks; j += 64) mx = fmaxf(mx, pr[j].x);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, shfl_xor(mx, o));
+  float sm = 0.f;
+  for (int j = lane; j < n_chunks; j += 64) {
+    const float2 v = pr[j];
+    if (v.x > -INFINITY) sm += v.y * expf(v.x - mx);
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) sm += shfl_xor(sm, o);
+  const float lse_full = mx + logf(sm);
+
+  const float* zr = zsel + (size_t)r * n_sel;
+  // argmax with the smallest index on ties
+  float best = -INFINITY;
+  int bi = n_allowed;  // sentinel; stays only if every logit is NaN
+  for (int j = lane; j < n_allowed; j += 64) {
+    const float z = zr[j];
+    if (z > best || (z == best && j < bi)) {
+      best = z;
+      bi = j;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const float ob = shfl_xor(best, o);
+    const int oi = shfl_xor(bi, o);
+    if (ob > best || (ob == best && oi < bi)) {
+      best = ob;
+      bi = oi;
+    }
+  }
+  if (bi >= n_allowed) bi = 0;  // keeps the index in bounds whatever the logits hold
+  float second = -INFINITY;
+  for (int j = lane; j < n_allowed; j += 64)
+    if (j != bi) second = fmaxf(second, zr[j]);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) second = fmaxf(second, shfl_xor(second, o));
+  float sa = 0.f;
+  for (int j = lane; j < n_allowed; j += 64) sa += expf(zr[j] - best);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) sa += shfl_xor(sa, o);
+  if (lane == 0) {
+    HeadPick hp;
+    hp.index = bi;
+    hp.token = allowed_tok[bi];
+    hp.logprob = -logf(sa);
+    hp.logprob_full = best - lse_full;
+    hp.margin = n_allowed > 1 ? best - second : INFINITY;
+    hp.pad[0] = hp.pad[1] = hp.pad[2] = 0.f;
+    out[r] = hp;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_embed(hipStream_t s, const int32_t* tok, int T, const half_bits* emb, int d,
+                        float* x) {
+  if (T == 0) return hipSuccess;
+  hipLaunchKernelGGL(embed_kernel, dim3(T), dim3(256), 0, s, tok, (const f16*)emb, d, x);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(hipStream_t s, const float* x, int ldx, const float* const* rowptr,
+                          int R, const float* gamma, int d, float eps, half_bits* out, int ldo) {
+  if (R == 0) return hipSuccess;
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3(R), dim3(256), 0, s, x, ldx, rowptr, gamma, d, eps,
+                     (f16*)out, ldo);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_kv(hipStream_t s, const half_bits* qkv, int ldqkv, int T,
+                          const int32_t* pos, const int32_t* slot, const float2* rope_tab,
+                          int nq, int nkv, int hd, half_bits* qout, half_bits* kcache,
+                          half_bits* vcache) {
+  if (T == 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_kv_kernel, dim3(T), dim3(256), 0, s, (const f16*)qkv, ldqkv, pos, slot,
+                     rope_tab, nq, nkv, hd, (f16*)qout, (f16*)kcache, (f16*)vcache);
+  return hipGetLastError();
+}
+
+hipError_t launch_repack_w4(hipStream_t s, const RepackSrc& src, const int32_t* colsrc,
+                            PackedW4& dst) {
+  const int kg_n = dst.kp / 32;
+  const size_t total = (size_t)(dst.np / 64) * kg_n * 256;
+  const int blocks = (int)((total + 255) / 256);
+  hipLaunchKernelGGL(repack_kernel, dim3(blocks), dim3(256), 0, s, src, colsrc, dst.np, kg_n,
+                     dst.qpack, (f16*)dst.spack);
+  return hipGetLastError();
+}
+
+hipError_t launch_head_finalize(hipStream_t s, const float2* part, int n_chunks,
+                                const float* zsel, int n_sel, int n_allowed,
+                                const int32_t* allowed_tok, int R, HeadPick* out) {
+  if (R == 0) return hipSuccess;
+  hipLaunchKernelGGL(head_finalize_kernel, dim3(R), dim3(64), 0, s, part, n_chunks, zsel, n_sel,
+                     n_allowed, allowed_tok, out);
+  return hipGetLastError();
+}
+
+}  // namespace lmop

@@ -1,0 +1,122 @@
+// Host-side launchers of the gfx950 kernels (internal to the library).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lmop {
+
+typedef uint16_t half_bits;  // fp16 storage as seen from host code
+
+// ---------------------------------------------------------------- W4A16 GEMM
+// Repacked int4 weight of one (possibly fused) linear map, N' x K':
+//   qpack: u32 [Np/64][KG][64 lanes][4]; lane 16g+c, word f holds the 8 codes
+//          of column nb*64 + 16f + c, features kg*32 + 8g .. +7, biased by +8,
+//          nibble p = feature 2p (p < 4) / 2(p-4)+1 (p >= 4)
+//   spack: fp16 [Np/64][KG][16 c][4 f]
+// Np is a multiple of 128, Kp (= 32*KG) a multiple of 64.
+struct PackedW4 {
+  uint32_t* qpack = nullptr;
+  half_bits* spack = nullptr;
+  int n = 0;   // logical output columns (fused)
+  int np = 0;  // padded columns
+  int kp = 0;  // padded input features (multiple of 64)
+  int k = 0;   // logical input features
+};
+
+enum Epilogue : int {
+  EPI_STORE_F16 = 0,  // C[m][n] = fp16(acc)
+  EPI_ADD_F32 = 1,    // X[m][n] += acc (residual stream)
+  EPI_SWIGLU = 2,     // fused [gate|up] blocks of 32: C[m][j] = fp16(silu(gate_j) * up_j)
+  EPI_HEAD = 3        // LM head: per-64-column (max, sum exp), allowed-token logits, debug dump
+};
+
+struct GemmArgs {
+  const void* A;  // fp16 [M][lda]; columns >= K are never read
+  int lda;
+  int M, N, K;    // N: columns of the (padded) weight walked by the grid; K multiple of 64
+  // int4 weight
+  const uint32_t* bq;
+  const half_bits* bs;
+  // fp16 weight (LM head): [N][ldb]
+  const half_bits* bh;
+  int ldb;
+  // epilogue outputs
+  void* C;        // fp16 [M][ldc]
+  int ldc;
+  int n_out;      // EPI_STORE_F16: valid columns; EPI_SWIGLU: output columns written
+  float* X;       // fp32 [M][ldx]
+  int ldx;
+  // head epilogue
+  float2* part;          // [M][ceil(N/64)] (max, sum exp(z - max))
+  const int32_t* sel;    // [N]: index of the column in the allowed list, or -1
+  float* zsel;           // [M][n_sel]
+  int n_sel;
+  float* dump;           // NULL or fp32 [M][ld_dump]
+  int ld_dump;
+};
+
+// Picks the tile shape for M and launches.  Returns hipSuccess or the launch error.
+hipError_t launch_gemm_w4(hipStream_t s, const GemmArgs& a, int epi);
+hipError_t launch_gemm_f16(hipStream_t s, const GemmArgs& a, int epi);  // head only
+
+// Repacks one source matrix's rows into columns of a packed weight.
+// colsrc[j] (device, [np]): (source index << 24) | source row, or -1 (zero column).
+struct RepackSrc {
+  const uint8_t* q[3];
+  const half_bits* s[3];
+  int kp_src[3];  // padded K of each source (multiple of 32)
+};
+hipError_t launch_repack_w4(hipStream_t s, const RepackSrc& src, const int32_t* colsrc,
+                            PackedW4& dst);
+
+// ---------------------------------------------------------------- elementwise
+hipError_t launch_embed(hipStream_t s, const int32_t* tok, int T, const half_bits* emb, int d,
+                        float* x);
+// out[i] = fp16(rows[i] / rms(rows[i]) * gamma); rows[i] = x + i*ldx, or rowptr[i] if given
+hipError_t launch_rmsnorm(hipStream_t s, const float* x, int ldx, const float* const* rowptr,
+                          int R, const float* gamma, int d, float eps, half_bits* out, int ldo);
+// q/k get rotate-half RoPE at pos[t]; q -> qout [T][nq*hd]; k, v -> kcache/vcache[slot[t]]
+hipError_t launch_rope_kv(hipStream_t s, const half_bits* qkv, int ldqkv, int T,
+                          const int32_t* pos, const int32_t* slot, const float2* rope_tab,
+                          int nq, int nkv, int hd, half_bits* qout, half_bits* kcache,
+                          half_bits* vcache);
+
+// ---------------------------------------------------------------- attention
+struct AttnRow {
+  const half_bits* seg_kv[2];  // prefix-chain KV storage [L][2][n][nkv][hd], or NULL
+  int seg_n[2];                // tokens of each segment (0 if absent)
+  int q_start;                 // first query token of the row in the batch buffers
+  int n_q;                     // query tokens of the row in this launch
+  int own_slot;                // slot of own token 0 in the own-KV buffer
+  int own_q0;                  // own index of the first query token
+};
+struct AttnArgs {
+  const half_bits* q;  // [T][ldq], post-RoPE
+  int ldq;
+  half_bits* out;      // [T][ldo]
+  int ldo;
+  const AttnRow* rows;
+  const int2* work;    // (row, 64-query tile)
+  int n_work;
+  const half_bits* own_kv;  // [L][2][own_cap][nkv][hd]
+  int own_cap;
+  int layer;
+  int nq, nkv, hd;
+};
+hipError_t launch_attention(hipStream_t s, const AttnArgs& a);
+
+// ---------------------------------------------------------------- head finalize
+struct HeadPick {
+  int32_t index;   // position in the allowed list
+  int32_t token;
+  float logprob;   // over the allowed set
+  float logprob_full;
+  float margin;    // top-two allowed gap
+  float pad[3];
+};
+// per row: combine partials -> LSE over V; pick among zsel[:n_allowed]
+hipError_t launch_head_finalize(hipStream_t s, const float2* part, int n_chunks,
+                                const float* zsel, int n_sel, int n_allowed,
+                                const int32_t* allowed_tok, int R, HeadPick* out);
+
+}  // namespace lmop

@@ -1,0 +1,1206 @@
+// Host runtime behind include/lmop.h: argument checks, early deduplication,
+// token-budget row batching, the prefix tree with its KV storage, the layer
+// loop that drives the gfx950 kernels, the constrained decode loop and
+// per-kernel timing.
+#include "lmop.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <set>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "kernels.h"
+
+using namespace lmop;
+
+namespace {
+
+constexpr int kDefaultBatchTokens = 16384;
+constexpr int kMaxBatchRows = 2048;
+
+int round_up(int x, int m) { return (x + m - 1) / m * m; }
+
+struct LayerW {
+  float* attn_norm = nullptr;
+  float* mlp_norm = nullptr;
+  PackedW4 qkv, o, gu, down;
+};
+
+struct Stat {
+  int64_t launches = 0;
+  double ms = 0, flops = 0, bytes = 0;
+};
+
+struct Span {
+  std::string name;
+  hipEvent_t a, b;
+  double flops, bytes;
+};
+
+struct BatchRow {
+  const lmop_prefix* pfx;
+  const int32_t* toks;
+  int len;
+};
+
+}  // namespace
+
+struct lmop_prefix {
+  lmop_ctx* ctx = nullptr;
+  lmop_prefix* parent = nullptr;
+  int n = 0;       // own tokens
+  int start = 0;   // tokens of the parent chain
+  uint16_t* kv = nullptr;     // device [L][2][n][nkv][hd]
+  float* hidden = nullptr;    // device [d]: last token's final-layer hidden state
+  int children = 0;
+  bool released = false;
+  uint64_t generation = 0;
+  int64_t id = 0;
+};
+
+struct lmop_ctx {
+  lmop_config cfg{};
+  int device = -1;
+  bool host_only = false;
+  hipStream_t stream = nullptr;
+  bool own_stream = false;
+  std::string err;
+  bool dead = false;
+  bool loaded = false;
+  uint64_t generation = 0;
+  int64_t next_prefix_id = 1;
+
+  // dims
+  int nq_dim = 0, nkv_dim = 0, qkv_n = 0, f64 = 0;
+
+  // weights (device)
+  uint16_t* emb = nullptr;
+  uint16_t* head = nullptr;
+  float* final_norm = nullptr;
+  std::vector<LayerW> layers;
+  std::vector<void*> weight_allocs;
+  float2* rope_tab = nullptr;
+
+  // workspace (grow-only)
+  std::map<std::string, std::pair<void*, size_t>> ws;
+
+  std::set<lmop_prefix*> prefixes;
+
+  // profiling
+  bool prof = false;
+  std::vector<hipEvent_t> ev_free;
+  std::vector<Span> spans;
+  std::map<std::string, Stat> stats;
+};
+
+namespace {
+
+lmop_status fail(lmop_ctx* c, lmop_status st, const char* fmt, ...) {
+  if (c) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    c->err = buf;
+    if (st == LMOP_ERR_DEVICE) c->dead = true;
+  }
+  return st;
+}
+
+#define HIP_OK(ctx, call)                                                                   \
+  do {                                                                                      \
+    hipError_t e_ = (call);                                                                 \
+    if (e_ != hipSuccess)                                                                   \
+      return fail(ctx, e_ == hipErrorOutOfMemory ? LMOP_ERR_OOM : LMOP_ERR_DEVICE,          \
+                  "%s failed: %s (%s:%d)", #call, hipGetErrorString(e_), __FILE__, __LINE__); \
+  } while (0)
+
+#define LMOP_TRY(expr)                \
+  do {                                \
+    lmop_status s_ = (expr);          \
+    if (s_ != LMOP_OK) return s_;     \
+  } while (0)
+
+lmop_status dev_alloc(lmop_ctx* c, void** p, size_t bytes) {
+  *p = nullptr;
+  if (bytes == 0) bytes = 256;
+  hipError_t e = hipMalloc(p, bytes);
+  if (e != hipSuccess) {
+    *p = nullptr;
+    (void)hipGetLastError();
+    return fail(c, LMOP_ERR_OOM, "hipMalloc(%zu bytes) failed: %s", bytes, hipGetErrorString(e));
+  }
+  return LMOP_OK;
+}
+
+// named grow-only scratch buffer
+template <typename T>
+lmop_status ws_get(lmop_ctx* c, const char* name, size_t count, T** out) {
+  size_t bytes = std::max<size_t>(count * sizeof(T), 256);
+  auto& slot = c->ws[name];
+  if (slot.second < bytes) {
+    if (slot.first) HIP_OK(c, hipFree(slot.first));
+    slot = {nullptr, 0};
+    size_t want = bytes + bytes / 4;
+    void* p = nullptr;
+    LMOP_TRY(dev_alloc(c, &p, want));
+    slot = {p, want};
+  }
+  *out = (T*)slot.first;
+  return LMOP_OK;
+}
+
+// ---------------------------------------------------------------- profiling
+hipEvent_t take_event(lmop_ctx* c) {
+  if (!c->ev_free.empty()) {
+    hipEvent_t e = c->ev_free.back();
+    c->ev_free.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <typename F>
+lmop_status timed(lmop_ctx* c, const char* name, double flops, double bytes, F&& launch) {
+  hipEvent_t a = nullptr, b = nullptr;
+  if (c->prof) {
+    a = take_event(c);
+    b = take_event(c);
+    if (a && b) HIP_OK(c, hipEventRecord(a, c->stream));
+  }
+  hipError_t e = launch();
+  if (e != hipSuccess) return fail(c, LMOP_ERR_DEVICE, "launch of %s failed: %s", name,
+                                   hipGetErrorString(e));
+  if (c->prof && a && b) {
+    HIP_OK(c, hipEventRecord(b, c->stream));
+    c->spans.push_back(Span{name, a, b, flops, bytes});
+  }
+  return LMOP_OK;
+}
+
+lmop_status resolve_spans(lmop_ctx* c) {
+  for (auto& s : c->spans) {
+    HIP_OK(c, hipEventSynchronize(s.b));
+    float ms = 0.f;
+    HIP_OK(c, hipEventElapsedTime(&ms, s.a, s.b));
+    Stat& st = c->stats[s.name];
+    st.launches += 1;
+    st.ms += ms;
+    st.flops += s.flops;
+    st.bytes += s.bytes;
+    c->ev_free.push_back(s.a);
+    c->ev_free.push_back(s.b);
+  }
+  c->spans.clear();
+  return LMOP_OK;
+}
+
+lmop_status sync(lmop_ctx* c) {
+  HIP_OK(c, hipStreamSynchronize(c->stream));
+  return resolve_spans(c);
+}
+
+// ---------------------------------------------------------------- validation
+lmop_status check_config(const lmop_config* cfg, lmop_ctx* c) {
+  if (!cfg) return fail(c, LMOP_ERR_INVALID_ARG, "config is NULL");
+  if (cfg->n_layers < 0 || cfg->d_model <= 0 || cfg->n_heads <= 0 || cfg->n_kv_heads <= 0 ||
+      cfg->head_dim <= 0 || cfg->d_ff <= 0 || cfg->vocab <= 1 || !(cfg->rms_eps >= 0.f) ||
+      !(cfg->rope_theta > 0.f) || cfg->max_seq < 0)
+    return fail(c, LMOP_ERR_INVALID_ARG, "config has a non-positive dimension or parameter");
+  if (cfg->head_dim != 64 && cfg->head_dim != 128)
+    return fail(c, LMOP_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", cfg->head_dim);
+  if (cfg->n_heads % cfg->n_kv_heads != 0)
+    return fail(c, LMOP_ERR_UNSUPPORTED, "n_heads %% n_kv_heads != 0");
+  if (cfg->d_model % 64 != 0)
+    return fail(c, LMOP_ERR_UNSUPPORTED, "d_model %d is not a multiple of 64", cfg->d_model);
+  if (cfg->group_size != 32)
+    return fail(c, LMOP_ERR_UNSUPPORTED, "group_size %d (supported: 32)", cfg->group_size);
+  if (cfg->vocab >= (1 << 24)) return fail(c, LMOP_ERR_UNSUPPORTED, "vocab too large");
+  return LMOP_OK;
+}
+
+lmop_status check_qmat(lmop_ctx* c, const char* what, int layer, const lmop_qmat& m, int n,
+                       int k) {
+  if (!m.qweight || !m.scales)
+    return fail(c, LMOP_ERR_INVALID_ARG, "layer %d %s: NULL qweight/scales", layer, what);
+  if (m.n != n || m.k != k)
+    return fail(c, LMOP_ERR_INVALID_ARG, "layer %d %s: shape [%d][%d], expected [%d][%d]", layer,
+                what, m.n, m.k, n, k);
+  return LMOP_OK;
+}
+
+bool prefix_live(const lmop_ctx* c, const lmop_prefix* p) {
+  return p && c->prefixes.count(const_cast<lmop_prefix*>(p)) && !p->released &&
+         p->generation == c->generation;
+}
+
+int prefix_total(const lmop_prefix* p) { return p ? p->start + p->n : 0; }
+
+lmop_status check_tokens(lmop_ctx* c, const int32_t* t, int64_t n, const char* what) {
+  const int V = c->cfg.vocab;
+  for (int64_t i = 0; i < n; ++i)
+    if (t[i] < 0 || t[i] >= V)
+      return fail(c, LMOP_ERR_INVALID_ARG, "%s token %lld = %d outside [0, %d)", what,
+                  (long long)i, t[i], V);
+  return LMOP_OK;
+}
+
+lmop_status check_type(lmop_ctx* c, const lmop_type* ty) {
+  if (!ty) return fail(c, LMOP_ERR_INVALID_ARG, "type is NULL");
+  if (ty->kind < LMOP_BOOL || ty->kind > LMOP_INT)
+    return fail(c, LMOP_ERR_INVALID_ARG, "unknown type kind %d", ty->kind);
+  if (!ty->tokens) return fail(c, LMOP_ERR_INVALID_ARG, "type tokens is NULL");
+  const int n = ty->n_tokens;
+  if (ty->kind == LMOP_BOOL && n != 2)
+    return fail(c, LMOP_ERR_INVALID_ARG, "BOOL needs 2 tokens, got %d", n);
+  if (ty->kind == LMOP_ENUM && (n < 1 || n > 4096))
+    return fail(c, LMOP_ERR_INVALID_ARG, "ENUM needs 1..4096 tokens, got %d", n);
+  if (ty->kind == LMOP_INT) {
+    if (n != 10) return fail(c, LMOP_ERR_INVALID_ARG, "INT needs 10 digit tokens, got %d", n);
+    if (ty->max_tokens < 1 || ty->max_tokens > 8)
+      return fail(c, LMOP_ERR_INVALID_ARG, "INT max_tokens %d outside 1..8", ty->max_tokens);
+    if (ty->eos_token < 0 || ty->eos_token >= c->cfg.vocab)
+      return fail(c, LMOP_ERR_INVALID_ARG, "INT eos_token %d outside the vocabulary",
+                  ty->eos_token);
+  }
+  LMOP_TRY(check_tokens(c, ty->tokens, n, "type"));
+  std::set<int32_t> seen(ty->tokens, ty->tokens + n);
+  if ((int)seen.size() != n) return fail(c, LMOP_ERR_INVALID_ARG, "type tokens are not distinct");
+  if (ty->kind == LMOP_INT && seen.count(ty->eos_token))
+    return fail(c, LMOP_ERR_INVALID_ARG, "INT eos_token is one of the digit tokens");
+  return LMOP_OK;
+}
+
+// ---------------------------------------------------------------- dedup
+uint64_t mix(uint64_t h, uint64_t v) {
+  h ^= v + 0x9e3779b97f4a7c15ull + (h << 6) + (h >> 2);
+  return h * 0xff51afd7ed558ccdull;
+}
+
+void dedup(const int32_t* tokens, const int64_t* offsets, int n_rows, const int64_t* keys,
+           int32_t* rep, int32_t* n_unique) {
+  std::unordered_map<uint64_t, std::vector<int32_t>> buckets;
+  buckets.reserve((size_t)n_rows * 2);
+  int u = 0;
+  for (int r = 0; r < n_rows; ++r) {
+    const int64_t b = offsets[r], e = offsets[r + 1];
+    uint64_t h = mix(0x1234567ull, (uint64_t)(keys ? keys[r] : 0));
+    h = mix(h, (uint64_t)(e - b));
+    for (int64_t i = b; i < e; ++i) h = mix(h, (uint32_t)tokens[i]);
+    auto& cand = buckets[h];
+    int found = -1;
+    for (int32_t q : cand) {
+      const int64_t qb = offsets[q], qe = offsets[q + 1];
+      if ((keys ? keys[q] : 0) != (keys ? keys[r] : 0)) continue;
+      if (qe - qb != e - b) continue;
+      if (std::equal(tokens + b, tokens + e, tokens + qb)) {
+        found = q;
+        break;
+      }
+    }
+    if (found < 0) {
+      cand.push_back(r);
+      rep[r] = r;
+      ++u;
+    } else {
+      rep[r] = found;
+    }
+  }
+  *n_unique = u;
+}
+
+// ---------------------------------------------------------------- weights
+lmop_status upload(lmop_ctx* c, const void* src, size_t bytes, bool on_device, void** dst) {
+  LMOP_TRY(dev_alloc(c, dst, bytes));
+  c->weight_allocs.push_back(*dst);
+  HIP_OK(c, hipMemcpyAsync(*dst, src, bytes,
+                           on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice,
+                           c->stream));
+  return LMOP_OK;
+}
+
+void free_weights(lmop_ctx* c) {
+  for (void* p : c->weight_allocs) (void)hipFree(p);
+  c->weight_allocs.clear();
+  c->layers.clear();
+  c->emb = c->head = nullptr;
+  c->final_norm = nullptr;
+}
+
+// Packs up to three source matrices (rows = output columns) into one tiled
+// int4 weight.  colmap[j] = (source << 24) | row, or -1 for a zero column.
+lmop_status pack(lmop_ctx* c, const lmop_qmat* const* srcs, int n_src, const std::vector<int32_t>& colmap,
+                 int n_logical, int k, bool on_device, PackedW4* out) {
+  PackedW4 w;
+  w.n = n_logical;
+  w.np = (int)colmap.size();
+  w.k = k;
+  w.kp = round_up(k, 64);
+  const int kg = w.kp / 32;
+  void* qp = nullptr;
+  void* sp = nullptr;
+  LMOP_TRY(dev_alloc(c, &qp, (size_t)(w.np / 64) * kg * 1024));
+  c->weight_allocs.push_back(qp);
+  LMOP_TRY(dev_alloc(c, &sp, (size_t)(w.np / 64) * kg * 128));
+  c->weight_allocs.push_back(sp);
+  w.qpack = (uint32_t*)qp;
+  w.spack = (half_bits*)sp;
+
+  RepackSrc rs{};
+  std::vector<void*> staging;
+  for (int i = 0; i < n_src; ++i) {
+    const lmop_qmat& m = *srcs[i];
+    const int kps = round_up(m.k, 32);
+    rs.kp_src[i] = kps;
+    if (on_device) {
+      rs.q[i] = m.qweight;
+      rs.s[i] = m.scales;
+    } else {
+      void* dq = nullptr;
+      void* ds = nullptr;
+      LMOP_TRY(dev_alloc(c, &dq, (size_t)m.n * kps / 2));
+      staging.push_back(dq);
+      LMOP_TRY(dev_alloc(c, &ds, (size_t)m.n * (kps / 32) * 2));
+      staging.push_back(ds);
+      HIP_OK(c, hipMemcpyAsync(dq, m.qweight, (size_t)m.n * kps / 2, hipMemcpyHostToDevice,
+                               c->stream));
+      HIP_OK(c, hipMemcpyAsync(ds, m.scales, (size_t)m.n * (kps / 32) * 2,
+                               hipMemcpyHostToDevice, c->stream));
+      rs.q[i] = (const uint8_t*)dq;
+      rs.s[i] = (const half_bits*)ds;
+    }
+  }
+  void* dmap = nullptr;
+  LMOP_TRY(dev_alloc(c, &dmap, colmap.size() * 4));
+  staging.push_back(dmap);
+  HIP_OK(c, hipMemcpyAsync(dmap, colmap.data(), colmap.size() * 4, hipMemcpyHostToDevice,
+                           c->stream));
+  LMOP_TRY(timed(c, "repack_w4", 0, 0, [&] { return launch_repack_w4(c->stream, rs, (const int32_t*)dmap, w); }));
+  HIP_OK(c, hipStreamSynchronize(c->stream));
+  for (void* p : staging) HIP_OK(c, hipFree(p));
+  *out = w;
+  return LMOP_OK;
+}
+
+std::vector<int32_t> concat_map(const int* rows, int n_parts, int np) {
+  std::vector<int32_t> m(np, -1);
+  int j = 0;
+  for (int s = 0; s < n_parts; ++s)
+    for (int r = 0; r < rows[s]; ++r) m[j++] = (s << 24) | r;
+  return m;
+}
+
+// ---------------------------------------------------------------- forward
+struct Batch {
+  int T = 0;        // query tokens of this launch
+  int R = 0;        // rows
+  int n_work = 0;   // attention work items
+  uint16_t* own_kv = nullptr;
+  int own_cap = 0;
+};
+
+// One pass of all layers over the T tokens whose ids/positions/slots and row
+// descriptors are already on the device (ws "tok", "pos", "slot", "rows", "work").
+lmop_status forward(lmop_ctx* c, const Batch& b) {
+  const lmop_config& cf = c->cfg;
+  const int T = b.T, d = cf.d_model, hd = cf.head_dim;
+  if (T == 0) return LMOP_OK;
+  int32_t *tok, *pos, *slot;
+  AttnRow* rows;
+  int2* work;
+  float* x;
+  uint16_t *h, *qkv, *q, *att, *act;
+  LMOP_TRY(ws_get(c, "tok", T, &tok));
+  LMOP_TRY(ws_get(c, "pos", T, &pos));
+  LMOP_TRY(ws_get(c, "slot", T, &slot));
+  LMOP_TRY(ws_get(c, "rows", b.R, &rows));
+  LMOP_TRY(ws_get(c, "work", b.n_work, &work));
+  LMOP_TRY(ws_get(c, "x", (size_t)T * d, &x));
+  LMOP_TRY(ws_get(c, "h", (size_t)T * d, &h));
+  LMOP_TRY(ws_get(c, "qkv", (size_t)T * c->qkv_n, &qkv));
+  LMOP_TRY(ws_get(c, "q", (size_t)T * c->nq_dim, &q));
+  LMOP_TRY(ws_get(c, "att", (size_t)T * c->nq_dim, &att));
+  LMOP_TRY(ws_get(c, "act", (size_t)T * c->f64, &act));
+
+  LMOP_TRY(timed(c, "embed", 0, (double)T * d * 6, [&] {
+    return launch_embed(c->stream, tok, T, c->emb, d, x);
+  }));
+  const size_t kv_layer = (size_t)2 * b.own_cap * c->nkv_dim;
+  for (int l = 0; l < cf.n_layers; ++l) {
+    const LayerW& L = c->layers[l];
+    const double nbytes_norm = (double)T * d * 6;
+    LMOP_TRY(timed(c, "rmsnorm", 0, nbytes_norm, [&] {
+      return launch_rmsnorm(c->stream, x, d, nullptr, T, L.attn_norm, d, cf.rms_eps, h, d);
+    }));
+    auto gemm = [&](const char* name, const void* A, int lda, const PackedW4& W, int epi,
+                    void* C, int ldc, int n_out) {
+      GemmArgs ga{};
+      ga.A = A;
+      ga.lda = lda;
+      ga.M = T;
+      ga.N = W.np;
+      ga.K = W.kp;
+      ga.bq = W.qpack;
+      ga.bs = W.spack;
+      ga.C = C;
+      ga.ldc = ldc;
+      ga.n_out = n_out;
+      ga.X = x;
+      ga.ldx = d;
+      const double flops = 2.0 * T * W.n * W.k;
+      const double bytes = (double)T * W.k * 2 + (double)W.n * W.k * 0.5625 +
+                           (double)T * W.n * (epi == EPI_ADD_F32 ? 8 : 2);
+      return timed(c, name, flops, bytes, [&] { return launch_gemm_w4(c->stream, ga, epi); });
+    };
+    LMOP_TRY(gemm("gemm_w4a16_qkv", h, d, L.qkv, EPI_STORE_F16, qkv, c->qkv_n, c->qkv_n));
+    uint16_t* kc = b.own_kv + l * kv_layer;
+    uint16_t* vc = kc + (size_t)b.own_cap * c->nkv_dim;
+    LMOP_TRY(timed(c, "rope_kv", 0, (double)T * c->qkv_n * 4, [&] {
+      return launch_rope_kv(c->stream, qkv, c->qkv_n, T, pos, slot, c->rope_tab, cf.n_heads,
+                            cf.n_kv_heads, hd, q, kc, vc);
+    }));
+    AttnArgs aa{};
+    aa.q = q;
+    aa.ldq = c->nq_dim;
+    aa.out = att;
+    aa.ldo = c->nq_dim;
+    aa.rows = rows;
+    aa.work = work;
+    aa.n_work = b.n_work;
+    aa.own_kv = b.own_kv;
+    aa.own_cap = b.own_cap;
+    aa.layer = l;
+    aa.nq = cf.n_heads;
+    aa.nkv = cf.n_kv_heads;
+    aa.hd = hd;
+    LMOP_TRY(timed(c, "attention", 0, 0, [&] { return launch_attention(c->stream, aa); }));
+    LMOP_TRY(gemm("gemm_w4a16_o", att, c->nq_dim, L.o, EPI_ADD_F32, nullptr, 0, d));
+    LMOP_TRY(timed(c, "rmsnorm", 0, nbytes_norm, [&] {
+      return launch_rmsnorm(c->stream, x, d, nullptr, T, L.mlp_norm, d, cf.rms_eps, h, d);
+    }));
+    LMOP_TRY(gemm("gemm_w4a16_gateup", h, d, L.gu, EPI_SWIGLU, act, c->f64, c->f64));
+    LMOP_TRY(gemm("gemm_w4a16_down", act, c->f64, L.down, EPI_ADD_F32, nullptr, 0, d));
+  }
+  return LMOP_OK;
+}
+
+// Uploads host-built per-token and per-row arrays for one forward pass.
+lmop_status upload_batch(lmop_ctx* c, const std::vector<int32_t>& tok,
+                         const std::vector<int32_t>& pos, const std::vector<int32_t>& slot,
+                         const std::vector<AttnRow>& rows, const std::vector<int2>& work) {
+  int32_t *dt, *dp, *ds;
+  AttnRow* dr;
+  int2* dw;
+  LMOP_TRY(ws_get(c, "tok", tok.size(), &dt));
+  LMOP_TRY(ws_get(c, "pos", pos.size(), &dp));
+  LMOP_TRY(ws_get(c, "slot", slot.size(), &ds));
+  LMOP_TRY(ws_get(c, "rows", rows.size(), &dr));
+  LMOP_TRY(ws_get(c, "work", work.size(), &dw));
+  if (!tok.empty()) {
+    HIP_OK(c, hipMemcpyAsync(dt, tok.data(), tok.size() * 4, hipMemcpyHostToDevice, c->stream));
+    HIP_OK(c, hipMemcpyAsync(dp, pos.data(), pos.size() * 4, hipMemcpyHostToDevice, c->stream));
+    HIP_OK(c, hipMemcpyAsync(ds, slot.data(), slot.size() * 4, hipMemcpyHostToDevice, c->stream));
+  }
+  if (!rows.empty())
+    HIP_OK(c, hipMemcpyAsync(dr, rows.data(), rows.size() * sizeof(AttnRow),
+                             hipMemcpyHostToDevice, c->stream));
+  if (!work.empty())
+    HIP_OK(c, hipMemcpyAsync(dw, work.data(), work.size() * sizeof(int2), hipMemcpyHostToDevice,
+                             c->stream));
+  // the host vectors die with the caller's scope: finish the copies now
+  HIP_OK(c, hipStreamSynchronize(c->stream));
+  return LMOP_OK;
+}
+
+void fill_segments(const lmop_prefix* p, AttnRow& r) {
+  r.seg_kv[0] = r.seg_kv[1] = nullptr;
+  r.seg_n[0] = r.seg_n[1] = 0;
+  if (!p) return;
+  if (p->parent) {
+    r.seg_kv[0] = p->parent->kv;
+    r.seg_n[0] = p->parent->n;
+    r.seg_kv[1] = p->kv;
+    r.seg_n[1] = p->n;
+  } else {
+    r.seg_kv[0] = p->kv;
+    r.seg_n[0] = p->n;
+  }
+}
+
+void add_work(std::vector<int2>& work, int row, int n_q, int G) {
+  const int tiles = (n_q * G + 63) / 64;
+  for (int t = 0; t < tiles; ++t) work.push_back(make_int2(row, t));
+}
+
+// Runs the constrained head over R rows whose final hidden states are at
+// d_rowptr[i]; picks -> host.  dump_host (optional) receives [R][V] logits.
+lmop_status run_head(lmop_ctx* c, int R, const std::vector<const float*>& rowptr,
+                     const int32_t* d_sel, const int32_t* d_allowed, int n_sel, int n_allowed,
+                     std::vector<HeadPick>& picks, float* dump_dev) {
+  const lmop_config& cf = c->cfg;
+  const int d = cf.d_model, V = cf.vocab;
+  const int n_chunks = (V + 63) / 64;
+  const float** drp;
+  uint16_t* hn;
+  float2* part;
+  float* zsel;
+  HeadPick* dpk;
+  LMOP_TRY(ws_get(c, "head_rowptr", R, &drp));
+  LMOP_TRY(ws_get(c, "head_hn", (size_t)R * d, &hn));
+  LMOP_TRY(ws_get(c, "head_part", (size_t)R * n_chunks, &part));
+  LMOP_TRY(ws_get(c, "head_zsel", (size_t)R * n_sel, &zsel));
+  LMOP_TRY(ws_get(c, "head_pick", R, &dpk));
+  HIP_OK(c, hipMemcpyAsync(drp, rowptr.data(), R * sizeof(float*), hipMemcpyHostToDevice,
+                           c->stream));
+  HIP_OK(c, hipStreamSynchronize(c->stream));
+  LMOP_TRY(timed(c, "rmsnorm_final", 0, (double)R * d * 6, [&] {
+    return launch_rmsnorm(c->stream, nullptr, 0, drp, R, c->final_norm, d, cf.rms_eps, hn, d);
+  }));
+  GemmArgs ga{};
+  ga.A = hn;
+  ga.lda = d;
+  ga.M = R;
+  ga.N = V;
+  ga.K = d;
+  ga.bh = c->head;
+  ga.ldb = d;
+  ga.part = part;
+  ga.sel = d_sel;
+  ga.zsel = zsel;
+  ga.n_sel = n_sel;
+  ga.dump = dump_dev;
+  ga.ld_dump = V;
+  LMOP_TRY(timed(c, "head_gemm", 2.0 * R * V * d, (double)V * d * 2 + (double)R * d * 2, [&] {
+    return launch_gemm_f16(c->stream, ga, EPI_HEAD);
+  }));
+  LMOP_TRY(timed(c, "head_finalize", 0, 0, [&] {
+    return launch_head_finalize(c->stream, part, n_chunks, zsel, n_sel, n_allowed, d_allowed, R,
+                                dpk);
+  }));
+  picks.resize(R);
+  HIP_OK(c, hipMemcpyAsync(picks.data(), dpk, R * sizeof(HeadPick), hipMemcpyDeviceToHost,
+                           c->stream));
+  return LMOP_OK;
+}
+
+}  // namespace
+
+// ====================================================================== ABI
+extern "C" {
+
+const char* lmop_status_string(lmop_status s) {
+  switch (s) {
+    case LMOP_OK: return "ok";
+    case LMOP_ERR_INVALID_ARG: return "invalid argument";
+    case LMOP_ERR_STATE: return "call out of order";
+    case LMOP_ERR_OOM: return "out of memory";
+    case LMOP_ERR_DEVICE: return "device error";
+    case LMOP_ERR_UNSUPPORTED: return "unsupported";
+  }
+  return "unknown status";
+}
+
+
+static thread_local std::string g_create_error;
+
+lmop_status lmop_create(const lmop_config* cfg, int32_t device, void* hip_stream, lmop_ctx** out) {
+  g_create_error.clear();
+  if (!out) return LMOP_ERR_INVALID_ARG;
+  *out = nullptr;
+  std::unique_ptr<lmop_ctx> c(new lmop_ctx());
+  lmop_ctx* cp = c.get();
+  auto bail = [&](lmop_status st) {
+    g_create_error = cp->err;
+    if (!cp->host_only) {
+      if (cp->rope_tab) (void)hipFree(cp->rope_tab);
+      if (cp->own_stream && cp->stream) (void)hipStreamDestroy(cp->stream);
+    }
+    return st;
+  };
+  lmop_status st = check_config(cfg, cp);
+  if (st != LMOP_OK) return bail(st);
+  c->cfg = *cfg;
+  if (c->cfg.max_seq == 0) c->cfg.max_seq = 4096;
+  const lmop_config& cf = c->cfg;
+  c->nq_dim = cf.n_heads * cf.head_dim;
+  c->nkv_dim = cf.n_kv_heads * cf.head_dim;
+  c->qkv_n = c->nq_dim + 2 * c->nkv_dim;
+  c->f64 = round_up(cf.d_ff, 64);
+  c->device = device;
+  if (device < 0) {
+    c->host_only = true;
+    *out = c.release();
+    return LMOP_OK;
+  }
+  int n_dev = 0;
+  if (hipGetDeviceCount(&n_dev) != hipSuccess || device >= n_dev) {
+    (void)hipGetLastError();
+    c->host_only = true;  // nothing to free on a device
+    return bail(fail(cp, LMOP_ERR_DEVICE, "HIP device %d not available (%d devices)", device,
+                     n_dev));
+  }
+  if (hipSetDevice(device) != hipSuccess)
+    return bail(fail(cp, LMOP_ERR_DEVICE, "hipSetDevice(%d) failed", device));
+  if (hip_stream) {
+    c->stream = (hipStream_t)hip_stream;
+  } else {
+    if (hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking) != hipSuccess)
+      return bail(fail(cp, LMOP_ERR_DEVICE, "hipStreamCreate failed"));
+    c->own_stream = true;
+  }
+  // rotary table: cos/sin of pos * theta^(-2i/hd) in double, stored fp32
+  const int half = cf.head_dim / 2;
+  std::vector<float2> tab((size_t)cf.max_seq * half);
+  for (int p = 0; p < cf.max_seq; ++p)
+    for (int i = 0; i < half; ++i) {
+      const double ang = (double)p * std::pow((double)cf.rope_theta, -2.0 * i / cf.head_dim);
+      tab[(size_t)p * half + i] = make_float2((float)std::cos(ang), (float)std::sin(ang));
+    }
+  void* rt = nullptr;
+  st = dev_alloc(cp, &rt, tab.size() * sizeof(float2));
+  if (st != LMOP_OK) return bail(st);
+  c->rope_tab = (float2*)rt;
+  if (hipMemcpy(rt, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice) != hipSuccess)
+    return bail(fail(cp, LMOP_ERR_DEVICE, "upload of the rotary table failed"));
+  *out = c.release();
+  return LMOP_OK;
+}
+
+const char* lmop_last_error(const lmop_ctx* ctx) {
+  return ctx ? ctx->err.c_str() : g_create_error.c_str();
+}
+
+static void destroy_prefix_storage(lmop_prefix* p) {
+  if (p->kv) (void)hipFree(p->kv);
+  if (p->hidden) (void)hipFree(p->hidden);
+  p->kv = nullptr;
+  p->hidden = nullptr;
+}
+
+void lmop_destroy(lmop_ctx* ctx) {
+  if (!ctx) return;
+  if (!ctx->host_only) {
+    (void)hipSetDevice(ctx->device);
+    if (ctx->stream) (void)hipStreamSynchronize(ctx->stream);
+  }
+  for (lmop_prefix* p : ctx->prefixes) {
+    destroy_prefix_storage(p);
+    delete p;
+  }
+  ctx->prefixes.clear();
+  if (!ctx->host_only) {
+    free_weights(ctx);
+    for (auto& kv : ctx->ws)
+      if (kv.second.first) (void)hipFree(kv.second.first);
+    if (ctx->rope_tab) (void)hipFree(ctx->rope_tab);
+    for (auto& s : ctx->spans) {
+      (void)hipEventDestroy(s.a);
+      (void)hipEventDestroy(s.b);
+    }
+    for (hipEvent_t e : ctx->ev_free) (void)hipEventDestroy(e);
+    if (ctx->own_stream && ctx->stream) (void)hipStreamDestroy(ctx->stream);
+  }
+  delete ctx;
+}
+
+static lmop_status enter(lmop_ctx* ctx) {
+  if (!ctx) return LMOP_ERR_INVALID_ARG;
+  if (ctx->dead)
+    return fail(ctx, LMOP_ERR_DEVICE, "ctx is unusable after an earlier error (%s)",
+                ctx->err.c_str());
+  ctx->err.clear();
+  if (!ctx->host_only) HIP_OK(ctx, hipSetDevice(ctx->device));
+  return LMOP_OK;
+}
+
+static void release_all_prefixes(lmop_ctx* c) {
+  for (lmop_prefix* p : c->prefixes) {
+    destroy_prefix_storage(p);
+    delete p;
+  }
+  c->prefixes.clear();
+}
+
+lmop_status lmop_load_weights(lmop_ctx* ctx, const lmop_weights* w) {
+  LMOP_TRY(enter(ctx));
+  const lmop_config& cf = ctx->cfg;
+  if (!w) return fail(ctx, LMOP_ERR_INVALID_ARG, "weights is NULL");
+  if (w->n_layers != cf.n_layers)
+    return fail(ctx, LMOP_ERR_INVALID_ARG, "weights have %d layers, config %d", w->n_layers,
+                cf.n_layers);
+  if (!w->tok_embedding || !w->lm_head || !w->final_norm || (cf.n_layers > 0 && !w->layers))
+    return fail(ctx, LMOP_ERR_INVALID_ARG, "NULL embedding, head, final norm or layer array");
+  const int d = cf.d_model, nq = ctx->nq_dim, nkv = ctx->nkv_dim, F = cf.d_ff;
+  for (int l = 0; l < cf.n_layers; ++l) {
+    const lmop_layer& L = w->layers[l];
+    if (!L.attn_norm || !L.mlp_norm)
+      return fail(ctx, LMOP_ERR_INVALID_ARG, "layer %d: NULL norm gain", l);
+    LMOP_TRY(check_qmat(ctx, "wq", l, L.wq, nq, d));
+    LMOP_TRY(check_qmat(ctx, "wk", l, L.wk, nkv, d));
+    LMOP_TRY(check_qmat(ctx, "wv", l, L.wv, nkv, d));
+    LMOP_TRY(check_qmat(ctx, "wo", l, L.wo, d, nq));
+    LMOP_TRY(check_qmat(ctx, "w_gate", l, L.w_gate, F, d));
+    LMOP_TRY(check_qmat(ctx, "w_up", l, L.w_up, F, d));
+    LMOP_TRY(check_qmat(ctx, "w_down", l, L.w_down, d, F));
+  }
+  if (ctx->host_only) {
+    release_all_prefixes(ctx);
+    ctx->generation++;
+    ctx->loaded = true;
+    return LMOP_OK;
+  }
+  HIP_OK(ctx, hipStreamSynchronize(ctx->stream));
+  release_all_prefixes(ctx);
+  free_weights(ctx);
+  ctx->loaded = false;
+  ctx->generation++;
+  const bool od = w->on_device != 0;
+  const size_t V = cf.vocab;
+  void* p = nullptr;
+  LMOP_TRY(upload(ctx, w->tok_embedding, V * d * 2, od, &p));
+  ctx->emb = (uint16_t*)p;
+  LMOP_TRY(upload(ctx, w->lm_head, V * d * 2, od, &p));
+  ctx->head = (uint16_t*)p;
+  LMOP_TRY(upload(ctx, w->final_norm, (size_t)d * 4, od, &p));
+  ctx->final_norm = (float*)p;
+  ctx->layers.resize(cf.n_layers);
+  for (int l = 0; l < cf.n_layers; ++l) {
+    const lmop_layer& L = w->layers[l];
+    LayerW& D = ctx->layers[l];
+    LMOP_TRY(upload(ctx, L.attn_norm, (size_t)d * 4, od, &p));
+    D.attn_norm = (float*)p;
+    LMOP_TRY(upload(ctx, L.mlp_norm, (size_t)d * 4, od, &p));
+    D.mlp_norm = (float*)p;
+    {  // fused q | k | v
+      const lmop_qmat* s[3] = {&L.wq, &L.wk, &L.wv};
+      const int rows[3] = {nq, nkv, nkv};
+      auto m = concat_map(rows, 3, round_up(ctx->qkv_n, 128));
+      LMOP_TRY(pack(ctx, s, 3, m, ctx->qkv_n, d, od, &D.qkv));
+    }
+    {
+      const lmop_qmat* s[1] = {&L.wo};
+      const int rows[1] = {d};
+      LMOP_TRY(pack(ctx, s, 1, concat_map(rows, 1, round_up(d, 128)), d, nq, od, &D.o));
+    }
+    {  // gate/up interleaved in blocks of 32: block b = [gate 32b..32b+31 | up 32b..32b+31]
+      const lmop_qmat* s[2] = {&L.w_gate, &L.w_up};
+      const int nblk = round_up(F, 32) / 32;
+      std::vector<int32_t> m(round_up(nblk * 64, 128), -1);
+      for (int b = 0; b < nblk; ++b)
+        for (int i = 0; i < 32; ++i) {
+          const int r = b * 32 + i;
+          if (r < F) {
+            m[b * 64 + i] = (0 << 24) | r;
+            m[b * 64 + 32 + i] = (1 << 24) | r;
+          }
+        }
+      LMOP_TRY(pack(ctx, s, 2, m, 2 * F, d, od, &D.gu));
+    }
+    {
+      const lmop_qmat* s[1] = {&L.w_down};
+      const int rows[1] = {d};
+      LMOP_TRY(pack(ctx, s, 1, concat_map(rows, 1, round_up(d, 128)), d, F, od, &D.down));
+    }
+  }
+  LMOP_TRY(sync(ctx));
+  ctx->loaded = true;
+  return LMOP_OK;
+}
+
+int32_t lmop_prefix_length(const lmop_prefix* p) { return p ? p->start + p->n : -1; }
+
+lmop_status lmop_set_prefix(lmop_ctx* ctx, const lmop_prefix* parent, const int32_t* tokens,
+                            int32_t n_tokens, lmop_prefix** out) {
+  if (out) *out = nullptr;
+  LMOP_TRY(enter(ctx));
+  if (!out) return fail(ctx, LMOP_ERR_INVALID_ARG, "out is NULL");
+  if (!ctx->loaded) return fail(ctx, LMOP_ERR_STATE, "lmop_load_weights has not succeeded");
+  if (n_tokens < 1 || !tokens)
+    return fail(ctx, LMOP_ERR_INVALID_ARG, "a prefix needs at least one token");
+  if (parent && !prefix_live(ctx, parent))
+    return fail(ctx, LMOP_ERR_INVALID_ARG, "parent prefix is released or from another ctx");
+  if (parent && parent->parent)
+    return fail(ctx, LMOP_ERR_UNSUPPORTED, "a child prefix cannot have children");
+  LMOP_TRY(check_tokens(ctx, tokens, n_tokens, "prefix"));
+  const lmop_config& cf = ctx->cfg;
+  const int start = prefix_total(parent);
+  if (start + n_tokens >= cf.max_seq)
+    return fail(ctx, LMOP_ERR_INVALID_ARG, "prefix length %d exceeds max_seq %d",
+                start + n_tokens, cf.max_seq);
+
+  std::unique_ptr<lmop_prefix> p(new lmop_prefix());
+  p->ctx = ctx;
+  p->parent = const_cast<lmop_prefix*>(parent);
+  p->n = n_tokens;
+  p->start = start;
+  p->generation = ctx->generation;
+  p->id = ctx->next_prefix_id++;
+  if (!ctx->host_only) {
+    void* kv = nullptr;
+    void* hid = nullptr;
+    LMOP_TRY(dev_alloc(ctx, &kv, (size_t)cf.n_layers * 2 * n_tokens * ctx->nkv_dim * 2));
+    p->kv = (uint16_t*)kv;
+    if (dev_alloc(ctx, &hid, (size_t)cf.d_model * 4) != LMOP_OK) {
+      destroy_prefix_storage(p.get());
+      return LMOP_ERR_OOM;
+    }
+    p->hidden = (float*)hid;
+    std::vector<int32_t> tok(tokens, tokens + n_tokens), pos(n_tokens), slot(n_tokens);
+    for (int j = 0; j < n_tokens; ++j) {
+      pos[j] = start + j;
+      slot[j] = j;
+    }
+    std::vector<AttnRow> rows(1);
+    fill_segments(parent, rows[0]);
+    rows[0].q_start = 0;
+    rows[0].n_q = n_tokens;
+    rows[0].own_slot = 0;
+    rows[0].own_q0 = 0;
+    std::vector<int2> work;
+    add_work(work, 0, n_tokens, cf.n_heads / cf.n_kv_heads);
+    lmop_status st = upload_batch(ctx, tok, pos, slot, rows, work);
+    Batch b;
+    b.T = n_tokens;
+    b.R = 1;
+    b.n_work = (int)work.size();
+    b.own_kv = p->kv;
+    b.own_cap = n_tokens;
+    if (st == LMOP_OK) st = forward(ctx, b);
+    if (st == LMOP_OK) {
+      float* x = nullptr;
+      st = ws_get(ctx, "x", (size_t)n_tokens * cf.d_model, &x);
+      if (st == LMOP_OK) {
+        hipError_t e = hipMemcpyAsync(p->hidden, x + (size_t)(n_tokens - 1) * cf.d_model,
+                                      (size_t)cf.d_model * 4, hipMemcpyDeviceToDevice,
+                                      ctx->stream);
+        if (e != hipSuccess) st = fail(ctx, LMOP_ERR_DEVICE, "copy of prefix hidden failed");
+      }
+    }
+    if (st == LMOP_OK) st = sync(ctx);
+    if (st != LMOP_OK) {
+      destroy_prefix_storage(p.get());
+      return st;
+    }
+  }
+  if (parent) const_cast<lmop_prefix*>(parent)->children++;
+  ctx->prefixes.insert(p.get());
+  *out = p.release();
+  return LMOP_OK;
+}
+
+static void maybe_free_prefix(lmop_ctx* ctx, lmop_prefix* p) {
+  while (p && p->released && p->children == 0) {
+    lmop_prefix* par = p->parent;
+    ctx->prefixes.erase(p);
+    destroy_prefix_storage(p);
+    delete p;
+    if (par) par->children--;
+    p = par;
+  }
+}
+
+lmop_status lmop_release_prefix(lmop_ctx* ctx, lmop_prefix* prefix) {
+  if (!ctx) return LMOP_ERR_INVALID_ARG;
+  ctx->err.clear();
+  if (!prefix || !ctx->prefixes.count(prefix) || prefix->released)
+    return fail(ctx, LMOP_ERR_INVALID_ARG, "prefix is NULL, already released or from another ctx");
+  if (!ctx->host_only && ctx->stream) {
+    hipError_t e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return fail(ctx, LMOP_ERR_DEVICE, "stream sync failed");
+  }
+  prefix->released = true;
+  maybe_free_prefix(ctx, prefix);
+  return LMOP_OK;
+}
+
+lmop_status lmop_dedup_rows(const int32_t* tokens, const int64_t* offsets, int32_t n_rows,
+                            const int64_t* keys, int32_t* rep, int32_t* n_unique) {
+  if (n_rows < 0 || !n_unique || (n_rows > 0 && (!offsets || !rep)))
+    return LMOP_ERR_INVALID_ARG;
+  if (n_rows == 0) {
+    *n_unique = 0;
+    return LMOP_OK;
+  }
+  if (offsets[0] != 0) return LMOP_ERR_INVALID_ARG;
+  for (int r = 0; r < n_rows; ++r)
+    if (offsets[r + 1] < offsets[r]) return LMOP_ERR_INVALID_ARG;
+  if (offsets[n_rows] > 0 && !tokens) return LMOP_ERR_INVALID_ARG;
+  dedup(tokens, offsets, n_rows, keys, rep, n_unique);
+  return LMOP_OK;
+}
+
+lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
+                           const lmop_prefix* const* row_prefix, const int32_t* tokens,
+                           const int64_t* offsets, int32_t n_rows, const lmop_type* type,
+                           lmop_result* out, const lmop_eval_opts* opts) {
+  LMOP_TRY(enter(ctx));
+  if (!ctx->loaded) return fail(ctx, LMOP_ERR_STATE, "lmop_load_weights has not succeeded");
+  if (n_rows < 0) return fail(ctx, LMOP_ERR_INVALID_ARG, "n_rows < 0");
+  LMOP_TRY(check_type(ctx, type));
+  if (n_rows == 0) return LMOP_OK;
+  if (!offsets || !out) return fail(ctx, LMOP_ERR_INVALID_ARG, "NULL offsets or out");
+  if (offsets[0] != 0) return fail(ctx, LMOP_ERR_INVALID_ARG, "offsets[0] != 0");
+  for (int r = 0; r < n_rows; ++r)
+    if (offsets[r + 1] < offsets[r])
+      return fail(ctx, LMOP_ERR_INVALID_ARG, "offsets decrease at row %d", r);
+  const int64_t total = offsets[n_rows];
+  if (total > 0 && !tokens) return fail(ctx, LMOP_ERR_INVALID_ARG, "tokens is NULL");
+  LMOP_TRY(check_tokens(ctx, tokens, total, "row"));
+  const lmop_config& cf = ctx->cfg;
+  const int steps = type->kind == LMOP_INT ? type->max_tokens : 1;
+  const int dec = steps - 1;
+  if (prefix && !prefix_live(ctx, prefix))
+    return fail(ctx, LMOP_ERR_INVALID_ARG, "prefix is released or from another ctx");
+  std::vector<const lmop_prefix*> pf(n_rows);
+  for (int r = 0; r < n_rows; ++r) {
+    const lmop_prefix* p = row_prefix ? row_prefix[r] : prefix;
+    if (p && p != prefix && !prefix_live(ctx, p))
+      return fail(ctx, LMOP_ERR_INVALID_ARG, "row %d: prefix is released or from another ctx", r);
+    const int64_t len = offsets[r + 1] - offsets[r];
+    if (!p && len == 0)
+      return fail(ctx, LMOP_ERR_INVALID_ARG, "row %d has neither a prefix nor suffix tokens", r);
+    if (prefix_total(p) + len + dec > cf.max_seq)
+      return fail(ctx, LMOP_ERR_INVALID_ARG, "row %d: sequence of %lld tokens exceeds max_seq %d",
+                  r, (long long)(prefix_total(p) + len + dec), cf.max_seq);
+    pf[r] = p;
+  }
+  if (ctx->host_only)
+    return fail(ctx, LMOP_ERR_UNSUPPORTED, "host-only ctx: arguments are valid, no device to run");
+
+  const uint32_t flags = opts ? opts->flags : 0u;
+  int budget = opts && opts->max_batch_tokens > 0 ? opts->max_batch_tokens : kDefaultBatchTokens;
+  float* dbg = opts ? opts->debug_logits : nullptr;
+  const int V = cf.vocab;
+
+  // early deduplication: one evaluation per distinct (prefix, suffix)
+  std::vector<int32_t> rep(n_rows);
+  int32_t n_unique = 0;
+  if (flags & LMOP_NO_DEDUP) {
+    for (int r = 0; r < n_rows; ++r) rep[r] = r;
+    n_unique = n_rows;
+  } else {
+    std::vector<int64_t> keys(n_rows);
+    for (int r = 0; r < n_rows; ++r) keys[r] = pf[r] ? pf[r]->id : 0;
+    dedup(tokens, offsets, n_rows, keys.data(), rep.data(), &n_unique);
+  }
+  std::vector<int32_t> uniq;
+  uniq.reserve(n_unique);
+  for (int r = 0; r < n_rows; ++r)
+    if (rep[r] == r) uniq.push_back(r);
+  // group rows of one prefix together (attention reads that prefix's KV)
+  std::stable_sort(uniq.begin(), uniq.end(), [&](int a, int b) {
+    const int64_t ia = pf[a] ? pf[a]->id : 0, ib = pf[b] ? pf[b]->id : 0;
+    return ia < ib;
+  });
+
+  // allowed-token map: sel[token] = position in the allowed list (INT: EOS last)
+  const int n_allowed0 = type->n_tokens;
+  std::vector<int32_t> allowed(type->tokens, type->tokens + n_allowed0);
+  if (type->kind == LMOP_INT) allowed.push_back(type->eos_token);
+  const int n_sel = (int)allowed.size();
+  std::vector<int32_t> sel(V, -1);
+  for (int i = 0; i < n_sel; ++i) sel[allowed[i]] = i;
+  int32_t *d_sel, *d_allowed;
+  LMOP_TRY(ws_get(ctx, "sel", V, &d_sel));
+  LMOP_TRY(ws_get(ctx, "allowed", n_sel, &d_allowed));
+  HIP_OK(ctx, hipMemcpyAsync(d_sel, sel.data(), V * 4, hipMemcpyHostToDevice, ctx->stream));
+  HIP_OK(ctx, hipMemcpyAsync(d_allowed, allowed.data(), n_sel * 4, hipMemcpyHostToDevice,
+                             ctx->stream));
+  HIP_OK(ctx, hipStreamSynchronize(ctx->stream));
+
+  const int G = cf.n_heads / cf.n_kv_heads;
+  const int d = cf.d_model;
+  std::vector<lmop_result> res(n_rows);
+  size_t u0 = 0;
+  while (u0 < uniq.size()) {
+    // ---- pack one batch
+    size_t u1 = u0;
+    int T = 0;
+    while (u1 < uniq.size() && (int)(u1 - u0) < kMaxBatchRows) {
+      const int len = (int)(offsets[uniq[u1] + 1] - offsets[uniq[u1]]);
+      if (u1 > u0 && T + len > budget) break;
+      T += len;
+      ++u1;
+    }
+    const int R = (int)(u1 - u0);
+    std::vector<int32_t> tok(T), pos(T), slot(T);
+    std::vector<AttnRow> rows(R);
+    std::vector<int2> work;
+    std::vector<int> len(R), own(R), qs(R);
+    int t = 0, cap = 0;
+    for (int i = 0; i < R; ++i) {
+      const int r = uniq[u0 + i];
+      const lmop_prefix* p = pf[r];
+      len[i] = (int)(offsets[r + 1] - offsets[r]);
+      own[i] = cap;
+      qs[i] = t;
+      const int P = prefix_total(p);
+      for (int j = 0; j < len[i]; ++j) {
+        tok[t + j] = tokens[offsets[r] + j];
+        pos[t + j] = P + j;
+        slot[t + j] = cap + j;
+      }
+      AttnRow& ar = rows[i];
+      fill_segments(p, ar);
+      ar.q_start = t;
+      ar.n_q = len[i];
+      ar.own_slot = cap;
+      ar.own_q0 = 0;
+      add_work(work, i, len[i], G);
+      t += len[i];
+      cap += len[i] + dec;
+    }
+    uint16_t* own_kv;
+    LMOP_TRY(ws_get(ctx, "own_kv", (size_t)cf.n_layers * 2 * std::max(cap, 1) * ctx->nkv_dim,
+                    &own_kv));
+    LMOP_TRY(upload_batch(ctx, tok, pos, slot, rows, work));
+    Batch b;
+    b.T = T;
+    b.R = R;
+    b.n_work = (int)work.size();
+    b.own_kv = own_kv;
+    b.own_cap = std::max(cap, 1);
+    LMOP_TRY(forward(ctx, b));
+    float* x;
+    LMOP_TRY(ws_get(ctx, "x", (size_t)std::max(T, 1) * d, &x));
+    std::vector<const float*> rowptr(R);
+    for (int i = 0; i < R; ++i) {
+      const int r = uniq[u0 + i];
+      rowptr[i] = len[i] > 0 ? x + (size_t)(qs[i] + len[i] - 1) * d : pf[r]->hidden;
+    }
+    float* dump = nullptr;
+    if (dbg) LMOP_TRY(ws_get(ctx, "dump", (size_t)R * V, &dump));
+
+    // ---- constrained steps
+    std::vector<int> live(R);
+    for (int i = 0; i < R; ++i) live[i] = i;
+    std::vector<int> last_tok(R, -1);
+    for (int i = 0; i < R; ++i) {
+      lmop_result& o = res[uniq[u0 + i]];
+      o.value = 0;
+      o.logprob = 0.f;
+      o.logprob_full = 0.f;
+      o.n_tokens = 0;
+      for (int k = 0; k < 8; ++k) o.tokens[k] = -1;
+    }
+    if (dbg)
+      for (int i = 0; i < R; ++i)
+        std::fill(dbg + (size_t)uniq[u0 + i] * steps * V,
+                  dbg + (size_t)(uniq[u0 + i] + 1) * steps * V, NAN);
+    for (int step = 0; step < steps && !live.empty(); ++step) {
+      const int nl = (int)live.size();
+      if (step > 0) {
+        // one more token per live row: its id, position and KV slot
+        std::vector<int32_t> st(nl), sp(nl), ss(nl);
+        std::vector<AttnRow> sr(nl);
+        std::vector<int2> sw;
+        for (int k = 0; k < nl; ++k) {
+          const int i = live[k];
+          const int r = uniq[u0 + i];
+          const int own_idx = len[i] + step - 1;
+          st[k] = last_tok[i];
+          sp[k] = prefix_total(pf[r]) + own_idx;
+          ss[k] = own[i] + own_idx;
+          fill_segments(pf[r], sr[k]);
+          sr[k].q_start = k;
+          sr[k].n_q = 1;
+          sr[k].own_slot = own[i];
+          sr[k].own_q0 = own_idx;
+          add_work(sw, k, 1, G);
+        }
+        LMOP_TRY(upload_batch(ctx, st, sp, ss, sr, sw));
+        Batch sb;
+        sb.T = nl;
+        sb.R = nl;
+        sb.n_work = (int)sw.size();
+        sb.own_kv = own_kv;
+        sb.own_cap = b.own_cap;
+        LMOP_TRY(forward(ctx, sb));
+        LMOP_TRY(ws_get(ctx, "x", (size_t)nl * d, &x));
+        rowptr.resize(nl);
+        for (int k = 0; k < nl; ++k) rowptr[k] = x + (size_t)k * d;
+      }
+      const int n_allowed = (type->kind == LMOP_INT && step > 0) ? n_sel : n_allowed0;
+      std::vector<HeadPick> picks;
+      LMOP_TRY(run_head(ctx, nl, rowptr, d_sel, d_allowed, n_sel, n_allowed, picks, dump));
+      LMOP_TRY(sync(ctx));
+      if (dbg) {
+        for (int k = 0; k < nl; ++k) {
+          const int r = uniq[u0 + live[k]];
+          HIP_OK(ctx, hipMemcpy(dbg + ((size_t)r * steps + step) * V, dump + (size_t)k * V,
+                                (size_t)V * 4, hipMemcpyDeviceToHost));
+        }
+      }
+      std::vector<int> next;
+      for (int k = 0; k < nl; ++k) {
+        const int i = live[k];
+        lmop_result& o = res[uniq[u0 + i]];
+        const HeadPick& hp = picks[k];
+        o.logprob += hp.logprob;
+        o.logprob_full += hp.logprob_full;
+        o.tokens[o.n_tokens++] = hp.token;
+        if (type->kind == LMOP_INT) {
+          if (hp.index == n_allowed0) continue;  // EOS
+          o.value = o.value * 10 + hp.index;
+          last_tok[i] = hp.token;
+          if (o.n_tokens < steps) next.push_back(i);
+        } else {
+          o.value = hp.index;
+        }
+      }
+      live.swap(next);
+    }
+    u0 = u1;
+  }
+  for (int r = 0; r < n_rows; ++r) {
+    out[r] = res[rep[r]];
+    if (dbg && rep[r] != r)
+      std::memcpy(dbg + (size_t)r * steps * V, dbg + (size_t)rep[r] * steps * V,
+                  (size_t)steps * V * sizeof(float));
+  }
+  return LMOP_OK;
+}
+
+lmop_status lmop_set_profiling(lmop_ctx* ctx, int32_t enable) {
+  if (!ctx) return LMOP_ERR_INVALID_ARG;
+  if (!ctx->host_only) LMOP_TRY(sync(ctx));
+  ctx->prof = enable != 0;
+  ctx->stats.clear();
+  return LMOP_OK;
+}
+
+lmop_status lmop_get_kernel_stats(lmop_ctx* ctx, lmop_kernel_stat* out, int32_t max_entries,
+                                  int32_t* n_entries) {
+  if (!ctx || !n_entries || max_entries < 0 || (max_entries > 0 && !out))
+    return LMOP_ERR_INVALID_ARG;
+  if (!ctx->host_only) LMOP_TRY(sync(ctx));
+  int i = 0;
+  for (auto& kv : ctx->stats) {
+    if (i < max_entries) {
+      lmop_kernel_stat& s = out[i];
+      std::memset(&s, 0, sizeof s);
+      std::snprintf(s.name, sizeof s.name, "%s", kv.first.c_str());
+      s.launches = kv.second.launches;
+      s.total_ms = kv.second.ms;
+      s.flops = kv.second.flops;
+      s.bytes = kv.second.bytes;
+    }
+    ++i;
+  }
+  *n_entries = i;
+  return LMOP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,311 @@
+"""Python binding of liblmop (include/lmop.h): argument marshalling only.
+
+Every computation runs in the library's HIP kernels; this module converts
+numpy / torch arguments to the C structs and back.  The functions keep the C
+names (lmop_create, lmop_load_weights, lmop_set_prefix, lmop_eval_rows, ...);
+`Context` bundles them for convenience.  If the built library is missing,
+importing the binding raises: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_lib", "liblmop.so")
+
+LMOP_OK, LMOP_ERR_INVALID_ARG, LMOP_ERR_STATE, LMOP_ERR_OOM, LMOP_ERR_DEVICE, \
+    LMOP_ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
+LMOP_BOOL, LMOP_ENUM, LMOP_INT = 0, 1, 2
+LMOP_NO_DEDUP = 1
+
+EXPORTED = (
+    "lmop_create", "lmop_destroy", "lmop_last_error", "lmop_status_string", "lmop_load_weights",
+    "lmop_set_prefix", "lmop_release_prefix", "lmop_prefix_length", "lmop_eval_rows",
+    "lmop_dedup_rows", "lmop_set_profiling", "lmop_get_kernel_stats",
+)
+
+
+class lmop_config(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_ff", C.c_int32),
+                ("vocab", C.c_int32), ("group_size", C.c_int32), ("rms_eps", C.c_float),
+                ("rope_theta", C.c_float), ("max_seq", C.c_int32)]
+
+
+class lmop_qmat(C.Structure):
+    _fields_ = [("qweight", C.c_void_p), ("scales", C.c_void_p), ("n", C.c_int32),
+                ("k", C.c_int32)]
+
+
+class lmop_layer(C.Structure):
+    _fields_ = [("attn_norm", C.c_void_p), ("mlp_norm", C.c_void_p), ("wq", lmop_qmat),
+                ("wk", lmop_qmat), ("wv", lmop_qmat), ("wo", lmop_qmat), ("w_gate", lmop_qmat),
+                ("w_up", lmop_qmat), ("w_down", lmop_qmat)]
+
+
+class lmop_weights(C.Structure):
+    _fields_ = [("tok_embedding", C.c_void_p), ("lm_head", C.c_void_p),
+                ("final_norm", C.c_void_p), ("layers", C.POINTER(lmop_layer)),
+                ("n_layers", C.c_int32), ("on_device", C.c_int32)]
+
+
+class lmop_type(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("tokens", C.POINTER(C.c_int32)), ("n_tokens", C.c_int32),
+                ("eos_token", C.c_int32), ("max_tokens", C.c_int32)]
+
+
+class lmop_result(C.Structure):
+    _fields_ = [("value", C.c_int64), ("logprob", C.c_float), ("logprob_full", C.c_float),
+                ("n_tokens", C.c_int32), ("tokens", C.c_int32 * 8)]
+
+
+class lmop_eval_opts(C.Structure):
+    _fields_ = [("flags", C.c_uint32), ("max_batch_tokens", C.c_int32),
+                ("debug_logits", C.POINTER(C.c_float))]
+
+
+class lmop_kernel_stat(C.Structure):
+    _fields_ = [("name", C.c_char * 48), ("launches", C.c_int64), ("total_ms", C.c_double),
+                ("flops", C.c_double), ("bytes", C.c_double)]
+
+
+RESULT_DTYPE = np.dtype([("value", "<i8"), ("logprob", "<f4"), ("logprob_full", "<f4"),
+                         ("n_tokens", "<i4"), ("tokens", "<i4", (8,)), ("_pad", "<i4")])
+assert C.sizeof(lmop_result) == RESULT_DTYPE.itemsize
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_31808_amd.build`")
+    lib = C.CDLL(LIB_PATH)
+    vp, i32, st = C.c_void_p, C.c_int32, C.c_int
+    sig = {
+        "lmop_create": (st, [C.POINTER(lmop_config), i32, vp, C.POINTER(vp)]),
+        "lmop_destroy": (None, [vp]),
+        "lmop_last_error": (C.c_char_p, [vp]),
+        "lmop_status_string": (C.c_char_p, [st]),
+        "lmop_load_weights": (st, [vp, C.POINTER(lmop_weights)]),
+        "lmop_set_prefix": (st, [vp, vp, C.POINTER(C.c_int32), i32, C.POINTER(vp)]),
+        "lmop_release_prefix": (st, [vp, vp]),
+        "lmop_prefix_length": (i32, [vp]),
+        "lmop_eval_rows": (st, [vp, vp, C.POINTER(vp), C.POINTER(C.c_int32),
+                                C.POINTER(C.c_int64), i32, C.POINTER(lmop_type), vp,
+                                C.POINTER(lmop_eval_opts)]),
+        "lmop_dedup_rows": (st, [C.POINTER(C.c_int32), C.POINTER(C.c_int64), i32,
+                                 C.POINTER(C.c_int64), C.POINTER(C.c_int32),
+                                 C.POINTER(C.c_int32)]),
+        "lmop_set_profiling": (st, [vp, i32]),
+        "lmop_get_kernel_stats": (st, [vp, C.POINTER(lmop_kernel_stat), i32,
+                                       C.POINTER(C.c_int32)]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+class LmopError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_lib.lmop_status_string(status).decode()} ({status}): {message}")
+        self.status = status
+
+
+def _check(status: int, ctx) -> None:
+    if status != LMOP_OK:
+        msg = _lib.lmop_last_error(ctx)
+        raise LmopError(status, msg.decode() if msg else "")
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _i64(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int64))
+
+
+def _ptr(a: np.ndarray, ct):
+    return a.ctypes.data_as(C.POINTER(ct))
+
+
+# ---------------------------------------------------------------- C-named calls
+def lmop_create(cfg: lmop_config, device: int = 0, stream: Optional[int] = None):
+    out = C.c_void_p()
+    st = _lib.lmop_create(C.byref(cfg), device, C.c_void_p(stream or 0), C.byref(out))
+    _check(st, None)
+    return out
+
+
+def lmop_destroy(ctx) -> None:
+    _lib.lmop_destroy(ctx)
+
+
+def _tensor_ptr(t, keep):
+    """Device or host address of a contiguous torch tensor / numpy array."""
+    if hasattr(t, "data_ptr"):
+        t = t.contiguous()
+        keep.append(t)
+        return t.data_ptr(), t.device.type != "cpu"
+    a = np.ascontiguousarray(t)
+    keep.append(a)
+    return a.ctypes.data, False
+
+
+def lmop_load_weights(ctx, weights) -> None:
+    """weights: object with tok_embedding, lm_head (fp16 [V][d]), final_norm, layers[...]
+    (attn_norm, mlp_norm, wq .. w_down each with qweight/scales/n/k), all on one device."""
+    keep = []
+    where = set()
+
+    def p(t):
+        a, dev = _tensor_ptr(t, keep)
+        where.add(dev)
+        return a
+
+    def qm(m):
+        return lmop_qmat(p(m.qweight), p(m.scales), int(m.n), int(m.k))
+
+    L = len(weights.layers)
+    arr = (lmop_layer * max(L, 1))()
+    for i, l in enumerate(weights.layers):
+        arr[i] = lmop_layer(p(l.attn_norm), p(l.mlp_norm), qm(l.wq), qm(l.wk), qm(l.wv), qm(l.wo),
+                            qm(l.w_gate), qm(l.w_up), qm(l.w_down))
+    w = lmop_weights(p(weights.tok_embedding), p(weights.lm_head), p(weights.final_norm),
+                     C.cast(arr, C.POINTER(lmop_layer)), L, 0)
+    if len(where) != 1:
+        raise ValueError("weights must all be on the host or all on the device")
+    w.on_device = 1 if where.pop() else 0
+    _check(_lib.lmop_load_weights(ctx, C.byref(w)), ctx)
+
+
+def lmop_set_prefix(ctx, tokens, parent=None):
+    t = _i32(tokens)
+    out = C.c_void_p()
+    _check(_lib.lmop_set_prefix(ctx, parent, _ptr(t, C.c_int32), len(t), C.byref(out)), ctx)
+    return out
+
+
+def lmop_release_prefix(ctx, prefix) -> None:
+    _check(_lib.lmop_release_prefix(ctx, prefix), ctx)
+
+
+def lmop_prefix_length(prefix) -> int:
+    return int(_lib.lmop_prefix_length(prefix))
+
+
+def lmop_eval_rows(ctx, tokens, offsets, kind: int, allowed: Sequence[int], eos: int = -1,
+                   max_tokens: int = 1, prefix=None, row_prefix=None, flags: int = 0,
+                   max_batch_tokens: int = 0, debug_logits: bool = False, vocab: int = 0):
+    """Returns a structured numpy array of lmop_result (value, logprob, logprob_full,
+    n_tokens, tokens) and, with debug_logits, fp32 logits [n_rows][steps][vocab]."""
+    toks = _i32(tokens)
+    offs = _i64(offsets)
+    n = len(offs) - 1
+    al = _i32(allowed)
+    ty = lmop_type(kind, _ptr(al, C.c_int32), len(al), int(eos), int(max_tokens))
+    out = np.zeros(max(n, 0), dtype=RESULT_DTYPE)
+    steps = max_tokens if kind == LMOP_INT else 1
+    dbg = None
+    opts = lmop_eval_opts(flags, max_batch_tokens, None)
+    if debug_logits:
+        if vocab <= 0:
+            raise ValueError("debug_logits needs vocab")
+        dbg = np.empty((n, steps, vocab), dtype=np.float32)
+        opts.debug_logits = _ptr(dbg, C.c_float)
+    rp = None
+    if row_prefix is not None:
+        rp = (C.c_void_p * max(n, 1))(*[r.value if isinstance(r, C.c_void_p) else r
+                                        for r in row_prefix])
+    _check(_lib.lmop_eval_rows(ctx, prefix, rp, _ptr(toks, C.c_int32), _ptr(offs, C.c_int64), n,
+                               C.byref(ty), out.ctypes.data, C.byref(opts)), ctx)
+    return out, dbg
+
+
+def lmop_dedup_rows(tokens, offsets, keys=None):
+    toks = _i32(tokens)
+    offs = _i64(offsets)
+    n = len(offs) - 1
+    rep = np.zeros(max(n, 0), dtype=np.int32)
+    nu = C.c_int32()
+    kp = None
+    if keys is not None:
+        k = _i64(keys)
+        kp = _ptr(k, C.c_int64)
+    st = _lib.lmop_dedup_rows(_ptr(toks, C.c_int32), _ptr(offs, C.c_int64), n, kp,
+                              _ptr(rep, C.c_int32), C.byref(nu))
+    if st != LMOP_OK:
+        raise LmopError(st, "invalid CSR arguments")
+    return rep, int(nu.value)
+
+
+def lmop_set_profiling(ctx, enable: bool) -> None:
+    _check(_lib.lmop_set_profiling(ctx, 1 if enable else 0), ctx)
+
+
+def lmop_get_kernel_stats(ctx):
+    n = C.c_int32()
+    _check(_lib.lmop_get_kernel_stats(ctx, None, 0, C.byref(n)), ctx)
+    arr = (lmop_kernel_stat * max(n.value, 1))()
+    _check(_lib.lmop_get_kernel_stats(ctx, arr, n.value, C.byref(n)), ctx)
+    return {arr[i].name.decode(): dict(launches=arr[i].launches, ms=arr[i].total_ms,
+                                       flops=arr[i].flops, bytes=arr[i].bytes)
+            for i in range(n.value)}
+
+
+# ---------------------------------------------------------------- convenience
+def config_from_shape(shape, max_seq: int = 0) -> lmop_config:
+    return lmop_config(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads,
+                       shape.head_dim, shape.d_ff, shape.vocab, shape.group_size,
+                       shape.rms_eps, shape.rope_theta, max_seq)
+
+
+class Context:
+    """One lmop ctx on a HIP device (device=-1: host-only, validation only)."""
+
+    def __init__(self, shape, device: int = 0, stream: Optional[int] = None, max_seq: int = 0,
+                 n_layers: Optional[int] = None):
+        cfg = config_from_shape(shape, max_seq)
+        if n_layers is not None:
+            cfg.n_layers = n_layers
+        self.vocab = shape.vocab
+        self.ctx = lmop_create(cfg, device, stream)
+
+    def close(self):
+        if self.ctx:
+            lmop_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def load_weights(self, weights):
+        lmop_load_weights(self.ctx, weights)
+
+    def set_prefix(self, tokens, parent=None):
+        return lmop_set_prefix(self.ctx, tokens, parent)
+
+    def release_prefix(self, p):
+        lmop_release_prefix(self.ctx, p)
+
+    def eval_rows(self, tokens, offsets, kind, allowed, eos=-1, max_tokens=1, prefix=None,
+                  row_prefix=None, no_dedup=False, max_batch_tokens=0, debug_logits=False):
+        return lmop_eval_rows(self.ctx, tokens, offsets, kind, allowed, eos, max_tokens, prefix,
+                              row_prefix, LMOP_NO_DEDUP if no_dedup else 0, max_batch_tokens,
+                              debug_logits, self.vocab)
+
+    def set_profiling(self, on: bool):
+        lmop_set_profiling(self.ctx, on)
+
+    def kernel_stats(self):
+        return lmop_get_kernel_stats(self.ctx)

@@ -1,0 +1,187 @@
+"""GPU parity of the whole row-evaluation path on the tiny decoder (2 layers,
+d 256, 4 heads, vocab 2048) against the fp64 oracle, through the C ABI.
+Sizes span several GEMM and attention tiles with ragged tails."""
+import dataclasses
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import KIND_BOOL, KIND_ENUM, KIND_INT, OracleLM
+from synth import SHAPES, make_weights, make_workload
+from tests.parity import assert_typed, compare
+
+pytestmark = pytest.mark.gpu
+TINY = SHAPES["tiny"]
+
+
+def _log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_31808_amd import lmop
+    return lmop
+
+
+@pytest.fixture(scope="module")
+def tiny(L):
+    w = make_weights(TINY, seed=1234)
+    orc = OracleLM(w, TINY)
+    ctx = L.Context(TINY, device=0)
+    ctx.load_weights(w)  # host weights
+    return w, orc, ctx
+
+
+def _run(ctx, wl, prefix, **kw):
+    return ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, eos=wl.eos,
+                         max_tokens=wl.max_tokens, prefix=prefix, debug_logits=True, **kw)
+
+
+def test_zero_layer_model_head_only(L):
+    """L = 0: embedding -> final RMSNorm -> LM head -> constrained pick."""
+    w = make_weights(TINY, seed=77, n_layers=0)
+    shape0 = dataclasses.replace(TINY, n_layers=0)
+    orc = OracleLM(w, shape0)
+    ctx = L.Context(shape0, device=0)
+    ctx.load_weights(w)
+    wl = make_workload("filter_tiny", n_rows=20)
+    _log("zero-layer: eval")
+    out, dbg = _run(ctx, wl, None)
+    ref = orc.eval_workload(dataclasses.replace(wl, prefix=np.zeros(0, np.int32)),
+                            keep_logits=True)
+    st = compare(ref, out, dbg, "zero-layer")
+    _log("zero-layer", st)
+    assert_typed(out, wl.kind, len(wl.allowed), wl.allowed)
+
+
+def test_tiny_filter_with_prefix(tiny, L):
+    w, orc, ctx = tiny
+    wl = make_workload("filter_tiny")
+    _log("tiny filter: set_prefix")
+    pre = ctx.set_prefix(wl.prefix)
+    _log("tiny filter: eval 64 rows")
+    out, dbg = _run(ctx, wl, pre)
+    ref = orc.eval_workload(wl, keep_logits=True)
+    st = compare(ref, out, dbg, "filter_tiny")
+    _log("filter_tiny", st)
+    assert st["exact_checked"] >= 32
+    assert_typed(out, wl.kind, 2, wl.allowed)
+    ctx.release_prefix(pre)
+
+
+def test_tiny_device_weights_match_host_weights(tiny, L):
+    w, orc, ctx = tiny
+    ctx2 = L.Context(TINY, device=0)
+    ctx2.load_weights(w.to("cuda"))
+    wl = make_workload("filter_tiny", n_rows=24)
+    p1, p2 = ctx.set_prefix(wl.prefix), ctx2.set_prefix(wl.prefix)
+    o1, d1 = _run(ctx, wl, p1)
+    o2, d2 = _run(ctx2, wl, p2)
+    assert np.array_equal(d1, d2) and np.array_equal(o1, o2)
+
+
+def test_tiny_no_prefix_and_empty_suffix(tiny, L):
+    w, orc, ctx = tiny
+    rng = np.random.default_rng(3)
+    rows = [rng.integers(0, TINY.vocab, size=int(n)).astype(np.int32)
+            for n in (1, 2, 63, 64, 65, 130, 7)]
+    offs = np.concatenate([[0], np.cumsum([len(r) for r in rows])])
+    allowed = rng.choice(TINY.vocab, 5, replace=False)
+    out, dbg = ctx.eval_rows(np.concatenate(rows), offs, KIND_ENUM, allowed, debug_logits=True)
+    ref = orc.eval_rows(None, rows, KIND_ENUM, allowed, keep_logits=True)
+    _log("no prefix", compare(ref, out, dbg, "no-prefix"))
+    # empty suffix rows take the prefix's last position
+    prefix = rng.integers(0, TINY.vocab, size=50).astype(np.int32)
+    pre = ctx.set_prefix(prefix)
+    rows2 = [np.zeros(0, np.int32), rows[0], np.zeros(0, np.int32), rows[3]]
+    offs2 = np.concatenate([[0], np.cumsum([len(r) for r in rows2])])
+    out2, dbg2 = ctx.eval_rows(np.concatenate(rows2), offs2, KIND_ENUM, allowed, prefix=pre,
+                               debug_logits=True)
+    ref2 = orc.eval_rows(prefix, rows2, KIND_ENUM, allowed, keep_logits=True)
+    _log("empty suffix", compare(ref2, out2, dbg2, "empty-suffix"))
+    assert np.array_equal(dbg2[0], dbg2[2])
+    ctx.release_prefix(pre)
+
+
+def test_tiny_join_two_level_prefix(tiny, L):
+    w, orc, ctx = tiny
+    rng = np.random.default_rng(4)
+    root_t = rng.integers(0, TINY.vocab, size=70).astype(np.int32)
+    kids_t = [rng.integers(0, TINY.vocab, size=int(n)).astype(np.int32) for n in (8, 17, 32, 9)]
+    rights = [rng.integers(0, TINY.vocab, size=int(n)).astype(np.int32) for n in (8, 20, 31, 12, 5)]
+    root = ctx.set_prefix(root_t)
+    kids = [ctx.set_prefix(k, parent=root) for k in kids_t]
+    rc = [i for i in range(4) for _ in range(5)]
+    rows = [rights[j] for i in range(4) for j in range(5)]
+    offs = np.concatenate([[0], np.cumsum([len(r) for r in rows])])
+    allowed = rng.choice(TINY.vocab, 2, replace=False)
+    out, dbg = ctx.eval_rows(np.concatenate(rows), offs, KIND_BOOL, allowed,
+                             row_prefix=[kids[i] for i in rc], debug_logits=True)
+    ref = orc.eval_rows(root_t, rows, KIND_BOOL, allowed, children=kids_t, row_child=rc,
+                        keep_logits=True)
+    _log("join", compare(ref, out, dbg, "join"))
+    ctx.release_prefix(root)  # children keep it alive
+    out2, _ = ctx.eval_rows(np.concatenate(rows), offs, KIND_BOOL, allowed,
+                            row_prefix=[kids[i] for i in rc])
+    assert np.array_equal(out2, out)
+    for k in kids:
+        ctx.release_prefix(k)
+
+
+def test_tiny_int_decode(L):
+    w = make_weights(TINY, seed=1234)
+    rng = np.random.default_rng(5)
+    digits = rng.choice(TINY.vocab, 10, replace=False).astype(np.int32)
+    eos = int(next(t for t in range(TINY.vocab) if t not in digits))
+    w.lm_head[eos] *= 3  # make EOS competitive so that numbers of every length appear
+    orc = OracleLM(w, TINY)
+    ctx = L.Context(TINY, device=0)
+    ctx.load_weights(w)
+    prefix = rng.integers(0, TINY.vocab, size=40).astype(np.int32)
+    rows = [rng.integers(0, TINY.vocab, size=int(rng.integers(1, 40))).astype(np.int32)
+            for _ in range(48)]
+    offs = np.concatenate([[0], np.cumsum([len(r) for r in rows])])
+    pre = ctx.set_prefix(prefix)
+    out, dbg = ctx.eval_rows(np.concatenate(rows), offs, KIND_INT, digits, eos=eos, max_tokens=4,
+                             prefix=pre, debug_logits=True)
+    ref = orc.eval_rows(prefix, rows, KIND_INT, digits, eos=eos, max_tokens=4, keep_logits=True)
+    forced = orc.eval_rows(prefix, rows, KIND_INT, digits, eos=eos, max_tokens=4,
+                           forced=[out["tokens"][r][: out["n_tokens"][r]] for r in range(48)],
+                           keep_logits=True)
+    st = compare(ref, out, dbg, "int", orc_forced=forced)
+    _log("int decode", st)
+    assert_typed(out, KIND_INT, 10, digits, eos, 4)
+    lens = set(out["n_tokens"].tolist())
+    assert len(lens) >= 2, lens
+
+
+def test_tiny_dedup_and_batch_invariance(tiny, L):
+    w, orc, ctx = tiny
+    wl = make_workload("filter_tiny")
+    pre = ctx.set_prefix(wl.prefix)
+    # a table with duplicated rows
+    idx = np.array([0, 5, 0, 7, 5, 5, 9, 0, 63, 9])
+    sub = wl.subset(idx)
+    o1, d1 = _run(ctx, sub, pre)
+    o2, d2 = _run(ctx, sub, pre, no_dedup=True)
+    o3, d3 = _run(ctx, sub, pre, max_batch_tokens=17)  # one row per batch
+    assert np.array_equal(o1, o2) and np.array_equal(d1, d2)
+    assert np.array_equal(o1, o3) and np.array_equal(d1, d3)
+    for a, b in [(0, 2), (0, 7), (1, 4), (1, 5), (6, 9)]:
+        assert np.array_equal(o1[a], o1[b])
+    # results do not depend on the other rows of the call
+    full, dfull = _run(ctx, wl, pre)
+    for j, r in enumerate(idx):
+        assert np.array_equal(full[r], o1[j]) and np.array_equal(dfull[r], d1[j])
+    # nor on the row order
+    perm = np.random.default_rng(6).permutation(wl.n_rows)
+    pw = wl.subset(perm)
+    op, dp = _run(ctx, pw, pre)
+    assert np.array_equal(op, full[perm]) and np.array_equal(dp, dfull[perm])
+    ctx.release_prefix(pre)

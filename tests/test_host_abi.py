@@ -1,0 +1,174 @@
+"""Host-side checks of the C-ABI library that need no GPU: it loads, exports
+every call its header declares, validates arguments and deduplicates rows."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2606_31808_amd import lmop as L
+from synth import SHAPES, make_weights
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+TINY = SHAPES["tiny"]
+
+
+def test_header_declarations_are_exported():
+    with open(os.path.join(ROOT, "include", "lmop.h")) as f:
+        hdr = f.read()
+    hdr = re.sub(r"/\*.*?\*/", "", hdr, flags=re.S)
+    declared = set(re.findall(r"\b(lmop_[a-z_]+)\s*\(", hdr))
+    assert declared == set(L.EXPORTED)
+    lib = C.CDLL(L.LIB_PATH)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    for st in (0, -1, -2, -3, -4, -5):
+        assert L._lib.lmop_status_string(st)
+
+
+def _host_ctx(shape=TINY):
+    return L.Context(shape, device=-1)
+
+
+def _expect(status, fn, *a, **k):
+    with pytest.raises(L.LmopError) as ei:
+        fn(*a, **k)
+    assert ei.value.status == status, str(ei.value)
+    return str(ei.value)
+
+
+def test_config_validation():
+    base = L.config_from_shape(TINY)
+    for field, val, st in [("head_dim", 96, L.LMOP_ERR_UNSUPPORTED),
+                           ("n_kv_heads", 3, L.LMOP_ERR_UNSUPPORTED),
+                           ("d_model", 200, L.LMOP_ERR_UNSUPPORTED),
+                           ("group_size", 64, L.LMOP_ERR_UNSUPPORTED),
+                           ("vocab", 0, L.LMOP_ERR_INVALID_ARG),
+                           ("d_ff", -1, L.LMOP_ERR_INVALID_ARG)]:
+        cfg = L.lmop_config.from_buffer_copy(base)
+        setattr(cfg, field, val)
+        msg = _expect(st, L.lmop_create, cfg, -1)
+        assert msg  # lmop_last_error(NULL) explains the failed create
+
+
+@pytest.fixture(scope="module")
+def tiny_w():
+    return make_weights(TINY, seed=5)
+
+
+def test_state_and_weight_validation(tiny_w):
+    ctx = _host_ctx()
+    _expect(L.LMOP_ERR_STATE, ctx.eval_rows, [1], [0, 1], L.LMOP_BOOL, [1, 2])
+    _expect(L.LMOP_ERR_STATE, ctx.set_prefix, [1, 2])
+    bad = make_weights(TINY, seed=5, n_layers=1)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.load_weights, bad)
+    import dataclasses
+    l0 = tiny_w.layers[0]
+    wrong = dataclasses.replace(l0, wo=l0.wq)  # same shape only because d == nq*hd here
+    tiny_w.layers[0] = dataclasses.replace(l0, w_down=l0.w_gate)
+    try:
+        _expect(L.LMOP_ERR_INVALID_ARG, ctx.load_weights, tiny_w)
+    finally:
+        tiny_w.layers[0] = l0
+    del wrong
+    ctx.load_weights(tiny_w)
+
+
+def test_eval_argument_validation(tiny_w):
+    ctx = _host_ctx()
+    ctx.load_weights(tiny_w)
+    V = TINY.vocab
+    ok = dict(kind=L.LMOP_BOOL, allowed=[3, 4])
+    # valid arguments on a host-only ctx stop at UNSUPPORTED after validation
+    _expect(L.LMOP_ERR_UNSUPPORTED, ctx.eval_rows, [1, 2, 3], [0, 2, 3], **ok)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [1, V, 3], [0, 2, 3], **ok)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [1, -1, 3], [0, 2, 3], **ok)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [1, 2, 3], [0, 3, 2], **ok)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [1, 2, 3], [1, 2, 3], **ok)
+    # a row with neither prefix nor suffix tokens
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [1, 2], [0, 2, 2], **ok)
+    # type checks
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [1], [0, 1], L.LMOP_BOOL, [3])
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [1], [0, 1], L.LMOP_ENUM, [3, 3])
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [1], [0, 1], L.LMOP_ENUM, [V + 5])
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [1], [0, 1], 7, [1, 2])
+    digits = list(range(10, 20))
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [1], [0, 1], L.LMOP_INT, digits[:9], eos=5,
+            max_tokens=4)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [1], [0, 1], L.LMOP_INT, digits, eos=12,
+            max_tokens=4)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [1], [0, 1], L.LMOP_INT, digits, eos=5,
+            max_tokens=9)
+    _expect(L.LMOP_ERR_UNSUPPORTED, ctx.eval_rows, [1], [0, 1], L.LMOP_INT, digits, eos=5,
+            max_tokens=8)
+    # too long for max_seq (4096 by default)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, np.ones(4097, np.int32), [0, 4097], **ok)
+    # zero rows is a no-op
+    out, _ = ctx.eval_rows([], [0], **ok)
+    assert len(out) == 0
+
+
+def test_prefix_lifetimes(tiny_w):
+    ctx = _host_ctx()
+    ctx.load_weights(tiny_w)
+    root = ctx.set_prefix([1, 2, 3])
+    assert L.lmop_prefix_length(root) == 3
+    child = ctx.set_prefix([4, 5], parent=root)
+    assert L.lmop_prefix_length(child) == 5
+    _expect(L.LMOP_ERR_UNSUPPORTED, ctx.set_prefix, [6], parent=child)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.set_prefix, [])
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.set_prefix, [TINY.vocab])
+    ok = dict(kind=L.LMOP_BOOL, allowed=[3, 4])
+    _expect(L.LMOP_ERR_UNSUPPORTED, ctx.eval_rows, [7], [0, 1], prefix=child, **ok)
+    # an empty suffix is fine with a prefix
+    _expect(L.LMOP_ERR_UNSUPPORTED, ctx.eval_rows, [], [0, 0], prefix=root, **ok)
+    ctx.release_prefix(root)  # parent released first: lives on while the child exists
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [7], [0, 1], prefix=root, **ok)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.release_prefix, root)
+    _expect(L.LMOP_ERR_UNSUPPORTED, ctx.eval_rows, [7], [0, 1], prefix=child, **ok)
+    ctx.release_prefix(child)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [7], [0, 1], prefix=child, **ok)
+    # prefixes of another ctx are rejected
+    other = _host_ctx()
+    other.load_weights(tiny_w)
+    p2 = other.set_prefix([1])
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [7], [0, 1], prefix=p2, **ok)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [7], [0, 1], row_prefix=[p2], **ok)
+    # reloading weights invalidates prefixes
+    p3 = ctx.set_prefix([9])
+    ctx.load_weights(tiny_w)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [7], [0, 1], prefix=p3, **ok)
+
+
+def _py_dedup(rows, keys):
+    first = {}
+    rep = []
+    for i, (r, k) in enumerate(zip(rows, keys)):
+        rep.append(first.setdefault((k, tuple(r)), i))
+    return rep, len(first)
+
+
+def test_dedup_matches_brute_force():
+    rng = np.random.default_rng(0)
+    for trial in range(20):
+        pool = [rng.integers(0, 5, size=rng.integers(0, 4)) for _ in range(12)]
+        rows = [pool[rng.integers(0, len(pool))] for _ in range(200)]
+        keys = rng.integers(0, 3, size=200) if trial % 2 else np.zeros(200, np.int64)
+        offs = np.concatenate([[0], np.cumsum([len(r) for r in rows])])
+        toks = np.concatenate(rows).astype(np.int32) if offs[-1] else np.zeros(0, np.int32)
+        rep, nu = L.lmop_dedup_rows(toks, offs, keys if trial % 2 else None)
+        want, wn = _py_dedup([r.tolist() for r in rows], keys.tolist())
+        assert nu == wn and rep.tolist() == want
+
+
+def test_dedup_rejects_bad_csr():
+    with pytest.raises(L.LmopError):
+        L.lmop_dedup_rows([1, 2], [0, 2, 1])
+    with pytest.raises(L.LmopError):
+        L.lmop_dedup_rows([1, 2], [1, 2])
+    rep, nu = L.lmop_dedup_rows([], [0])
+    assert nu == 0 and len(rep) == 0
