@@ -1,0 +1,169 @@
+"""Throughput of the LM-operator row evaluation on one MI355X.
+
+A step is one lmop_eval_rows call over the whole table: early dedup, the
+batched prefill of every row's suffix against the shared prefix's KV
+(W4A16 GEMMs, attention, norms), the constrained LM head, and (integer
+types) the decode steps.  The shared prefix is computed once before the
+timed region (lmop_set_prefix), weights and prefix KV are resident in HBM.
+
+Default workload: the 8B-shape LM filter (32 layers, d 4096, 32/8 heads,
+SwiGLU 14336, vocab 128256, int4 g32 weights; 10,000 rows, shared prefix 512,
+suffix lognormal mean 60 clipped to [8, 512]; enum over 24 tokens).
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_F16_TFLOPS = 2500.0   # MI355X dense fp16/bf16 MFMA
+PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def gemm_roofline(stats):
+    """Dominant kernel family: the W4A16 GEMMs (all four projections)."""
+    names = [n for n in stats if n.startswith("gemm_w4a16")]
+    ms = sum(stats[n]["ms"] for n in names)
+    fl = sum(stats[n]["flops"] for n in names)
+    launches = sum(stats[n]["launches"] for n in names)
+    if ms <= 0:
+        return None
+    ach = fl / (ms * 1e-3) / 1e12
+    return {"bound": "mfma", "kernel": "gemm_w4a16 (qkv, o, gate/up, down)", "achieved": ach,
+            "peak": PEAK_F16_TFLOPS, "unit": "TFLOP/s", "frac": ach / PEAK_F16_TFLOPS,
+            "traffic": None, "launches": launches, "avg_launch_ms": ms / launches,
+            "flops_per_launch": fl / launches}
+
+
+def head_roofline(stats):
+    s = stats.get("head_gemm")
+    if not s or s["ms"] <= 0:
+        return None
+    gbs = s["bytes"] / (s["ms"] * 1e-3) / 1e9
+    tfl = s["flops"] / (s["ms"] * 1e-3) / 1e12
+    return {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": gbs / PEAK_HBM_GBS, "tflops": tfl, "launches": s["launches"],
+            "avg_launch_ms": s["ms"] / s["launches"]}
+
+
+def cpu_baseline(weights, shape, wl, n_rows):
+    """The oracle (fp32, as it stands) on the first n_rows rows of the table,
+    including its pass over the shared prefix and its weight dequantisation."""
+    import numpy as np
+    from oracle import OracleLM
+    t0 = time.perf_counter()
+    orc = OracleLM(weights, shape, dtype=np.float32, cache_dequant=False)
+    sub = wl.subset(range(n_rows))
+    orc.eval_workload(sub)
+    dt = time.perf_counter() - t0
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": n_rows / dt, "unit": "rows/s", "cores": cores, "kind": "oracle",
+            "sample": f"shared prefix ({len(wl.prefix)} tokens) + first {n_rows} rows "
+                      f"({sub.n_suffix_tokens} suffix tokens), fp32 numpy, {dt:.1f} s "
+                      f"including per-layer int4 dequantisation"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="filter_8b")
+    ap.add_argument("--rows", type=int, default=None, help="truncate the table")
+    ap.add_argument("--batch-tokens", type=int, default=0)
+    ap.add_argument("--cpu-rows", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2606_31808_amd import lmop as L
+    from synth import make_weights, make_workload
+
+    wl = make_workload(args.workload, n_rows=args.rows)
+    shape = wl.shape
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    log(f"[bench] generating {shape.name} weights on the GPU")
+    t0 = time.perf_counter()
+    w = make_weights(shape, seed=1234, device=dev)
+    torch.cuda.synchronize()
+    log(f"[bench] weights {time.perf_counter() - t0:.1f} s; loading into the library")
+    ctx = L.Context(shape, device=0, stream=stream)
+    t0 = time.perf_counter()
+    ctx.load_weights(w)
+    t_load = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    root = ctx.set_prefix(wl.prefix)
+    kids = None
+    row_prefix = None
+    if wl.children is not None:
+        kids = [ctx.set_prefix(c, parent=root) for c in wl.children]
+        row_prefix = [kids[int(i)] for i in wl.row_child]
+    t_prefix = time.perf_counter() - t0
+    log(f"[bench] load {t_load:.2f} s, prefix {t_prefix * 1e3:.1f} ms")
+
+    def step():
+        out, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, eos=wl.eos,
+                               max_tokens=wl.max_tokens, prefix=None if row_prefix else root,
+                               row_prefix=row_prefix, max_batch_tokens=args.batch_tokens)
+        return out
+
+    for i in range(args.warmup):
+        t0 = time.perf_counter()
+        step()
+        log(f"[bench] warmup {i}: {time.perf_counter() - t0:.2f} s")
+    ctx.set_profiling(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        out = step()
+        log(f"[bench] step {i} done")
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    stats = ctx.kernel_stats()
+    ctx.set_profiling(False)
+    ms_step = elapsed * 1e3 / args.steps
+    rows = wl.n_rows
+    n_tok = wl.n_suffix_tokens
+    value = rows / (ms_step * 1e-3)
+    rep, n_unique = L.lmop_dedup_rows(wl.tokens, wl.offsets,
+                                      None if wl.row_child is None else wl.row_child)
+    res = {
+        "metric": "rows/sec, 8B-shape W4 LM filter (10k rows); MFMA util %, HBM GB/s",
+        "value": value, "unit": "rows/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f16 (int4 weights, fp32 accum)",
+        "data": "synthetic (seeded uniform token ids, random-init N(0,0.02) int4-g32 weights)",
+        "config": {"workload": wl.name, "model_shape": shape.name, "rows": rows,
+                   "unique_rows": n_unique, "prefix_tokens": len(wl.prefix),
+                   "suffix_tokens": n_tok, "suffix_tokens_per_s": n_tok / (ms_step * 1e-3),
+                   "batch_tokens": args.batch_tokens or 16384, "parallelism": "single GPU"},
+        "roofline": gemm_roofline(stats),
+        "head_roofline": head_roofline(stats),
+        "load_weights_s": t_load, "set_prefix_ms": t_prefix * 1e3,
+        "kernels_ms_per_step": {k: v["ms"] / args.steps for k, v in sorted(stats.items())},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] oracle CPU baseline")
+        res["cpu_baseline"] = cpu_baseline(w, shape, wl, args.cpu_rows)
+    print(json.dumps(res), flush=True)
+    ctx.close()
+
+
+if __name__ == "__main__":
+    main()
