@@ -1,26 +1,46 @@
-// W4A16 GEMM for gfx950: C = A . deq(W)^T with A fp16 [M][K], W int4 with one
-// fp16 scale per 32 input features, fp32 accumulation on MFMA 16x16x32 f16.
+// W4A16 GEMM for gfx950: C = A . deq(W)^T with A fp16 [M][K] (tokens x
+// features), W int4 [N][K] with one fp16 scale per 32 input features, fp32
+// accumulation on MFMA 16x16x32 f16.  The same body with an fp16 weight is
+// the LM head.
 //
-// Workgroup: 256 threads = 4 waves in a 2 (M) x 2 (N) grid; wave tile
-// (16*MI) x 64, workgroup tile (32*MI) x 128, K step 64 (two scale groups).
-// The A tile goes global -> registers -> LDS (padded rows); the next tile's
-// loads are issued before the current tile's MFMAs.  Each wave fetches its
-// own int4 weight words straight from global memory (the packed layout puts
-// one 16-byte word per lane per group, so a wave reads 1 KB contiguously),
-// dequantises them in registers (nibble | 0x6400 -> 1024 + u, minus 1032,
-// times the scale: exact code, one fp16 rounding of code * scale) and reuses
-// each dequantised fragment for all MI row sub-tiles.
+// Tiling.  4 waves in a 2 (M) x 2 (N) grid; a wave owns (16*MI) tokens x
+// (16*NI) output columns, the workgroup (32*MI) x (32*NI).  K advances 64
+// features (two scale groups) per step through a two-stage LDS ring filled
+// by direct global->LDS loads (global_load_lds_dwordx4, 1 KB per wave
+// instruction), so the next step's tiles stream in while the current step's
+// MFMAs run and one barrier per step suffices.
+//   A tile: 128-byte rows, 16-byte chunks XOR-swizzled by row so that the 16
+//           rows read by one fragment load hit distinct LDS banks.
+//   int4 tile: copied verbatim from the packed layout (1 KB per 64 columns x
+//           32 features: lane 16g+c holds the 8 codes of 4 columns), scales
+//           likewise (128 B per 64 columns x 32 features).
+// Each wave dequantises its weight fragments in registers (nibble | 0x6400
+// = 1024 + u in fp16, minus 1032 gives the exact code, times the fp16 scale:
+// one rounding) and reuses each for all MI token sub-tiles.
 //
-// The same kernel body, with an fp16 weight, computes the LM head; its
-// epilogue reduces every 64-column slice of logits to (max, sum exp) and
-// extracts the logits of the allowed tokens, so no [rows x vocab] matrix is
-// written unless a debug dump is requested.
+// The MFMA takes the weight fragment as its A operand and the activations
+// as its B operand, so the accumulator holds C^T: every lane owns 4
+// consecutive output columns of one token, which makes the epilogue's
+// stores 8-byte (fp16) or 16-byte (fp32) vectors.
+//
+// Workgroups are mapped to tiles XCD-aware: the hardware deals workgroups to
+// the 8 XCDs round-robin, so each XCD is given one contiguous range of
+// tiles, ordered in groups of GM token tiles so that concurrently running
+// tiles on an XCD share A and W panels in that XCD's L2.
 #include "common.h"
 #include "kernels.h"
 
 namespace lmop {
 
 namespace {
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef __attribute__((address_space(1))) void* gbl_ptr_t;
+
+// 16 bytes per lane from global address g to LDS at base + lane*16
+LMOP_DEVICE void g2l16(const void* g, void* lds_base) {
+  __builtin_amdgcn_global_load_lds((gbl_ptr_t)g, (lds_ptr_t)lds_base, 16, 0, 0);
+}
 
 LMOP_DEVICE f16x8 dequant8(uint32_t w, f16 s) {
   const uint32_t kMask = 0x000F000Fu, kMagic = 0x64006400u;
@@ -35,220 +55,274 @@ LMOP_DEVICE f16x8 dequant8(uint32_t w, f16 s) {
 
 LMOP_DEVICE float silu(float g) { return g / (1.0f + __expf(-g)); }
 
-constexpr int BN = 128;
-constexpr int BK = 64;
-constexpr int LDS_ROW = BK + 8;  // halves; padding spreads rows over LDS banks
+// chunk swizzle of a 128-byte LDS row: distinct for any 8 rows aligned at 8
+// and, per row parity, for any 16 rows aligned at 16
+LMOP_DEVICE int swz(int row) { return (row ^ (row >> 3)) & 7; }
 
-template <int MI, bool INT4, int EPI>
+constexpr int BK = 64;
+constexpr int GM = 8;  // token tiles per L2 group
+
+template <int MI, int NI, bool INT4>
+struct Cfg {
+  static constexpr int BM = 32 * MI;
+  static constexpr int BN = 32 * NI;
+  static constexpr int A_BYTES = BM * 128;
+  static constexpr int B_BYTES = INT4 ? BN * 32 : BN * 128;
+  static constexpr int S_BYTES = INT4 ? (BN * 4 > 1024 ? BN * 4 : 1024) : 0;
+  static constexpr int STAGE = A_BYTES + B_BYTES + S_BYTES;
+  static constexpr int LDS = 2 * STAGE;
+};
+
+template <int MI, int NI, bool INT4, int EPI>
 __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs p) {
-  constexpr int BM = 32 * MI;
-  constexpr int ACH = BM * (BK / 8) / 256;  // 16-byte A chunks per thread per K step
-  __shared__ f16 sA[BM * LDS_ROW];
+  using C = Cfg<MI, NI, INT4>;
+  constexpr int BM = C::BM, BN = C::BN;
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int g = lane >> 4, c = lane & 15;
-  const int ntn = (p.N + BN - 1) / BN;
-  const int mt = blockIdx.x / ntn, nt = blockIdx.x - mt * ntn;
+
+  // ---- XCD-aware tile mapping
+  const int ntm = (p.M + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
+  const int total = ntm * ntn;
+  const int b = blockIdx.x;
+  const int xcd = b & 7, j = b >> 3;
+  const int per = total >> 3, rem = total & 7;
+  const int logical = xcd * per + (xcd < rem ? xcd : rem) + j;
+  const int grp = logical / (GM * ntn);
+  const int within = logical - grp * GM * ntn;
+  const int gsz = (ntm - grp * GM) < GM ? (ntm - grp * GM) : GM;
+  const int mt = grp * GM + within % gsz;
+  const int nt = within / gsz;
   const int m0 = mt * BM, n0 = nt * BN;
+
   const int KT = p.K / BK;
   const int KG = p.K / 32;
   const f16* A = (const f16*)p.A;
 
-  f32x4 acc[MI][4];
+  // ---- global -> LDS issue of one K step into stage st
+  auto issue = [&](int st, int kt) {
+    char* sA = smem + st * C::STAGE;
+    char* sB = sA + C::A_BYTES;
+    char* sS = sB + C::B_BYTES;
+    // A: BM/8 instructions of 8 rows each
 #pragma unroll
-  for (int i = 0; i < MI; ++i)
-#pragma unroll
-    for (int f = 0; f < 4; ++f) acc[i][f] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  f16x8 areg[ACH];
-  auto loadA = [&](int kt) {
-#pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int ch = tid + i * 256, r = ch >> 3, cc = (ch & 7) * 8;
-      const int gm = m0 + r;
-      if (gm < p.M)
-        areg[i] = *(const f16x8*)(A + (size_t)gm * p.lda + kt * BK + cc);
-      else
-        areg[i] = f16x8{0, 0, 0, 0, 0, 0, 0, 0};
+    for (int q = wave; q < BM / 8; q += 4) {
+      const int r = q * 8 + (lane >> 3);
+      const int chunk = (lane & 7) ^ swz(r);
+      int gm = m0 + r;
+      gm = gm < p.M ? gm : p.M - 1;
+      g2l16(A + (size_t)gm * p.lda + kt * BK + chunk * 8, sA + q * 1024);
     }
-  };
-  auto storeA = [&]() {
+    if constexpr (INT4) {
+      const size_t nb0 = (size_t)(n0 >> 6);
 #pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int ch = tid + i * 256, r = ch >> 3, cc = (ch & 7) * 8;
-      *(f16x8*)(sA + r * LDS_ROW + cc) = areg[i];
-    }
-  };
-
-  // weight fragments of one K step (two groups)
-  uint4 bq[2];
-  uint2 bsc[2];
-  f16x8 bh[2][4];
-  const int nb = (n0 >> 6) + wn;  // global 64-column block of this wave
-  auto loadB = [&](int kt) {
+      for (int q = wave; q < BN / 32; q += 4) {  // (64-col block, group) pairs
+        const size_t blk = (nb0 + (q >> 1)) * KG + kt * 2 + (q & 1);
+        g2l16((const char*)p.bq + blk * 1024 + lane * 16, sB + q * 1024);
+      }
+      if (wave == 0) {
+        int pi = lane >> 3;  // pair index
+        if (pi >= BN / 32) pi = BN / 32 - 1;  // lanes past the tile fill the pad
+        const size_t blk = (nb0 + (pi >> 1)) * KG + kt * 2 + (pi & 1);
+        g2l16((const char*)p.bs + blk * 128 + (lane & 7) * 16, sS);
+      }
+    } else {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int kg = kt * 2 + j;
-      if constexpr (INT4) {
-        const size_t blk = (size_t)nb * KG + kg;
-        bq[j] = ((const uint4*)p.bq)[blk * 64 + lane];
-        bsc[j] = ((const uint2*)p.bs)[blk * 16 + c];
-      } else {
-#pragma unroll
-        for (int f = 0; f < 4; ++f) {
-          int n = n0 + wn * 64 + f * 16 + c;
-          n = n < p.N ? n : p.N - 1;  // clamped; masked in the epilogue
-          bh[j][f] = *(const f16x8*)((const f16*)p.bh + (size_t)n * p.ldb + kg * 32 + g * 8);
-        }
+      for (int q = wave; q < BN / 8; q += 4) {
+        const int r = q * 8 + (lane >> 3);
+        const int chunk = (lane & 7) ^ swz(r);
+        int gn = n0 + r;
+        gn = gn < p.N ? gn : p.N - 1;
+        g2l16((const f16*)p.bh + (size_t)gn * p.ldb + kt * BK + chunk * 8, sB + q * 1024);
       }
     }
   };
 
-  loadA(0);
-  loadB(0);
+  f32x4 acc[NI][MI];
+#pragma unroll
+  for (int f = 0; f < NI; ++f)
+#pragma unroll
+    for (int i = 0; i < MI; ++i) acc[f][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  issue(0, 0);
   for (int kt = 0; kt < KT; ++kt) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    storeA();
-    __syncthreads();
-    uint4 cq[2] = {bq[0], bq[1]};
-    uint2 cs[2] = {bsc[0], bsc[1]};
-    f16x8 ch[2][4];
-    if constexpr (!INT4) {
+    if (kt + 1 < KT) issue((kt + 1) & 1, kt + 1);
+    const char* sA = smem + (kt & 1) * C::STAGE;
+    const char* sB = sA + C::A_BYTES;
+    const char* sS = sB + C::B_BYTES;
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int f = 0; f < 4; ++f) ch[j][f] = bh[j][f];
-    }
-    if (kt + 1 < KT) {
-      loadA(kt + 1);
-      loadB(kt + 1);
-    }
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      f16x8 b[4];
-      if constexpr (INT4) {
-        const f16x4 s4 = __builtin_bit_cast(f16x4, cs[j]);
-        b[0] = dequant8(cq[j].x, s4.x);
-        b[1] = dequant8(cq[j].y, s4.y);
-        b[2] = dequant8(cq[j].z, s4.z);
-        b[3] = dequant8(cq[j].w, s4.w);
-      } else {
-#pragma unroll
-        for (int f = 0; f < 4; ++f) b[f] = ch[j][f];
-      }
+    for (int kk = 0; kk < 2; ++kk) {
+      f16x8 a[MI];
 #pragma unroll
       for (int i = 0; i < MI; ++i) {
-        const f16x8 a =
-            *(const f16x8*)(sA + (wm * 16 * MI + 16 * i + c) * LDS_ROW + j * 32 + g * 8);
+        const int r = wm * 16 * MI + 16 * i + c;
+        a[i] = *(const f16x8*)(sA + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
+      }
 #pragma unroll
-        for (int f = 0; f < 4; ++f) acc[i][f] = mfma16x16x32(a, b[f], acc[i][f]);
+      for (int bl = 0; bl < NI / 4; ++bl) {
+        f16x8 w[4];
+        if constexpr (INT4) {
+          const int q = (wn * (NI / 4) + bl) * 2 + kk;
+          const uint4 codes = *(const uint4*)(sB + q * 1024 + lane * 16);
+          const f16x4 s4 = *(const f16x4*)(sS + q * 128 + c * 8);
+          w[0] = dequant8(codes.x, s4.x);
+          w[1] = dequant8(codes.y, s4.y);
+          w[2] = dequant8(codes.z, s4.z);
+          w[3] = dequant8(codes.w, s4.w);
+        } else {
+#pragma unroll
+          for (int f = 0; f < 4; ++f) {
+            const int r = wn * 16 * NI + 16 * (bl * 4 + f) + c;
+            w[f] = *(const f16x8*)(sB + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
+          }
+        }
+#pragma unroll
+        for (int f = 0; f < 4; ++f)
+#pragma unroll
+          for (int i = 0; i < MI; ++i)
+            acc[bl * 4 + f][i] = mfma16x16x32(w[f], a[i], acc[bl * 4 + f][i]);
       }
     }
   }
 
   // ------------------------------------------------------------ epilogue
-  const int row_base = m0 + wm * 16 * MI + 4 * g;
+  // acc[f][i][r] = C[m][n], m = m0 + wm*16*MI + 16i + c,
+  //                        n = n0 + wn*16*NI + 16f + 4g + r
+  const int mrow = m0 + wm * 16 * MI + c;
+  const int ncol = n0 + wn * 16 * NI + 4 * g;
   if constexpr (EPI == EPI_STORE_F16) {
-    f16* C = (f16*)p.C;
-#pragma unroll
-    for (int i = 0; i < MI; ++i)
-#pragma unroll
-      for (int f = 0; f < 4; ++f) {
-        const int col = n0 + wn * 64 + 16 * f + c;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = row_base + 16 * i + r;
-          if (row < p.M && col < p.n_out) C[(size_t)row * p.ldc + col] = (f16)acc[i][f][r];
-        }
-      }
-  } else if constexpr (EPI == EPI_ADD_F32) {
-#pragma unroll
-    for (int i = 0; i < MI; ++i)
-#pragma unroll
-      for (int f = 0; f < 4; ++f) {
-        const int col = n0 + wn * 64 + 16 * f + c;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = row_base + 16 * i + r;
-          if (row < p.M && col < p.n_out) p.X[(size_t)row * p.ldx + col] += acc[i][f][r];
-        }
-      }
-  } else if constexpr (EPI == EPI_SWIGLU) {
-    // block nb holds gate columns nb*32 + 0..31 in f = 0,1 and the matching up
-    // columns in f = 2,3
-    f16* C = (f16*)p.C;
-#pragma unroll
-    for (int i = 0; i < MI; ++i)
-#pragma unroll
-      for (int f = 0; f < 2; ++f) {
-        const int col = nb * 32 + 16 * f + c;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = row_base + 16 * i + r;
-          if (row < p.M && col < p.n_out)
-            C[(size_t)row * p.ldc + col] = (f16)(silu(acc[i][f][r]) * acc[i][f + 2][r]);
-        }
-      }
-  } else {  // EPI_HEAD
-    const int n_chunks = (p.N + 63) / 64;
+    f16* Cp = (f16*)p.C;
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
+      const int m = mrow + 16 * i;
+      if (m >= p.M) continue;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = row_base + 16 * i + r;
-        float mx = -INFINITY;
-#pragma unroll
-        for (int f = 0; f < 4; ++f) {
-          const int col = n0 + wn * 64 + 16 * f + c;
-          if (col < p.N) mx = fmaxf(mx, acc[i][f][r]);
+      for (int f = 0; f < NI; ++f) {
+        const int n = ncol + 16 * f;
+        if (n < p.n_out) {
+          const f32x4 v = acc[f][i];
+          *(f16x4*)(Cp + (size_t)m * p.ldc + n) = f16x4{(f16)v[0], (f16)v[1], (f16)v[2], (f16)v[3]};
         }
-        // lanes 16g .. 16g+15 hold the 64 columns of this row
+      }
+    }
+  } else if constexpr (EPI == EPI_ADD_F32) {
 #pragma unroll
-        for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, shfl_xor(mx, o));
-        float sm = 0.f;
+    for (int i = 0; i < MI; ++i) {
+      const int m = mrow + 16 * i;
+      if (m >= p.M) continue;
 #pragma unroll
-        for (int f = 0; f < 4; ++f) {
-          const int col = n0 + wn * 64 + 16 * f + c;
-          if (col < p.N) {
-            const float z = acc[i][f][r];
-            sm += __expf(z - mx);
-            if (row < p.M) {
-              const int si = p.sel[col];
-              if (si >= 0) p.zsel[(size_t)row * p.n_sel + si] = z;
-              if (p.dump) p.dump[(size_t)row * p.ld_dump + col] = z;
-            }
+      for (int f = 0; f < NI; ++f) {
+        const int n = ncol + 16 * f;
+        if (n < p.n_out) {
+          float4* xp = (float4*)(p.X + (size_t)m * p.ldx + n);
+          float4 x = *xp;
+          const f32x4 v = acc[f][i];
+          x.x += v[0];
+          x.y += v[1];
+          x.z += v[2];
+          x.w += v[3];
+          *xp = x;
+        }
+      }
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    // 64-column block nb holds gate columns nb*32 + 0..31 (sub-tiles 0, 1)
+    // and the matching up columns (sub-tiles 2, 3)
+    f16* Cp = (f16*)p.C;
+    const int nb0 = (n0 + wn * 16 * NI) >> 6;
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+      const int m = mrow + 16 * i;
+      if (m >= p.M) continue;
+#pragma unroll
+      for (int bl = 0; bl < NI / 4; ++bl)
+#pragma unroll
+        for (int f = 0; f < 2; ++f) {
+          const int col = (nb0 + bl) * 32 + 16 * f + 4 * g;
+          if (col < p.n_out) {
+            const f32x4 gt = acc[bl * 4 + f][i], up = acc[bl * 4 + f + 2][i];
+            *(f16x4*)(Cp + (size_t)m * p.ldc + col) =
+                f16x4{(f16)(silu(gt[0]) * up[0]), (f16)(silu(gt[1]) * up[1]),
+                      (f16)(silu(gt[2]) * up[2]), (f16)(silu(gt[3]) * up[3])};
           }
         }
+    }
+  } else {  // EPI_HEAD: per token and 64-column block: (max, sum exp), allowed logits
+    const int n_chunks = (p.N + 63) / 64;
+    const int nb0 = (n0 + wn * 16 * NI) >> 6;
 #pragma unroll
-        for (int o = 1; o < 16; o <<= 1) sm += shfl_xor(sm, o);
-        if (c == 0 && row < p.M && nb < n_chunks)
-          p.part[(size_t)row * n_chunks + nb] = make_float2(mx, sm);
+    for (int i = 0; i < MI; ++i) {
+      const int m = mrow + 16 * i;
+#pragma unroll
+      for (int bl = 0; bl < NI / 4; ++bl) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int f = 0; f < 4; ++f)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int n = ncol + 16 * (bl * 4 + f) + r;
+            if (n < p.N) mx = fmaxf(mx, acc[bl * 4 + f][i][r]);
+          }
+        mx = fmaxf(mx, shfl_xor(mx, 16));
+        mx = fmaxf(mx, shfl_xor(mx, 32));
+        float sm = 0.f;
+#pragma unroll
+        for (int f = 0; f < 4; ++f)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int n = ncol + 16 * (bl * 4 + f) + r;
+            if (n < p.N) {
+              const float z = acc[bl * 4 + f][i][r];
+              sm += __expf(z - mx);
+              if (m < p.M) {
+                const int si = p.sel[n];
+                if (si >= 0) p.zsel[(size_t)m * p.n_sel + si] = z;
+                if (p.dump) p.dump[(size_t)m * p.ld_dump + n] = z;
+              }
+            }
+          }
+        sm += shfl_xor(sm, 16);
+        sm += shfl_xor(sm, 32);
+        if (g == 0 && m < p.M && nb0 + bl < n_chunks)
+          p.part[(size_t)m * n_chunks + nb0 + bl] = make_float2(mx, sm);
       }
     }
   }
 }
 
-template <int MI, bool INT4, int EPI>
-hipError_t launch_mi(hipStream_t s, const GemmArgs& a) {
-  constexpr int BM = 32 * MI;
-  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+template <int MI, int NI, bool INT4, int EPI>
+hipError_t launch_cfg(hipStream_t s, const GemmArgs& a) {
+  using C = Cfg<MI, NI, INT4>;
+  const int tiles = ((a.M + C::BM - 1) / C::BM) * ((a.N + C::BN - 1) / C::BN);
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_kernel<MI, INT4, EPI>), dim3(tiles), dim3(256), 0, s, a);
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<MI, NI, INT4, EPI>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL((gemm_kernel<MI, NI, INT4, EPI>), dim3(tiles), dim3(256), C::LDS, s, a);
   return hipGetLastError();
 }
 
 template <bool INT4, int EPI>
 hipError_t launch_epi(hipStream_t s, const GemmArgs& a) {
-  if (a.M > 1024) return launch_mi<8, INT4, EPI>(s, a);
-  if (a.M > 256) return launch_mi<4, INT4, EPI>(s, a);
-  return launch_mi<2, INT4, EPI>(s, a);
+  // the head's epilogue does not fit the register file next to a 256x256 tile
+  if (INT4 && a.M > 1024) return launch_cfg<8, 8, true, EPI>(s, a);
+  if (a.M > 128) return launch_cfg<4, 8, INT4, EPI>(s, a);
+  return launch_cfg<2, 4, INT4, EPI>(s, a);
 }
 
 }  // namespace
 
 hipError_t launch_gemm_w4(hipStream_t s, const GemmArgs& a, int epi) {
-  if (a.K % BK != 0 || a.N % BN != 0) return hipErrorInvalidValue;
+  // the packed weight is padded to 256 columns so every tile shape divides it
+  if (a.K % BK != 0 || a.N % 256 != 0) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_STORE_F16: return launch_epi<true, EPI_STORE_F16>(s, a);
     case EPI_ADD_F32: return launch_epi<true, EPI_ADD_F32>(s, a);

@@ -13,7 +13,7 @@ typedef uint16_t half_bits;  // fp16 storage as seen from host code
 //          of column nb*64 + 16f + c, features kg*32 + 8g .. +7, biased by +8,
 //          nibble p = feature 2p (p < 4) / 2(p-4)+1 (p >= 4)
 //   spack: fp16 [Np/64][KG][16 c][4 f]
-// Np is a multiple of 128, Kp (= 32*KG) a multiple of 64.
+// Np is a multiple of 256, Kp (= 32*KG) a multiple of 64.
 struct PackedW4 {
   uint32_t* qpack = nullptr;
   half_bits* spack = nullptr;

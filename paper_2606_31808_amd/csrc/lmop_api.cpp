@@ -786,18 +786,18 @@ lmop_status lmop_load_weights(lmop_ctx* ctx, const lmop_weights* w) {
     {  // fused q | k | v
       const lmop_qmat* s[3] = {&L.wq, &L.wk, &L.wv};
       const int rows[3] = {nq, nkv, nkv};
-      auto m = concat_map(rows, 3, round_up(ctx->qkv_n, 128));
+      auto m = concat_map(rows, 3, round_up(ctx->qkv_n, 256));
       LMOP_TRY(pack(ctx, s, 3, m, ctx->qkv_n, d, od, &D.qkv));
     }
     {
       const lmop_qmat* s[1] = {&L.wo};
       const int rows[1] = {d};
-      LMOP_TRY(pack(ctx, s, 1, concat_map(rows, 1, round_up(d, 128)), d, nq, od, &D.o));
+      LMOP_TRY(pack(ctx, s, 1, concat_map(rows, 1, round_up(d, 256)), d, nq, od, &D.o));
     }
     {  // gate/up interleaved in blocks of 32: block b = [gate 32b..32b+31 | up 32b..32b+31]
       const lmop_qmat* s[2] = {&L.w_gate, &L.w_up};
       const int nblk = round_up(F, 32) / 32;
-      std::vector<int32_t> m(round_up(nblk * 64, 128), -1);
+      std::vector<int32_t> m(round_up(nblk * 64, 256), -1);
       for (int b = 0; b < nblk; ++b)
         for (int i = 0; i < 32; ++i) {
           const int r = b * 32 + i;
@@ -811,7 +811,7 @@ lmop_status lmop_load_weights(lmop_ctx* ctx, const lmop_weights* w) {
     {
       const lmop_qmat* s[1] = {&L.w_down};
       const int rows[1] = {d};
-      LMOP_TRY(pack(ctx, s, 1, concat_map(rows, 1, round_up(d, 128)), d, F, od, &D.down));
+      LMOP_TRY(pack(ctx, s, 1, concat_map(rows, 1, round_up(d, 256)), d, F, od, &D.down));
     }
   }
   LMOP_TRY(sync(ctx));
