@@ -3,20 +3,21 @@
 // accumulation on MFMA 16x16x32 f16.  The same body with an fp16 weight is
 // the LM head.
 //
-// Tiling.  4 waves in a 2 (M) x 2 (N) grid; a wave owns (16*MI) tokens x
-// (16*NI) output columns, the workgroup (32*MI) x (32*NI).  K advances 64
-// features (two scale groups) per step through a two-stage LDS ring filled
-// by direct global->LDS loads (global_load_lds_dwordx4, 1 KB per wave
-// instruction), so the next step's tiles stream in while the current step's
-// MFMAs run and one barrier per step suffices.
+// Tiling.  4 waves side by side along N; a wave owns all (16*MI) tokens of
+// the tile and 64 output columns, the workgroup (16*MI) x 256.  K advances
+// 64 features (two scale groups) per step through a three-stage LDS ring
+// filled by direct global->LDS loads (global_load_lds_dwordx4, 1 KB per wave
+// instruction): two steps' tiles stream in while the current step's MFMAs
+// run, and one barrier per step suffices.
 //   A tile: 128-byte rows, 16-byte chunks XOR-swizzled by row so that the 16
 //           rows read by one fragment load hit distinct LDS banks.
 //   int4 tile: copied verbatim from the packed layout (1 KB per 64 columns x
 //           32 features: lane 16g+c holds the 8 codes of 4 columns), scales
 //           likewise (128 B per 64 columns x 32 features).
-// Each wave dequantises its weight fragments in registers (nibble | 0x6400
-// = 1024 + u in fp16, minus 1032 gives the exact code, times the fp16 scale:
-// one rounding) and reuses each for all MI token sub-tiles.
+// Each wave dequantises its own weight fragments in registers (nibble |
+// 0x6400 = 1024 + u in fp16, minus 1032 gives the exact code, times the fp16
+// scale: one rounding), once per workgroup, and reuses each for all MI token
+// sub-tiles.
 //
 // The MFMA takes the weight fragment as its A operand and the activations
 // as its B operand, so the accumulator holds C^T: every lane owns 4
@@ -42,45 +43,72 @@ LMOP_DEVICE void g2l16(const void* g, void* lds_base) {
   __builtin_amdgcn_global_load_lds((gbl_ptr_t)g, (lds_ptr_t)lds_base, 16, 0, 0);
 }
 
+// (x & 0x000F000F) | 0x64006400 in one VALU op
+LMOP_DEVICE uint32_t and_or(uint32_t x, uint32_t mask, uint32_t magic) {
+  uint32_t r;
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(mask), "v"(magic));
+  return r;
+}
+
 LMOP_DEVICE f16x8 dequant8(uint32_t w, f16 s) {
   const uint32_t kMask = 0x000F000Fu, kMagic = 0x64006400u;
   const f16x2 bias = {(f16)1032.0f, (f16)1032.0f};
   const f16x2 s2 = {s, s};
-  f16x2 h0 = (__builtin_bit_cast(f16x2, (w & kMask) | kMagic) - bias) * s2;
-  f16x2 h1 = (__builtin_bit_cast(f16x2, ((w >> 4) & kMask) | kMagic) - bias) * s2;
-  f16x2 h2 = (__builtin_bit_cast(f16x2, ((w >> 8) & kMask) | kMagic) - bias) * s2;
-  f16x2 h3 = (__builtin_bit_cast(f16x2, ((w >> 12) & kMask) | kMagic) - bias) * s2;
+  f16x2 h0 = (__builtin_bit_cast(f16x2, and_or(w, kMask, kMagic)) - bias) * s2;
+  f16x2 h1 = (__builtin_bit_cast(f16x2, and_or(w >> 4, kMask, kMagic)) - bias) * s2;
+  f16x2 h2 = (__builtin_bit_cast(f16x2, and_or(w >> 8, kMask, kMagic)) - bias) * s2;
+  f16x2 h3 = (__builtin_bit_cast(f16x2, and_or(w >> 12, kMask, kMagic)) - bias) * s2;
   return f16x8{h0.x, h0.y, h1.x, h1.y, h2.x, h2.y, h3.x, h3.y};
 }
 
-LMOP_DEVICE float silu(float g) { return g / (1.0f + __expf(-g)); }
+LMOP_DEVICE float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
 
 // chunk swizzle of a 128-byte LDS row: distinct for any 8 rows aligned at 8
 // and, per row parity, for any 16 rows aligned at 16
 LMOP_DEVICE int swz(int row) { return (row ^ (row >> 3)) & 7; }
 
-constexpr int BK = 64;
-constexpr int GM = 8;  // token tiles per L2 group
+// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding)
+template <int N>
+LMOP_DEVICE void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
 
-template <int MI, int NI, bool INT4>
+constexpr int BK = 64;
+constexpr int BN = 256;    // 4 waves x 64 columns
+constexpr int GM = 8;      // token tiles per L2 group
+constexpr int NSTAGE = 3;  // LDS ring depth
+
+template <int MI, bool INT4>
 struct Cfg {
-  static constexpr int BM = 32 * MI;
-  static constexpr int BN = 32 * NI;
+  static constexpr int BM = 16 * MI;
   static constexpr int A_BYTES = BM * 128;
   static constexpr int B_BYTES = INT4 ? BN * 32 : BN * 128;
-  static constexpr int S_BYTES = INT4 ? (BN * 4 > 1024 ? BN * 4 : 1024) : 0;
+  static constexpr int S_BYTES = INT4 ? 1024 : 0;
   static constexpr int STAGE = A_BYTES + B_BYTES + S_BYTES;
-  static constexpr int LDS = 2 * STAGE;
+  static constexpr int LDS = NSTAGE * STAGE;
+  // global->LDS instructions one wave issues per K step (A rows, weight tile, scales)
+  static constexpr int A_LOADS = (BM / 8 + 3) / 4;
+  static constexpr int B_LOADS = INT4 ? BN / 32 / 4 : BN / 8 / 4;
+  static constexpr int LOADS = A_LOADS + B_LOADS + (INT4 ? 1 : 0);
 };
 
-template <int MI, int NI, bool INT4, int EPI>
-__global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs p) {
-  using C = Cfg<MI, NI, INT4>;
-  constexpr int BM = C::BM, BN = C::BN;
+// Workgroup: 4 waves side by side along N; wave w owns all BM tokens of the
+// tile and columns n0 + 64w .. +63, so every weight fragment is dequantised
+// once per workgroup and feeds MI MFMAs.
+// 16-token sub-tiles per wave -> workgroups per CU the kernel is built for
+template <int MI>
+struct Occ {
+  static constexpr int value = MI >= 16 ? 1 : 2;
+};
+
+template <int MI, bool INT4, int EPI>
+__global__ __launch_bounds__(256, Occ<MI>::value) void gemm_kernel(const GemmArgs p) {
+  using C = Cfg<MI, INT4>;
+  constexpr int BM = C::BM;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
   const int g = lane >> 4, c = lane & 15;
 
   // ---- XCD-aware tile mapping
@@ -101,14 +129,16 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs p) {
   const int KG = p.K / 32;
   const f16* A = (const f16*)p.A;
 
-  // ---- global -> LDS issue of one K step into stage st
+  // ---- global -> LDS issue of one K step into stage st; every wave issues
+  // exactly C::LOADS instructions, which the vmcnt waits below rely on
   auto issue = [&](int st, int kt) {
     char* sA = smem + st * C::STAGE;
     char* sB = sA + C::A_BYTES;
     char* sS = sB + C::B_BYTES;
-    // A: BM/8 instructions of 8 rows each
 #pragma unroll
-    for (int q = wave; q < BM / 8; q += 4) {
+    for (int i = 0; i < C::A_LOADS; ++i) {
+      int q = wave + 4 * i;  // 8 rows per instruction
+      if (q >= BM / 8) q = BM / 8 - 1;  // surplus waves repeat the last rows
       const int r = q * 8 + (lane >> 3);
       const int chunk = (lane & 7) ^ swz(r);
       int gm = m0 + r;
@@ -118,19 +148,20 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs p) {
     if constexpr (INT4) {
       const size_t nb0 = (size_t)(n0 >> 6);
 #pragma unroll
-      for (int q = wave; q < BN / 32; q += 4) {  // (64-col block, group) pairs
+      for (int i = 0; i < C::B_LOADS; ++i) {  // (64-column block, group) pairs
+        const int q = wave + 4 * i;
         const size_t blk = (nb0 + (q >> 1)) * KG + kt * 2 + (q & 1);
         g2l16((const char*)p.bq + blk * 1024 + lane * 16, sB + q * 1024);
       }
-      if (wave == 0) {
-        int pi = lane >> 3;  // pair index
-        if (pi >= BN / 32) pi = BN / 32 - 1;  // lanes past the tile fill the pad
+      {  // scales: 8 pairs x 128 B = one 1 KB instruction, spread over the waves
+        const int pi = lane >> 3;
         const size_t blk = (nb0 + (pi >> 1)) * KG + kt * 2 + (pi & 1);
-        g2l16((const char*)p.bs + blk * 128 + (lane & 7) * 16, sS);
+        if ((lane >> 4) == wave) g2l16((const char*)p.bs + blk * 128 + (lane & 7) * 16, sS);
       }
     } else {
 #pragma unroll
-      for (int q = wave; q < BN / 8; q += 4) {
+      for (int i = 0; i < C::B_LOADS; ++i) {
+        const int q = wave + 4 * i;
         const int r = q * 8 + (lane >> 3);
         const int chunk = (lane & 7) ^ swz(r);
         int gn = n0 + r;
@@ -140,60 +171,57 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs p) {
     }
   };
 
-  f32x4 acc[NI][MI];
+  f32x4 acc[4][MI];
 #pragma unroll
-  for (int f = 0; f < NI; ++f)
+  for (int f = 0; f < 4; ++f)
 #pragma unroll
     for (int i = 0; i < MI; ++i) acc[f][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   issue(0, 0);
+  if (KT > 1) issue(1, 1);
   for (int kt = 0; kt < KT; ++kt) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // this step's stage is complete once at most the next step's loads are in flight
+    if (kt + 1 < KT)
+      wait_vmcnt<C::LOADS>();
+    else
+      wait_vmcnt<0>();
     __syncthreads();
-    if (kt + 1 < KT) issue((kt + 1) & 1, kt + 1);
-    const char* sA = smem + (kt & 1) * C::STAGE;
+    if (kt + 2 < KT) issue((kt + 2) % NSTAGE, kt + 2);
+    const char* sA = smem + (kt % NSTAGE) * C::STAGE;
     const char* sB = sA + C::A_BYTES;
     const char* sS = sB + C::B_BYTES;
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      f16x8 a[MI];
+      f16x8 w[4];
+      if constexpr (INT4) {
+        const int q = wave * 2 + kk;
+        const uint4 codes = *(const uint4*)(sB + q * 1024 + lane * 16);
+        const f16x4 s4 = *(const f16x4*)(sS + q * 128 + c * 8);
+        w[0] = dequant8(codes.x, s4.x);
+        w[1] = dequant8(codes.y, s4.y);
+        w[2] = dequant8(codes.z, s4.z);
+        w[3] = dequant8(codes.w, s4.w);
+      } else {
 #pragma unroll
-      for (int i = 0; i < MI; ++i) {
-        const int r = wm * 16 * MI + 16 * i + c;
-        a[i] = *(const f16x8*)(sA + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
+        for (int f = 0; f < 4; ++f) {
+          const int r = wave * 64 + 16 * f + c;
+          w[f] = *(const f16x8*)(sB + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
+        }
       }
 #pragma unroll
-      for (int bl = 0; bl < NI / 4; ++bl) {
-        f16x8 w[4];
-        if constexpr (INT4) {
-          const int q = (wn * (NI / 4) + bl) * 2 + kk;
-          const uint4 codes = *(const uint4*)(sB + q * 1024 + lane * 16);
-          const f16x4 s4 = *(const f16x4*)(sS + q * 128 + c * 8);
-          w[0] = dequant8(codes.x, s4.x);
-          w[1] = dequant8(codes.y, s4.y);
-          w[2] = dequant8(codes.z, s4.z);
-          w[3] = dequant8(codes.w, s4.w);
-        } else {
+      for (int i = 0; i < MI; ++i) {
+        const int r = 16 * i + c;
+        const f16x8 a = *(const f16x8*)(sA + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
 #pragma unroll
-          for (int f = 0; f < 4; ++f) {
-            const int r = wn * 16 * NI + 16 * (bl * 4 + f) + c;
-            w[f] = *(const f16x8*)(sB + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
-          }
-        }
-#pragma unroll
-        for (int f = 0; f < 4; ++f)
-#pragma unroll
-          for (int i = 0; i < MI; ++i)
-            acc[bl * 4 + f][i] = mfma16x16x32(w[f], a[i], acc[bl * 4 + f][i]);
+        for (int f = 0; f < 4; ++f) acc[f][i] = mfma16x16x32(w[f], a, acc[f][i]);
       }
     }
   }
 
   // ------------------------------------------------------------ epilogue
-  // acc[f][i][r] = C[m][n], m = m0 + wm*16*MI + 16i + c,
-  //                        n = n0 + wn*16*NI + 16f + 4g + r
-  const int mrow = m0 + wm * 16 * MI + c;
-  const int ncol = n0 + wn * 16 * NI + 4 * g;
+  // acc[f][i][r] = C[m][n], m = m0 + 16i + c, n = n0 + 64*wave + 16f + 4g + r
+  const int mrow = m0 + c;
+  const int ncol = n0 + wave * 64 + 4 * g;
   if constexpr (EPI == EPI_STORE_F16) {
     f16* Cp = (f16*)p.C;
 #pragma unroll
@@ -201,7 +229,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs p) {
       const int m = mrow + 16 * i;
       if (m >= p.M) continue;
 #pragma unroll
-      for (int f = 0; f < NI; ++f) {
+      for (int f = 0; f < 4; ++f) {
         const int n = ncol + 16 * f;
         if (n < p.n_out) {
           const f32x4 v = acc[f][i];
@@ -215,7 +243,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs p) {
       const int m = mrow + 16 * i;
       if (m >= p.M) continue;
 #pragma unroll
-      for (int f = 0; f < NI; ++f) {
+      for (int f = 0; f < 4; ++f) {
         const int n = ncol + 16 * f;
         if (n < p.n_out) {
           float4* xp = (float4*)(p.X + (size_t)m * p.ldx + n);
@@ -230,92 +258,85 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs p) {
       }
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
-    // 64-column block nb holds gate columns nb*32 + 0..31 (sub-tiles 0, 1)
-    // and the matching up columns (sub-tiles 2, 3)
+    // the wave's 64-column block holds gate columns blk*32 + 0..31 (sub-tiles
+    // 0, 1) and the matching up columns (sub-tiles 2, 3)
     f16* Cp = (f16*)p.C;
-    const int nb0 = (n0 + wn * 16 * NI) >> 6;
+    const int blk = (n0 >> 6) + wave;
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
       const int m = mrow + 16 * i;
       if (m >= p.M) continue;
 #pragma unroll
-      for (int bl = 0; bl < NI / 4; ++bl)
-#pragma unroll
-        for (int f = 0; f < 2; ++f) {
-          const int col = (nb0 + bl) * 32 + 16 * f + 4 * g;
-          if (col < p.n_out) {
-            const f32x4 gt = acc[bl * 4 + f][i], up = acc[bl * 4 + f + 2][i];
-            *(f16x4*)(Cp + (size_t)m * p.ldc + col) =
-                f16x4{(f16)(silu(gt[0]) * up[0]), (f16)(silu(gt[1]) * up[1]),
-                      (f16)(silu(gt[2]) * up[2]), (f16)(silu(gt[3]) * up[3])};
-          }
+      for (int f = 0; f < 2; ++f) {
+        const int col = blk * 32 + 16 * f + 4 * g;
+        if (col < p.n_out) {
+          const f32x4 gt = acc[f][i], up = acc[f + 2][i];
+          *(f16x4*)(Cp + (size_t)m * p.ldc + col) =
+              f16x4{(f16)(silu(gt[0]) * up[0]), (f16)(silu(gt[1]) * up[1]),
+                    (f16)(silu(gt[2]) * up[2]), (f16)(silu(gt[3]) * up[3])};
         }
+      }
     }
   } else {  // EPI_HEAD: per token and 64-column block: (max, sum exp), allowed logits
     const int n_chunks = (p.N + 63) / 64;
-    const int nb0 = (n0 + wn * 16 * NI) >> 6;
+    const int blk = (n0 >> 6) + wave;
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
       const int m = mrow + 16 * i;
+      float mx = -INFINITY;
 #pragma unroll
-      for (int bl = 0; bl < NI / 4; ++bl) {
-        float mx = -INFINITY;
+      for (int f = 0; f < 4; ++f)
 #pragma unroll
-        for (int f = 0; f < 4; ++f)
+        for (int r = 0; r < 4; ++r)
+          if (ncol + 16 * f + r < p.N) mx = fmaxf(mx, acc[f][i][r]);
+      mx = fmaxf(mx, shfl_xor(mx, 16));
+      mx = fmaxf(mx, shfl_xor(mx, 32));
+      float sm = 0.f;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int n = ncol + 16 * (bl * 4 + f) + r;
-            if (n < p.N) mx = fmaxf(mx, acc[bl * 4 + f][i][r]);
-          }
-        mx = fmaxf(mx, shfl_xor(mx, 16));
-        mx = fmaxf(mx, shfl_xor(mx, 32));
-        float sm = 0.f;
+      for (int f = 0; f < 4; ++f)
 #pragma unroll
-        for (int f = 0; f < 4; ++f)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int n = ncol + 16 * (bl * 4 + f) + r;
-            if (n < p.N) {
-              const float z = acc[bl * 4 + f][i][r];
-              sm += __expf(z - mx);
-              if (m < p.M) {
-                const int si = p.sel[n];
-                if (si >= 0) p.zsel[(size_t)m * p.n_sel + si] = z;
-                if (p.dump) p.dump[(size_t)m * p.ld_dump + n] = z;
-              }
+        for (int r = 0; r < 4; ++r) {
+          const int n = ncol + 16 * f + r;
+          if (n < p.N) {
+            const float z = acc[f][i][r];
+            sm += __expf(z - mx);
+            if (m < p.M) {
+              const int si = p.sel[n];
+              if (si >= 0) p.zsel[(size_t)m * p.n_sel + si] = z;
+              if (p.dump) p.dump[(size_t)m * p.ld_dump + n] = z;
             }
           }
-        sm += shfl_xor(sm, 16);
-        sm += shfl_xor(sm, 32);
-        if (g == 0 && m < p.M && nb0 + bl < n_chunks)
-          p.part[(size_t)m * n_chunks + nb0 + bl] = make_float2(mx, sm);
-      }
+        }
+      sm += shfl_xor(sm, 16);
+      sm += shfl_xor(sm, 32);
+      if (g == 0 && m < p.M && blk < n_chunks)
+        p.part[(size_t)m * n_chunks + blk] = make_float2(mx, sm);
     }
   }
 }
 
-template <int MI, int NI, bool INT4, int EPI>
+template <int MI, bool INT4, int EPI>
 hipError_t launch_cfg(hipStream_t s, const GemmArgs& a) {
-  using C = Cfg<MI, NI, INT4>;
-  const int tiles = ((a.M + C::BM - 1) / C::BM) * ((a.N + C::BN - 1) / C::BN);
+  using C = Cfg<MI, INT4>;
+  const int tiles = ((a.M + C::BM - 1) / C::BM) * ((a.N + BN - 1) / BN);
   if (tiles == 0) return hipSuccess;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<MI, NI, INT4, EPI>,
+    hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<MI, INT4, EPI>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL((gemm_kernel<MI, NI, INT4, EPI>), dim3(tiles), dim3(256), C::LDS, s, a);
+  hipLaunchKernelGGL((gemm_kernel<MI, INT4, EPI>), dim3(tiles), dim3(256), C::LDS, s, a);
   return hipGetLastError();
 }
 
 template <bool INT4, int EPI>
 hipError_t launch_epi(hipStream_t s, const GemmArgs& a) {
-  // the head's epilogue does not fit the register file next to a 256x256 tile
-  if (INT4 && a.M > 1024) return launch_cfg<8, 8, true, EPI>(s, a);
-  if (a.M > 128) return launch_cfg<4, 8, INT4, EPI>(s, a);
-  return launch_cfg<2, 4, INT4, EPI>(s, a);
+  // the head's epilogue does not fit the register file next to a 256-token tile
+  if (a.M > 256) return launch_cfg<8, INT4, EPI>(s, a);
+  if (a.M > 64) return launch_cfg<4, INT4, EPI>(s, a);
+  return launch_cfg<2, INT4, EPI>(s, a);
 }
 
 }  // namespace
