@@ -1,18 +1,24 @@
 // Row-batched attention over a shared prefix plus each row's own tokens.
 //
-// Every row r of a batch attends to the keys of its prefix chain (a root
-// and optionally a child prefix, stored once per prefix and shared by all
-// rows that use it) followed by its own keys, causally.  Query head j reads
-// key/value head j / G (grouped-query attention, G = n_heads / n_kv_heads).
+// Every row of a batch attends to the keys of its prefix chain (a root and
+// optionally a child prefix, each stored once and shared by all rows that
+// use it) followed by its own keys, causally.  Query head j reads key/value
+// head j / G (grouped-query attention, G = n_heads / n_kv_heads).
 //
-// Workgroup = one (row, 64-query-vector tile, kv head); a query vector is a
-// (token, head-in-group) pair, so the G heads that share a kv head share
-// every K/V tile read.  Keys are walked in blocks of 32 staged in LDS (K
-// row-major, V transposed) and shared by the 4 waves; each wave owns 16
-// query vectors and keeps an online softmax (running max and sum in fp32,
-// base-2 exponent) with the scores computed transposed, S^T = K Q^T, so the
-// MFMA result layout of P^T is directly the B operand of O^T = V^T P^T and
-// every lane holds values of exactly one query.
+// KV store layout (per layer, capacity C slots, C a multiple of 64):
+//   K   [C][n_kv][hd]      (row-major per token)
+//   V^T [n_kv][hd][C]      (transposed, so a 64-key tile of one head is 128-byte rows)
+// so that both tiles copy into LDS with direct global->LDS loads and the
+// P.V product reads V^T rows with no transposition in the kernel.
+//
+// Workgroup = one (row, 128-query-vector tile, kv head); a query vector is
+// a (token, head-in-group) pair, so the G heads sharing a kv head share all
+// K/V tile reads.  Keys are walked segment by segment (root prefix, child
+// prefix, own) in blocks of 64 through a two-stage LDS ring.  Each wave
+// owns 32 query vectors and keeps an online softmax (fp32 running max and
+// sum, base-2 exponent).  Scores are computed transposed, S^T = K Q^T, so
+// the MFMA result layout of P^T is directly the B operand of O^T = V^T P^T
+// and every lane holds values of exactly one query.
 #include "common.h"
 #include "kernels.h"
 
@@ -20,16 +26,50 @@ namespace lmop {
 
 namespace {
 
-constexpr int KB = 32;  // keys per block
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef __attribute__((address_space(1))) void* gbl_ptr_t;
+
+LMOP_DEVICE void g2l16(const void* g, void* lds_base) {
+  __builtin_amdgcn_global_load_lds((gbl_ptr_t)g, (lds_ptr_t)lds_base, 16, 0, 0);
+}
+
+template <int N>
+LMOP_DEVICE void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+constexpr int KB = 64;   // keys per block
+constexpr int QW = 32;   // query vectors per wave
+constexpr int QT = ATTN_QTILE;  // query vectors per workgroup
+
+// 16-byte chunk swizzle: K rows (hd/8 chunks) by key, V^T rows (8 chunks) by dim
+template <int HD>
+LMOP_DEVICE int kswz(int key) {
+  return HD == 128 ? (key & 15) : ((key ^ (key >> 3)) & 7);
+}
+LMOP_DEVICE int vswz(int row) { return (row ^ (row >> 3)) & 7; }
+
+struct Seg {
+  const f16* kbase;  // layer's K [C][nkv][hd]
+  const f16* vbase;  // layer's V^T [nkv][hd][C]
+  int cap;           // C
+  int start;         // first slot of the segment
+  int n;             // keys needed from the segment
+};
 
 template <int HD>
-__global__ __launch_bounds__(256) void attn_kernel(const AttnArgs p, float scale_log2) {
-  constexpr int KS = HD + 8;   // K row stride in LDS (halves)
-  constexpr int VS = KB + 8;   // V^T row stride in LDS (halves)
+__global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float scale_log2) {
+  constexpr int K_BYTES = KB * HD * 2;
+  constexpr int V_BYTES = HD * KB * 2;
+  constexpr int STAGE = K_BYTES + V_BYTES;
+  constexpr int K_LOADS = K_BYTES / 1024 / 4;  // per wave
+  constexpr int V_LOADS = V_BYTES / 1024 / 4;
+  constexpr int LOADS = K_LOADS + V_LOADS;
   constexpr int NS = HD / 32;  // k-steps of the score MFMA
   constexpr int NT = HD / 16;  // 16-dim output tiles
-  __shared__ f16 sK[KB * KS];
-  __shared__ f16 sV[HD * VS];
+  constexpr int KCH = HD / 8;  // 16-byte chunks per K row
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
@@ -38,127 +78,190 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs p, float scale
   const int h = blockIdx.y;  // kv head
   const int G = p.nq / p.nkv;
   const int kvdim = p.nkv * HD;
+
+  // segments: root prefix, child prefix, own tokens
+  int t_last = (wk.y * QT + QT - 1) / G;
+  if (t_last > row.n_q - 1) t_last = row.n_q - 1;
+  Seg seg[3];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int cap = row.seg_cap[s];
+    const f16* base = (const f16*)row.seg_kv[s] + (size_t)p.layer * 2 * cap * kvdim;
+    seg[s] = Seg{base, base + (size_t)cap * kvdim, cap, 0, row.seg_n[s]};
+  }
+  {
+    const f16* base = (const f16*)p.own_kv + (size_t)p.layer * 2 * p.own_cap * kvdim;
+    seg[2] = Seg{base, base + (size_t)p.own_cap * kvdim, p.own_cap, row.own_slot,
+                 row.own_q0 + t_last + 1};
+  }
+  const int nb0 = (seg[0].n + KB - 1) / KB, nb1 = (seg[1].n + KB - 1) / KB;
+  const int nb2 = (seg[2].n + KB - 1) / KB;
+  const int NB = nb0 + nb1 + nb2;
   const int P = row.seg_n[0] + row.seg_n[1];
 
-  // this lane's query vector
-  const int v = wk.y * 64 + wave * 16 + c;
-  const int t = v / G;
-  const bool qvalid = t < row.n_q;
-  const int hq = h * G + (v - t * G);
-  const int n_vis = qvalid ? P + row.own_q0 + t + 1 : 1;
+  // block b -> (segment, first key of the block within the segment)
+  auto locate = [&](int b, int& s, int& kb) {
+    if (b < nb0) {
+      s = 0;
+      kb = b * KB;
+    } else if (b < nb0 + nb1) {
+      s = 1;
+      kb = (b - nb0) * KB;
+    } else {
+      s = 2;
+      kb = (b - nb0 - nb1) * KB;
+    }
+  };
 
-  // keys needed by the workgroup: up to its last valid token
-  int t_last = (wk.y * 64 + 63) / G;
-  if (t_last > row.n_q - 1) t_last = row.n_q - 1;
-  const int n_keys = P + row.own_q0 + t_last + 1;
+  auto issue = [&](int st, int b) {
+    int s, kb;
+    locate(b, s, kb);
+    const Seg& sg = seg[s];
+    char* sK = smem + st * STAGE;
+    char* sV = sK + K_BYTES;
+#pragma unroll
+    for (int i = 0; i < K_LOADS; ++i) {
+      const int q = wave + 4 * i;                // 1 KB = 1024 / (2*HD) keys
+      const int key = q * (512 / HD) + lane / KCH;
+      const int chunk = (lane % KCH) ^ kswz<HD>(key);
+      const f16* src = sg.kbase + (size_t)(sg.start + kb + key) * kvdim + h * HD + chunk * 8;
+      g2l16(src, sK + q * 1024);
+    }
+#pragma unroll
+    for (int i = 0; i < V_LOADS; ++i) {
+      const int q = wave + 4 * i;  // 8 dim rows of 128 bytes
+      const int dim = q * 8 + (lane >> 3);
+      const int chunk = (lane & 7) ^ vswz(dim);
+      const f16* src = sg.vbase + (size_t)(h * HD + dim) * sg.cap + sg.start + kb + chunk * 8;
+      g2l16(src, sV + q * 1024);
+    }
+  };
 
-  f16x8 qf[NS];
-  if (qvalid) {
-    const f16* qp = (const f16*)p.q + (size_t)(row.q_start + t) * p.ldq + hq * HD;
+  // this lane's query vectors: v = tile*128 + wave*32 + 16*qs + c
+  f16x8 qf[2][NS];
+  int n_vis[2];  // own keys visible to the query (prefix keys are all visible)
+  bool qvalid[2];
+  int tok[2], hq[2];
 #pragma unroll
-    for (int s = 0; s < NS; ++s) qf[s] = *(const f16x8*)(qp + s * 32 + g * 8);
-  } else {
+  for (int qs = 0; qs < 2; ++qs) {
+    const int v = wk.y * QT + wave * QW + 16 * qs + c;
+    const int t = v / G;
+    qvalid[qs] = t < row.n_q;
+    tok[qs] = t;
+    hq[qs] = h * G + (v - t * G);
+    n_vis[qs] = qvalid[qs] ? row.own_q0 + t + 1 : 1;
+    if (qvalid[qs]) {
+      const f16* qp = (const f16*)p.q + (size_t)(row.q_start + t) * p.ldq + hq[qs] * HD;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) qf[s] = f16x8{0, 0, 0, 0, 0, 0, 0, 0};
+      for (int s = 0; s < NS; ++s) qf[qs][s] = *(const f16x8*)(qp + s * 32 + g * 8);
+    } else {
+#pragma unroll
+      for (int s = 0; s < NS; ++s) qf[qs][s] = f16x8{0, 0, 0, 0, 0, 0, 0, 0};
+    }
   }
 
-  f32x4 o[NT];
+  f32x4 o[2][NT];
 #pragma unroll
-  for (int i = 0; i < NT; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -1e30f, l_run = 0.f;
+  for (int qs = 0; qs < 2; ++qs)
+#pragma unroll
+    for (int i = 0; i < NT; ++i) o[qs][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run[2] = {-1e30f, -1e30f}, l_run[2] = {0.f, 0.f};
 
-  const size_t own_layer = (size_t)p.layer * 2 * p.own_cap * kvdim;
-  for (int kb = 0; kb < n_keys; kb += KB) {
+  issue(0, 0);
+  for (int b = 0; b < NB; ++b) {
+    if (b + 1 < NB) {
+      issue((b + 1) & 1, b + 1);
+      wait_vmcnt<LOADS>();
+    } else {
+      wait_vmcnt<0>();
+    }
     __syncthreads();
-    // stage K (row-major) and V (transposed) of keys kb .. kb+31
-    for (int ch = tid; ch < KB * HD / 8; ch += 256) {
-      const int kl = ch / (HD / 8), d0 = (ch - kl * (HD / 8)) * 8;
-      const int kk = kb + kl;
-      f16x8 kv = f16x8{0, 0, 0, 0, 0, 0, 0, 0}, vv = kv;
-      if (kk < n_keys) {
-        const f16* base;
-        size_t voff;
-        if (kk < row.seg_n[0]) {
-          const int n = row.seg_n[0];
-          base = (const f16*)row.seg_kv[0] + (size_t)p.layer * 2 * n * kvdim + (size_t)kk * kvdim;
-          voff = (size_t)n * kvdim;
-        } else if (kk < P) {
-          const int n = row.seg_n[1];
-          base = (const f16*)row.seg_kv[1] + (size_t)p.layer * 2 * n * kvdim +
-                 (size_t)(kk - row.seg_n[0]) * kvdim;
-          voff = (size_t)n * kvdim;
-        } else {
-          base = (const f16*)p.own_kv + own_layer + (size_t)(row.own_slot + kk - P) * kvdim;
-          voff = (size_t)p.own_cap * kvdim;
+    int s, kb;
+    locate(b, s, kb);
+    const char* sK = smem + (b & 1) * STAGE;
+    const char* sV = sK + K_BYTES;
+    const int seg_n = seg[s].n;
+
+    // S^T: keys kb + 16*kt + 4g + r (kt = 0..3), queries (qs, c)
+    f32x4 st[2][4];
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+      f16x8 a[NS];
+      const int key = kt * 16 + c;
+#pragma unroll
+      for (int ks = 0; ks < NS; ++ks)
+        a[ks] = *(const f16x8*)(sK + key * (HD * 2) + (((ks * 4 + g) ^ kswz<HD>(key)) * 16));
+#pragma unroll
+      for (int qs = 0; qs < 2; ++qs) {
+        st[qs][kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < NS; ++ks) st[qs][kt] = mfma16x16x32(a[ks], qf[qs][ks], st[qs][kt]);
+      }
+    }
+    f16x8 pb[2][2];
+#pragma unroll
+    for (int qs = 0; qs < 2; ++qs) {
+      float mb = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int kk = kb + kt * 16 + 4 * g + r;
+          const bool vis = kk < seg_n && (s < 2 || kk < n_vis[qs]);
+          const float sc = vis ? st[qs][kt][r] * scale_log2 : -INFINITY;
+          st[qs][kt][r] = sc;
+          mb = fmaxf(mb, sc);
         }
-        base += h * HD + d0;
-        kv = *(const f16x8*)base;
-        vv = *(const f16x8*)(base + voff);
-      }
-      *(f16x8*)(sK + kl * KS + d0) = kv;
+      mb = fmaxf(mb, shfl_xor(mb, 16));
+      mb = fmaxf(mb, shfl_xor(mb, 32));
+      const float m_new = fmaxf(m_run[qs], mb);
+      const float alpha = exp2f(m_run[qs] - m_new);
+      m_run[qs] = m_new;
+      float ps = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sV[(d0 + e) * VS + kl] = vv[e];
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float e = exp2f(st[qs][kt][r] - m_new);
+          ps += e;
+          pb[qs][kt >> 1][(kt & 1) * 4 + r] = (f16)e;
+        }
+      l_run[qs] = l_run[qs] * alpha + ps;
+#pragma unroll
+      for (int i = 0; i < NT; ++i) o[qs][i] *= alpha;
     }
-    __syncthreads();
-
-    // S^T for keys kb + 16*half + (4g + r), query c
-    f32x4 st[2];
+    // O^T += V^T P^T over two 32-key chunks
 #pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-      st[hf] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int kc = 0; kc < 2; ++kc) {
 #pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const f16x8 a = *(const f16x8*)(sK + (hf * 16 + c) * KS + s * 32 + g * 8);
-        st[hf] = mfma16x16x32(a, qf[s], st[hf]);
+      for (int i = 0; i < NT; ++i) {
+        const int dim = 16 * i + c;
+        const int sw = vswz(dim);
+        const char* rowp = sV + dim * 128;
+        const f16x4 lo = *(const f16x4*)(rowp + (((4 * kc + (g >> 1)) ^ sw) * 16) + (g & 1) * 8);
+        const f16x4 hi =
+            *(const f16x4*)(rowp + (((4 * kc + 2 + (g >> 1)) ^ sw) * 16) + (g & 1) * 8);
+        const f16x8 a = f16x8{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+        for (int qs = 0; qs < 2; ++qs) o[qs][i] = mfma16x16x32(a, pb[qs][kc], o[qs][i]);
       }
     }
-    float mb = -INFINITY;
-#pragma unroll
-    for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int kk = kb + hf * 16 + 4 * g + r;
-        const float sc = kk < n_vis ? st[hf][r] * scale_log2 : -INFINITY;
-        st[hf][r] = sc;
-        mb = fmaxf(mb, sc);
-      }
-    mb = fmaxf(mb, shfl_xor(mb, 16));
-    mb = fmaxf(mb, shfl_xor(mb, 32));
-    const float m_new = fmaxf(m_run, mb);
-    const float alpha = exp2f(m_run - m_new);
-    m_run = m_new;
-    f16x8 pb;
-    float ps = 0.f;
-#pragma unroll
-    for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float e = exp2f(st[hf][r] - m_new);
-        ps += e;
-        pb[hf * 4 + r] = (f16)e;
-      }
-    l_run = l_run * alpha + ps;
-#pragma unroll
-    for (int i = 0; i < NT; ++i) {
-      o[i] *= alpha;
-      // A = V^T rows 16i + c, keys matching P^T's register order
-      const f16x4 lo = *(const f16x4*)(sV + (16 * i + c) * VS + 4 * g);
-      const f16x4 hi = *(const f16x4*)(sV + (16 * i + c) * VS + 16 + 4 * g);
-      const f16x8 a = f16x8{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-      o[i] = mfma16x16x32(a, pb, o[i]);
-    }
+    __syncthreads();  // the next issue overwrites this stage
   }
 
-  float l_tot = l_run + shfl_xor(l_run, 16);
-  l_tot += shfl_xor(l_tot, 32);
-  if (qvalid) {
-    const float inv = 1.0f / l_tot;
-    f16* op = (f16*)p.out + (size_t)(row.q_start + t) * p.ldo + hq * HD;
 #pragma unroll
-    for (int i = 0; i < NT; ++i) {
-      f16x4 w = {(f16)(o[i][0] * inv), (f16)(o[i][1] * inv), (f16)(o[i][2] * inv),
-                 (f16)(o[i][3] * inv)};
-      *(f16x4*)(op + 16 * i + 4 * g) = w;
+  for (int qs = 0; qs < 2; ++qs) {
+    float l_tot = l_run[qs] + shfl_xor(l_run[qs], 16);
+    l_tot += shfl_xor(l_tot, 32);
+    if (qvalid[qs]) {
+      const float inv = 1.0f / l_tot;
+      f16* op = (f16*)p.out + (size_t)(row.q_start + tok[qs]) * p.ldo + hq[qs] * HD;
+#pragma unroll
+      for (int i = 0; i < NT; ++i) {
+        f16x4 w = {(f16)(o[qs][i][0] * inv), (f16)(o[qs][i][1] * inv), (f16)(o[qs][i][2] * inv),
+                   (f16)(o[qs][i][3] * inv)};
+        *(f16x4*)(op + 16 * i + 4 * g) = w;
+      }
     }
   }
 }

@@ -1,7 +1,7 @@
 // HBM-bound kernels of the row-evaluation path: embedding gather, RMSNorm
-// (fp32 residual -> fp16 GEMM operand), rotary embedding with the key/value
-// write into the KV store, the load-time int4 repack, and the per-row
-// finish of the constrained LM head.
+// (fp32 residual -> fp16 GEMM operand), the load-time int4 repack, and the
+// per-row finish of the constrained LM head.  (RoPE and the key/value write
+// live in the QKV GEMM's epilogue.)
 #include "common.h"
 #include "kernels.h"
 
@@ -56,42 +56,6 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
                (f16)(v.w * rstd * gm.w)};
     *(f16x4*)(o + j) = h;
   }
-}
-
-// --------------------------------------------------------------- RoPE + KV write
-// qkv row layout: [q heads | k heads | v heads], each head hd wide.  Pair
-// (i, i + hd/2) of every q and k head turns by the angle of position pos[t]
-// (cos/sin table built on the host in double precision).  q goes to qout,
-// k and v to slot[t] of the KV store ([slot][nkv][hd]).
-__global__ __launch_bounds__(256) void rope_kv_kernel(const f16* __restrict__ qkv, int ldqkv,
-                                                      const int32_t* __restrict__ pos,
-                                                      const int32_t* __restrict__ slot,
-                                                      const float2* __restrict__ tab, int nq,
-                                                      int nkv, int hd, f16* __restrict__ qout,
-                                                      f16* __restrict__ kc, f16* __restrict__ vc) {
-  const int t = blockIdx.x;
-  const int half = hd / 2;
-  const f16* src = qkv + (size_t)t * ldqkv;
-  const float2* cs = tab + (size_t)pos[t] * half;
-  const size_t kvoff = (size_t)slot[t] * nkv * hd;
-  const int n_rot = (nq + nkv) * half;
-  for (int e = threadIdx.x; e < n_rot; e += 256) {
-    const int h = e / half, i = e - h * half;
-    const float x1 = (float)src[h * hd + i], x2 = (float)src[h * hd + i + half];
-    const float2 a = cs[i];
-    const f16 y1 = (f16)(x1 * a.x - x2 * a.y), y2 = (f16)(x1 * a.y + x2 * a.x);
-    if (h < nq) {
-      f16* dq = qout + (size_t)t * nq * hd + h * hd;
-      dq[i] = y1;
-      dq[i + half] = y2;
-    } else {
-      f16* dk = kc + kvoff + (h - nq) * hd;
-      dk[i] = y1;
-      dk[i + half] = y2;
-    }
-  }
-  const f16* vsrc = src + (nq + nkv) * hd;
-  for (int e = threadIdx.x; e < nkv * hd; e += 256) vc[kvoff + e] = vsrc[e];
 }
 
 // --------------------------------------------------------------- int4 repack
@@ -214,16 +178,6 @@ hipError_t launch_rmsnorm(hipStream_t s, const float* x, int ldx, const float* c
   if (R == 0) return hipSuccess;
   hipLaunchKernelGGL(rmsnorm_kernel, dim3(R), dim3(256), 0, s, x, ldx, rowptr, gamma, d, eps,
                      (f16*)out, ldo);
-  return hipGetLastError();
-}
-
-hipError_t launch_rope_kv(hipStream_t s, const half_bits* qkv, int ldqkv, int T,
-                          const int32_t* pos, const int32_t* slot, const float2* rope_tab,
-                          int nq, int nkv, int hd, half_bits* qout, half_bits* kcache,
-                          half_bits* vcache) {
-  if (T == 0) return hipSuccess;
-  hipLaunchKernelGGL(rope_kv_kernel, dim3(T), dim3(256), 0, s, (const f16*)qkv, ldqkv, pos, slot,
-                     rope_tab, nq, nkv, hd, (f16*)qout, (f16*)kcache, (f16*)vcache);
   return hipGetLastError();
 }
 

@@ -277,6 +277,52 @@ __global__ __launch_bounds__(256, Occ<MI>::value) void gemm_kernel(const GemmArg
         }
       }
     }
+  } else if constexpr (EPI == EPI_QKV) {
+    const int blk = (n0 >> 6) + wave;
+    const int bph = p.hd >> 6;  // 64-column blocks per head
+    const int nqb = p.nq * bph, nkb = p.nkv * bph;
+    if (blk < nqb + 2 * nkb) {
+      const int sec = blk < nqb ? 0 : (blk < nqb + nkb ? 1 : 2);
+      const int hb = blk - (sec == 0 ? 0 : (sec == 1 ? nqb : nqb + nkb));
+      const int head = hb / bph, sub = hb - head * bph;
+      const int half = p.hd >> 1;
+      const int kvdim = p.nkv * p.hd;
+#pragma unroll
+      for (int i = 0; i < MI; ++i) {
+        const int m = mrow + 16 * i;
+        if (m >= p.M) continue;
+        const int sl = p.slot[m];
+        if (sec < 2) {
+          const float2* cs = p.rope + (size_t)p.pos[m] * half;
+          f16* dst = sec == 0 ? (f16*)p.qout + (size_t)m * p.nq * p.hd + head * p.hd
+                              : (f16*)p.kc + (size_t)sl * kvdim + head * p.hd;
+#pragma unroll
+          for (int f = 0; f < 2; ++f) {
+            const int d = 32 * sub + 16 * f + 4 * g;
+            const f32x4 x1 = acc[f][i], x2 = acc[f + 2][i];
+            const float4 c01 = *(const float4*)(cs + d);
+            const float4 c23 = *(const float4*)(cs + d + 2);
+            const float cr[4] = {c01.x, c01.z, c23.x, c23.z};
+            const float sr[4] = {c01.y, c01.w, c23.y, c23.w};
+            f16x4 y1, y2;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              y1[r] = (f16)(x1[r] * cr[r] - x2[r] * sr[r]);
+              y2[r] = (f16)(x1[r] * sr[r] + x2[r] * cr[r]);
+            }
+            *(f16x4*)(dst + d) = y1;
+            *(f16x4*)(dst + half + d) = y2;
+          }
+        } else {
+          f16* vt = (f16*)p.vt + (size_t)head * p.hd * p.cap + sl;
+#pragma unroll
+          for (int f = 0; f < 4; ++f)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              vt[(size_t)(64 * sub + 16 * f + 4 * g + r) * p.cap] = (f16)acc[f][i][r];
+        }
+      }
+    }
   } else {  // EPI_HEAD: per token and 64-column block: (max, sum exp), allowed logits
     const int n_chunks = (p.N + 63) / 64;
     const int blk = (n0 >> 6) + wave;
@@ -348,6 +394,7 @@ hipError_t launch_gemm_w4(hipStream_t s, const GemmArgs& a, int epi) {
     case EPI_STORE_F16: return launch_epi<true, EPI_STORE_F16>(s, a);
     case EPI_ADD_F32: return launch_epi<true, EPI_ADD_F32>(s, a);
     case EPI_SWIGLU: return launch_epi<true, EPI_SWIGLU>(s, a);
+    case EPI_QKV: return launch_epi<true, EPI_QKV>(s, a);
     default: return hipErrorInvalidValue;
   }
 }

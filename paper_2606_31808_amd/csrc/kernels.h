@@ -27,7 +27,8 @@ enum Epilogue : int {
   EPI_STORE_F16 = 0,  // C[m][n] = fp16(acc)
   EPI_ADD_F32 = 1,    // X[m][n] += acc (residual stream)
   EPI_SWIGLU = 2,     // fused [gate|up] blocks of 32: C[m][j] = fp16(silu(gate_j) * up_j)
-  EPI_HEAD = 3        // LM head: per-64-column (max, sum exp), allowed-token logits, debug dump
+  EPI_HEAD = 3,       // LM head: per-64-column (max, sum exp), allowed-token logits, debug dump
+  EPI_QKV = 4         // fused q|k|v: RoPE on q, k; q -> qout, k -> K store, v -> V^T store
 };
 
 struct GemmArgs {
@@ -53,6 +54,18 @@ struct GemmArgs {
   int n_sel;
   float* dump;           // NULL or fp32 [M][ld_dump]
   int ld_dump;
+  // qkv epilogue.  Packed column order: q heads, k heads, v heads; every head
+  // is hd/64 blocks of 64 columns; in a q/k block b of a head the columns are
+  // dims [32b, 32b+32) then [hd/2 + 32b, hd/2 + 32b + 32), so each rotation
+  // pair (d, d + hd/2) sits in one lane; v blocks keep the natural order.
+  const int32_t* pos;    // [M] position of each token
+  const int32_t* slot;   // [M] KV slot of each token
+  const float2* rope;    // [max_seq][hd/2] (cos, sin)
+  half_bits* qout;       // [M][nq*hd]
+  half_bits* kc;         // layer's K store [cap][nkv][hd]
+  half_bits* vt;         // layer's V^T store [nkv][hd][cap]
+  int cap;
+  int nq, nkv, hd;
 };
 
 // Picks the tile shape for M and launches.  Returns hipSuccess or the launch error.
@@ -75,30 +88,30 @@ hipError_t launch_embed(hipStream_t s, const int32_t* tok, int T, const half_bit
 // out[i] = fp16(rows[i] / rms(rows[i]) * gamma); rows[i] = x + i*ldx, or rowptr[i] if given
 hipError_t launch_rmsnorm(hipStream_t s, const float* x, int ldx, const float* const* rowptr,
                           int R, const float* gamma, int d, float eps, half_bits* out, int ldo);
-// q/k get rotate-half RoPE at pos[t]; q -> qout [T][nq*hd]; k, v -> kcache/vcache[slot[t]]
-hipError_t launch_rope_kv(hipStream_t s, const half_bits* qkv, int ldqkv, int T,
-                          const int32_t* pos, const int32_t* slot, const float2* rope_tab,
-                          int nq, int nkv, int hd, half_bits* qout, half_bits* kcache,
-                          half_bits* vcache);
 
 // ---------------------------------------------------------------- attention
+// KV store of C slots (C a multiple of 64), per layer: K [C][nkv][hd] then
+// V^T [nkv][hd][C]; layers follow each other ([L][2][C*nkv*hd]).
 struct AttnRow {
-  const half_bits* seg_kv[2];  // prefix-chain KV storage [L][2][n][nkv][hd], or NULL
+  const half_bits* seg_kv[2];  // prefix-chain KV stores (root, child), or NULL
   int seg_n[2];                // tokens of each segment (0 if absent)
+  int seg_cap[2];              // slots C of each segment's store
   int q_start;                 // first query token of the row in the batch buffers
   int n_q;                     // query tokens of the row in this launch
-  int own_slot;                // slot of own token 0 in the own-KV buffer
+  int own_slot;                // slot of own token 0 in the own-KV store (multiple of 8)
   int own_q0;                  // own index of the first query token
 };
+constexpr int ATTN_QTILE = 128;  // query vectors (token, head-in-group) per workgroup
+
 struct AttnArgs {
   const half_bits* q;  // [T][ldq], post-RoPE
   int ldq;
   half_bits* out;      // [T][ldo]
   int ldo;
   const AttnRow* rows;
-  const int2* work;    // (row, 64-query tile)
+  const int2* work;    // (row, ATTN_QTILE-query tile)
   int n_work;
-  const half_bits* own_kv;  // [L][2][own_cap][nkv][hd]
+  const half_bits* own_kv;  // own-KV store, own_cap slots
   int own_cap;
   int layer;
   int nq, nkv, hd;

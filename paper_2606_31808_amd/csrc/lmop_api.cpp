@@ -59,7 +59,8 @@ struct lmop_prefix {
   lmop_prefix* parent = nullptr;
   int n = 0;       // own tokens
   int start = 0;   // tokens of the parent chain
-  uint16_t* kv = nullptr;     // device [L][2][n][nkv][hd]
+  int cap = 0;     // slots of the KV store (n rounded up to 64)
+  uint16_t* kv = nullptr;     // device KV store: per layer K [cap][nkv][hd], V^T [nkv][hd][cap]
   float* hidden = nullptr;    // device [d]: last token's final-layer hidden state
   int children = 0;
   bool released = false;
@@ -143,18 +144,22 @@ lmop_status dev_alloc(lmop_ctx* c, void** p, size_t bytes) {
   return LMOP_OK;
 }
 
-// named grow-only scratch buffer
+// named grow-only scratch buffer; `zero` clears it whenever it is (re)allocated
 template <typename T>
-lmop_status ws_get(lmop_ctx* c, const char* name, size_t count, T** out) {
+lmop_status ws_get(lmop_ctx* c, const char* name, size_t count, T** out, bool zero = false) {
   size_t bytes = std::max<size_t>(count * sizeof(T), 256);
   auto& slot = c->ws[name];
   if (slot.second < bytes) {
-    if (slot.first) HIP_OK(c, hipFree(slot.first));
+    if (slot.first) {
+      HIP_OK(c, hipStreamSynchronize(c->stream));
+      HIP_OK(c, hipFree(slot.first));
+    }
     slot = {nullptr, 0};
     size_t want = bytes + bytes / 4;
     void* p = nullptr;
     LMOP_TRY(dev_alloc(c, &p, want));
     slot = {p, want};
+    if (zero) HIP_OK(c, hipMemsetAsync(p, 0, want, c->stream));
   }
   *out = (T*)slot.first;
   return LMOP_OK;
@@ -421,7 +426,7 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
   AttnRow* rows;
   int2* work;
   float* x;
-  uint16_t *h, *qkv, *q, *att, *act;
+  uint16_t *h, *q, *att, *act;
   LMOP_TRY(ws_get(c, "tok", T, &tok));
   LMOP_TRY(ws_get(c, "pos", T, &pos));
   LMOP_TRY(ws_get(c, "slot", T, &slot));
@@ -429,7 +434,6 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
   LMOP_TRY(ws_get(c, "work", b.n_work, &work));
   LMOP_TRY(ws_get(c, "x", (size_t)T * d, &x));
   LMOP_TRY(ws_get(c, "h", (size_t)T * d, &h));
-  LMOP_TRY(ws_get(c, "qkv", (size_t)T * c->qkv_n, &qkv));
   LMOP_TRY(ws_get(c, "q", (size_t)T * c->nq_dim, &q));
   LMOP_TRY(ws_get(c, "att", (size_t)T * c->nq_dim, &att));
   LMOP_TRY(ws_get(c, "act", (size_t)T * c->f64, &act));
@@ -464,13 +468,33 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
                            (double)T * W.n * (epi == EPI_ADD_F32 ? 8 : 2);
       return timed(c, name, flops, bytes, [&] { return launch_gemm_w4(c->stream, ga, epi); });
     };
-    LMOP_TRY(gemm("gemm_w4a16_qkv", h, d, L.qkv, EPI_STORE_F16, qkv, c->qkv_n, c->qkv_n));
     uint16_t* kc = b.own_kv + l * kv_layer;
-    uint16_t* vc = kc + (size_t)b.own_cap * c->nkv_dim;
-    LMOP_TRY(timed(c, "rope_kv", 0, (double)T * c->qkv_n * 4, [&] {
-      return launch_rope_kv(c->stream, qkv, c->qkv_n, T, pos, slot, c->rope_tab, cf.n_heads,
-                            cf.n_kv_heads, hd, q, kc, vc);
-    }));
+    uint16_t* vt = kc + (size_t)b.own_cap * c->nkv_dim;
+    {
+      GemmArgs ga{};
+      ga.A = h;
+      ga.lda = d;
+      ga.M = T;
+      ga.N = L.qkv.np;
+      ga.K = L.qkv.kp;
+      ga.bq = L.qkv.qpack;
+      ga.bs = L.qkv.spack;
+      ga.pos = pos;
+      ga.slot = slot;
+      ga.rope = c->rope_tab;
+      ga.qout = q;
+      ga.kc = kc;
+      ga.vt = vt;
+      ga.cap = b.own_cap;
+      ga.nq = cf.n_heads;
+      ga.nkv = cf.n_kv_heads;
+      ga.hd = hd;
+      const double flops = 2.0 * T * L.qkv.n * L.qkv.k;
+      const double bytes = (double)T * L.qkv.k * 2 + (double)L.qkv.n * L.qkv.k * 0.5625 +
+                           (double)T * L.qkv.n * 2;
+      LMOP_TRY(timed(c, "gemm_w4a16_qkv", flops, bytes,
+                     [&] { return launch_gemm_w4(c->stream, ga, EPI_QKV); }));
+    }
     AttnArgs aa{};
     aa.q = q;
     aa.ldq = c->nq_dim;
@@ -527,20 +551,23 @@ lmop_status upload_batch(lmop_ctx* c, const std::vector<int32_t>& tok,
 void fill_segments(const lmop_prefix* p, AttnRow& r) {
   r.seg_kv[0] = r.seg_kv[1] = nullptr;
   r.seg_n[0] = r.seg_n[1] = 0;
+  r.seg_cap[0] = r.seg_cap[1] = 0;
   if (!p) return;
-  if (p->parent) {
-    r.seg_kv[0] = p->parent->kv;
-    r.seg_n[0] = p->parent->n;
-    r.seg_kv[1] = p->kv;
-    r.seg_n[1] = p->n;
-  } else {
-    r.seg_kv[0] = p->kv;
-    r.seg_n[0] = p->n;
-  }
+  const lmop_prefix* chain[2] = {p->parent ? p->parent : p, p->parent ? p : nullptr};
+  for (int s = 0; s < 2; ++s)
+    if (chain[s]) {
+      r.seg_kv[s] = chain[s]->kv;
+      r.seg_n[s] = chain[s]->n;
+      r.seg_cap[s] = chain[s]->cap;
+    }
 }
 
+// own-KV slots: each row starts at a multiple of 8 (16-byte aligned V^T runs);
+// the store has 64 spare slots so a row's last 64-key block stays in bounds
+int own_store_cap(int used) { return round_up(used + 64, 64); }
+
 void add_work(std::vector<int2>& work, int row, int n_q, int G) {
-  const int tiles = (n_q * G + 63) / 64;
+  const int tiles = (n_q * G + ATTN_QTILE - 1) / ATTN_QTILE;
   for (int t = 0; t < tiles; ++t) work.push_back(make_int2(row, t));
 }
 
@@ -783,10 +810,23 @@ lmop_status lmop_load_weights(lmop_ctx* ctx, const lmop_weights* w) {
     D.attn_norm = (float*)p;
     LMOP_TRY(upload(ctx, L.mlp_norm, (size_t)d * 4, od, &p));
     D.mlp_norm = (float*)p;
-    {  // fused q | k | v
+    {  // fused q | k | v; q and k columns ordered so rotation pairs share a lane
       const lmop_qmat* s[3] = {&L.wq, &L.wk, &L.wv};
-      const int rows[3] = {nq, nkv, nkv};
-      auto m = concat_map(rows, 3, round_up(ctx->qkv_n, 256));
+      std::vector<int32_t> m(round_up(ctx->qkv_n, 256), -1);
+      const int hd = cf.head_dim, half = hd / 2, bph = hd / 64;
+      int j = 0;
+      for (int sec = 0; sec < 3; ++sec) {
+        const int heads = sec == 0 ? cf.n_heads : cf.n_kv_heads;
+        for (int h = 0; h < heads; ++h)
+          for (int sub = 0; sub < bph; ++sub)
+            for (int w = 0; w < 64; ++w, ++j) {
+              const int f = w / 16, e = w % 16;
+              const int dim = sec == 2 ? 64 * sub + w
+                                       : (f < 2 ? 32 * sub + 16 * f + e
+                                                : half + 32 * sub + 16 * (f - 2) + e);
+              m[j] = (sec << 24) | (h * hd + dim);
+            }
+      }
       LMOP_TRY(pack(ctx, s, 3, m, ctx->qkv_n, d, od, &D.qkv));
     }
     {
@@ -847,11 +887,18 @@ lmop_status lmop_set_prefix(lmop_ctx* ctx, const lmop_prefix* parent, const int3
   p->start = start;
   p->generation = ctx->generation;
   p->id = ctx->next_prefix_id++;
+  p->cap = round_up(n_tokens, 64);
   if (!ctx->host_only) {
     void* kv = nullptr;
     void* hid = nullptr;
-    LMOP_TRY(dev_alloc(ctx, &kv, (size_t)cf.n_layers * 2 * n_tokens * ctx->nkv_dim * 2));
+    const size_t kv_bytes = (size_t)cf.n_layers * 2 * p->cap * ctx->nkv_dim * 2;
+    LMOP_TRY(dev_alloc(ctx, &kv, kv_bytes));
     p->kv = (uint16_t*)kv;
+    // pad slots are read (masked) by attention: keep them finite
+    if (hipMemsetAsync(kv, 0, kv_bytes, ctx->stream) != hipSuccess) {
+      destroy_prefix_storage(p.get());
+      return fail(ctx, LMOP_ERR_DEVICE, "hipMemsetAsync of a prefix KV store failed");
+    }
     if (dev_alloc(ctx, &hid, (size_t)cf.d_model * 4) != LMOP_OK) {
       destroy_prefix_storage(p.get());
       return LMOP_ERR_OOM;
@@ -876,7 +923,7 @@ lmop_status lmop_set_prefix(lmop_ctx* ctx, const lmop_prefix* parent, const int3
     b.R = 1;
     b.n_work = (int)work.size();
     b.own_kv = p->kv;
-    b.own_cap = n_tokens;
+    b.own_cap = p->cap;
     if (st == LMOP_OK) st = forward(ctx, b);
     if (st == LMOP_OK) {
       float* x = nullptr;
@@ -1060,18 +1107,18 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
       ar.own_q0 = 0;
       add_work(work, i, len[i], G);
       t += len[i];
-      cap += len[i] + dec;
+      cap = round_up(cap + len[i] + dec, 8);
     }
+    cap = own_store_cap(cap);
     uint16_t* own_kv;
-    LMOP_TRY(ws_get(ctx, "own_kv", (size_t)cf.n_layers * 2 * std::max(cap, 1) * ctx->nkv_dim,
-                    &own_kv));
+    LMOP_TRY(ws_get(ctx, "own_kv", (size_t)cf.n_layers * 2 * cap * ctx->nkv_dim, &own_kv, true));
     LMOP_TRY(upload_batch(ctx, tok, pos, slot, rows, work));
     Batch b;
     b.T = T;
     b.R = R;
     b.n_work = (int)work.size();
     b.own_kv = own_kv;
-    b.own_cap = std::max(cap, 1);
+    b.own_cap = cap;
     LMOP_TRY(forward(ctx, b));
     float* x;
     LMOP_TRY(ws_get(ctx, "x", (size_t)std::max(T, 1) * d, &x));

@@ -171,6 +171,8 @@ def test_tiny_dedup_and_batch_invariance(tiny, L):
     o1, d1 = _run(ctx, sub, pre)
     o2, d2 = _run(ctx, sub, pre, no_dedup=True)
     o3, d3 = _run(ctx, sub, pre, max_batch_tokens=17)  # one row per batch
+    _log("dedup vs no-dedup per-row max|dz|:", np.abs(d1 - d2).max(axis=(1, 2)))
+    _log("dedup vs one-row batches per-row max|dz|:", np.abs(d1 - d3).max(axis=(1, 2)))
     assert np.array_equal(o1, o2) and np.array_equal(d1, d2)
     assert np.array_equal(o1, o3) and np.array_equal(d1, d3)
     for a, b in [(0, 2), (0, 7), (1, 4), (1, 5), (6, 9)]:
