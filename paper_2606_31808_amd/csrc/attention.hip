@@ -21,34 +21,30 @@
 // and every lane holds values of exactly one query.
 #include "common.h"
 #include "kernels.h"
+#include "lds_dma.h"
 
 namespace lmop {
 
 namespace {
 
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
-typedef __attribute__((address_space(1))) void* gbl_ptr_t;
-
-LMOP_DEVICE void g2l16(const void* g, void* lds_base) {
-  __builtin_amdgcn_global_load_lds((gbl_ptr_t)g, (lds_ptr_t)lds_base, 16, 0, 0);
-}
-
-template <int N>
-LMOP_DEVICE void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
 constexpr int KB = 64;   // keys per block
 constexpr int QW = 32;   // query vectors per wave
 constexpr int QT = ATTN_QTILE;  // query vectors per workgroup
 
-// 16-byte chunk swizzle: K rows (hd/8 chunks) by key, V^T rows (8 chunks) by dim
+// Key order inside a 32-key chunk: score tile hf (0, 1) row m = 4a + b
+// (a, b in 0..3) holds key 8a + 4hf + b, so that the MFMA result layout puts
+// keys 8g .. 8g+7 in the registers of lane group g and the P.V operand reads
+// one contiguous 16-byte run of a V^T row.
+LMOP_DEVICE int score_key(int hf, int m) { return 8 * (m >> 2) + 4 * hf + (m & 3); }
+
+// 16-byte chunk swizzles (conflict-free fragment loads on gfx950, measured
+// with SQ_LDS_BANK_CONFLICT): K rows by key, V^T rows by dim
 template <int HD>
 LMOP_DEVICE int kswz(int key) {
-  return HD == 128 ? (key & 15) : ((key ^ (key >> 3)) & 7);
+  const int s = ((key >> 1) & 12) | (key & 3);  // = m of score_key within a tile
+  return HD == 128 ? s : (s & 7);
 }
-LMOP_DEVICE int vswz(int row) { return (row ^ (row >> 3)) & 7; }
+LMOP_DEVICE int vswz(int row) { return row & 7; }
 
 struct Seg {
   const f16* kbase;  // layer's K [C][nkv][hd]
@@ -175,19 +171,20 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
     } else {
       wait_vmcnt<0>();
     }
-    __syncthreads();
+    barrier();
     int s, kb;
     locate(b, s, kb);
     const char* sK = smem + (b & 1) * STAGE;
     const char* sV = sK + K_BYTES;
     const int seg_n = seg[s].n;
 
-    // S^T: keys kb + 16*kt + 4g + r (kt = 0..3), queries (qs, c)
+    // S^T tiles kt = 2*kc + hf: register r of lane group g holds key
+    // kb + 32*kc + 8g + 4hf + r, query (qs, c)
     f32x4 st[2][4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
       f16x8 a[NS];
-      const int key = kt * 16 + c;
+      const int key = 32 * (kt >> 1) + score_key(kt & 1, c);
 #pragma unroll
       for (int ks = 0; ks < NS; ++ks)
         a[ks] = *(const f16x8*)(sK + key * (HD * 2) + (((ks * 4 + g) ^ kswz<HD>(key)) * 16));
@@ -206,7 +203,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int kk = kb + kt * 16 + 4 * g + r;
+          const int kk = kb + 32 * (kt >> 1) + 8 * g + 4 * (kt & 1) + r;
           const bool vis = kk < seg_n && (s < 2 || kk < n_vis[qs]);
           const float sc = vis ? st[qs][kt][r] * scale_log2 : -INFINITY;
           st[qs][kt][r] = sc;
@@ -230,23 +227,19 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
 #pragma unroll
       for (int i = 0; i < NT; ++i) o[qs][i] *= alpha;
     }
-    // O^T += V^T P^T over two 32-key chunks
+    // O^T += V^T P^T over two 32-key chunks; lane group g's operand is keys
+    // 32kc + 8g .. +7 of V^T row `dim`, one 16-byte chunk
 #pragma unroll
     for (int kc = 0; kc < 2; ++kc) {
 #pragma unroll
       for (int i = 0; i < NT; ++i) {
         const int dim = 16 * i + c;
-        const int sw = vswz(dim);
-        const char* rowp = sV + dim * 128;
-        const f16x4 lo = *(const f16x4*)(rowp + (((4 * kc + (g >> 1)) ^ sw) * 16) + (g & 1) * 8);
-        const f16x4 hi =
-            *(const f16x4*)(rowp + (((4 * kc + 2 + (g >> 1)) ^ sw) * 16) + (g & 1) * 8);
-        const f16x8 a = f16x8{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        const f16x8 a = *(const f16x8*)(sV + dim * 128 + (((4 * kc + g) ^ vswz(dim)) * 16));
 #pragma unroll
         for (int qs = 0; qs < 2; ++qs) o[qs][i] = mfma16x16x32(a, pb[qs][kc], o[qs][i]);
       }
     }
-    __syncthreads();  // the next issue overwrites this stage
+    barrier();  // the next issue overwrites this stage
   }
 
 #pragma unroll

@@ -9,8 +9,8 @@
 // filled by direct global->LDS loads (global_load_lds_dwordx4, 1 KB per wave
 // instruction): two steps' tiles stream in while the current step's MFMAs
 // run, and one barrier per step suffices.
-//   A tile: 128-byte rows, 16-byte chunks XOR-swizzled by row so that the 16
-//           rows read by one fragment load hit distinct LDS banks.
+//   A tile: 128-byte rows, 16-byte chunks XOR-swizzled by row so that one
+//           fragment load (16 rows) is free of LDS bank conflicts.
 //   int4 tile: copied verbatim from the packed layout (1 KB per 64 columns x
 //           32 features: lane 16g+c holds the 8 codes of 4 columns), scales
 //           likewise (128 B per 64 columns x 32 features).
@@ -30,18 +30,11 @@
 // tiles on an XCD share A and W panels in that XCD's L2.
 #include "common.h"
 #include "kernels.h"
+#include "lds_dma.h"
 
 namespace lmop {
 
 namespace {
-
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
-typedef __attribute__((address_space(1))) void* gbl_ptr_t;
-
-// 16 bytes per lane from global address g to LDS at base + lane*16
-LMOP_DEVICE void g2l16(const void* g, void* lds_base) {
-  __builtin_amdgcn_global_load_lds((gbl_ptr_t)g, (lds_ptr_t)lds_base, 16, 0, 0);
-}
 
 // (x & 0x000F000F) | 0x64006400 in one VALU op
 LMOP_DEVICE uint32_t and_or(uint32_t x, uint32_t mask, uint32_t magic) {
@@ -63,16 +56,10 @@ LMOP_DEVICE f16x8 dequant8(uint32_t w, f16 s) {
 
 LMOP_DEVICE float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
 
-// chunk swizzle of a 128-byte LDS row: distinct for any 8 rows aligned at 8
-// and, per row parity, for any 16 rows aligned at 16
-LMOP_DEVICE int swz(int row) { return (row ^ (row >> 3)) & 7; }
-
-// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding)
-template <int N>
-LMOP_DEVICE void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
+// 16-byte chunk swizzle of a 128-byte LDS row; with it a fragment load (16
+// rows x 4 chunks) is free of bank conflicts on gfx950 (measured with the
+// SQ_LDS_BANK_CONFLICT counter)
+LMOP_DEVICE int swz(int row) { return row & 7; }
 
 constexpr int BK = 64;
 constexpr int BN = 256;    // 4 waves x 64 columns
@@ -185,7 +172,7 @@ __global__ __launch_bounds__(256, Occ<MI>::value) void gemm_kernel(const GemmArg
       wait_vmcnt<C::LOADS>();
     else
       wait_vmcnt<0>();
-    __syncthreads();
+    barrier();
     if (kt + 2 < KT) issue((kt + 2) % NSTAGE, kt + 2);
     const char* sA = smem + (kt % NSTAGE) * C::STAGE;
     const char* sB = sA + C::A_BYTES;
