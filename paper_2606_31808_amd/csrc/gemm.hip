@@ -36,21 +36,24 @@ namespace lmop {
 
 namespace {
 
-// (x & 0x000F000F) | 0x64006400 in one VALU op
-LMOP_DEVICE uint32_t and_or(uint32_t x, uint32_t mask, uint32_t magic) {
-  uint32_t r;
-  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(mask), "v"(magic));
-  return r;
-}
-
-LMOP_DEVICE f16x8 dequant8(uint32_t w, f16 s) {
-  const uint32_t kMask = 0x000F000Fu, kMagic = 0x64006400u;
+// Dequantises the 8 biased codes of one word: nibble pair j (bits 4j and
+// 16+4j) | 0x6400 is fp16 1024 + u; minus 1032 gives the exact code; times
+// the scale gives one rounding.  `mask` and `magic` arrive in registers the
+// compiler cannot see through, so (x & mask) | (magic & ~mask) becomes a
+// single v_bitop3; the four pairs are independent chains the scheduler can
+// interleave with MFMAs.
+LMOP_DEVICE f16x8 dequant8(uint32_t w, f16 s, uint32_t mask, uint32_t magic) {
   const f16x2 bias = {(f16)1032.0f, (f16)1032.0f};
   const f16x2 s2 = {s, s};
-  f16x2 h0 = (__builtin_bit_cast(f16x2, and_or(w, kMask, kMagic)) - bias) * s2;
-  f16x2 h1 = (__builtin_bit_cast(f16x2, and_or(w >> 4, kMask, kMagic)) - bias) * s2;
-  f16x2 h2 = (__builtin_bit_cast(f16x2, and_or(w >> 8, kMask, kMagic)) - bias) * s2;
-  f16x2 h3 = (__builtin_bit_cast(f16x2, and_or(w >> 12, kMask, kMagic)) - bias) * s2;
+  const uint32_t nm = magic & ~mask;
+  const uint32_t t0 = (w & mask) | nm;
+  const uint32_t t1 = ((w >> 4) & mask) | nm;
+  const uint32_t t2 = ((w >> 8) & mask) | nm;
+  const uint32_t t3 = ((w >> 12) & mask) | nm;
+  const f16x2 h0 = (__builtin_bit_cast(f16x2, t0) - bias) * s2;
+  const f16x2 h1 = (__builtin_bit_cast(f16x2, t1) - bias) * s2;
+  const f16x2 h2 = (__builtin_bit_cast(f16x2, t2) - bias) * s2;
+  const f16x2 h3 = (__builtin_bit_cast(f16x2, t3) - bias) * s2;
   return f16x8{h0.x, h0.y, h1.x, h1.y, h2.x, h2.y, h3.x, h3.y};
 }
 
@@ -158,6 +161,11 @@ __global__ __launch_bounds__(256, Occ<MI>::value) void gemm_kernel(const GemmArg
     }
   };
 
+  // dequant constants kept opaque to the optimiser (see dequant8)
+  uint32_t dq_mask = 0x000F000Fu, dq_magic = 0x64006400u;
+  asm volatile("" : "+s"(dq_mask));
+  asm volatile("" : "+v"(dq_magic));
+
   f32x4 acc[4][MI];
 #pragma unroll
   for (int f = 0; f < 4; ++f)
@@ -179,28 +187,33 @@ __global__ __launch_bounds__(256, Occ<MI>::value) void gemm_kernel(const GemmArg
     const char* sS = sB + C::B_BYTES;
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      f16x8 w[4];
-      if constexpr (INT4) {
-        const int q = wave * 2 + kk;
-        const uint4 codes = *(const uint4*)(sB + q * 1024 + lane * 16);
-        const f16x4 s4 = *(const f16x4*)(sS + q * 128 + c * 8);
-        w[0] = dequant8(codes.x, s4.x);
-        w[1] = dequant8(codes.y, s4.y);
-        w[2] = dequant8(codes.z, s4.z);
-        w[3] = dequant8(codes.w, s4.w);
-      } else {
-#pragma unroll
-        for (int f = 0; f < 4; ++f) {
-          const int r = wave * 64 + 16 * f + c;
-          w[f] = *(const f16x8*)(sB + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
-        }
-      }
+      // all MI activation fragments of this 32-feature group, then one
+      // weight fragment at a time: its MI MFMAs overlap the next dequant
+      f16x8 a[MI];
 #pragma unroll
       for (int i = 0; i < MI; ++i) {
         const int r = 16 * i + c;
-        const f16x8 a = *(const f16x8*)(sA + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
+        a[i] = *(const f16x8*)(sA + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
+      }
+      uint4 codes;
+      f16x4 s4;
+      if constexpr (INT4) {
+        const int q = wave * 2 + kk;
+        codes = *(const uint4*)(sB + q * 1024 + lane * 16);
+        s4 = *(const f16x4*)(sS + q * 128 + c * 8);
+      }
 #pragma unroll
-        for (int f = 0; f < 4; ++f) acc[f][i] = mfma16x16x32(w[f], a, acc[f][i]);
+      for (int f = 0; f < 4; ++f) {
+        f16x8 w;
+        if constexpr (INT4) {
+          w = dequant8(f == 0 ? codes.x : f == 1 ? codes.y : f == 2 ? codes.z : codes.w, s4[f],
+                       dq_mask, dq_magic);
+        } else {
+          const int r = wave * 64 + 16 * f + c;
+          w = *(const f16x8*)(sB + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
+        }
+#pragma unroll
+        for (int i = 0; i < MI; ++i) acc[f][i] = mfma16x16x32(w, a[i], acc[f][i]);
       }
     }
   }
