@@ -1,0 +1,160 @@
+"""GPU parity at the full model shapes (1B and 8B) through the C ABI.
+
+Each test evaluates the whole synthetic table in the launch configuration the
+benchmark times (default batch budget, whole-table call), then evaluates a
+sample of its rows again with logit dumps and compares those with the fp32
+oracle (the precision the target names for its CPU forward).  The library's
+results do not depend on which other rows share a call, so the sampled call
+must reproduce the full call's typed outputs and log-probabilities exactly.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import OracleLM
+from synth import SHAPES, make_weights, make_workload
+from tests.parity import assert_typed, compare
+
+pytestmark = pytest.mark.gpu
+
+
+def _log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_31808_amd import lmop
+    return lmop
+
+
+def _model(L, name):
+    shape = SHAPES[name]
+    w = make_weights(shape, seed=1234, device="cuda")
+    torch.cuda.synchronize()
+    ctx = L.Context(shape, device=0, stream=torch.cuda.current_stream().cuda_stream)
+    ctx.load_weights(w)
+    return w, ctx
+
+
+@pytest.fixture(scope="module")
+def m8b(L):
+    _log("8B: weights on the GPU, library load, oracle setup")
+    w, ctx = _model(L, "8b")
+    orc = OracleLM(w, SHAPES["8b"], dtype=np.float32, cache_dequant=True)
+    yield w, ctx, orc
+    ctx.close()
+    del w
+    torch.cuda.empty_cache()
+
+
+def _same_rows(full, sub, rows, label):
+    for j, r in enumerate(rows):
+        assert np.array_equal(full[r], sub[j]), f"{label}: row {r} differs between calls"
+
+
+def _check_filter(ctx, orc, wl, pre, sample, label):
+    _log(f"{label}: full table ({wl.n_rows} rows, {wl.n_suffix_tokens} tokens)")
+    full, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, prefix=pre)
+    assert_typed(full, wl.kind, len(wl.allowed), wl.allowed)
+    sub = wl.subset(sample)
+    out, dbg = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, prefix=pre,
+                             debug_logits=True)
+    _same_rows(full, out, sample, label)
+    _log(f"{label}: oracle on {len(sample)} rows")
+    ref = orc.eval_workload(sub, keep_logits=True)
+    st = compare(ref, out, dbg, label)
+    _log(label, st)
+    return st
+
+
+def _sample(wl, n, seed):
+    lens = np.diff(wl.offsets)
+    rng = np.random.default_rng(seed)
+    pick = {int(np.argmax(lens)), int(np.argmin(lens)), 0, wl.n_rows - 1}
+    while len(pick) < n:
+        pick.add(int(rng.integers(0, wl.n_rows)))
+    return sorted(pick)
+
+
+def test_filter_1b_sampled_rows(L):
+    w, ctx = _model(L, "1b")
+    orc = OracleLM(w, SHAPES["1b"], dtype=np.float32, cache_dequant=True)
+    wl = make_workload("filter_1b")
+    pre = ctx.set_prefix(wl.prefix)
+    _check_filter(ctx, orc, wl, pre, _sample(wl, 12, 1), "filter_1b")
+    ctx.close()
+    del w, orc
+    torch.cuda.empty_cache()
+
+
+def test_filter_8b_sampled_rows(m8b):
+    w, ctx, orc = m8b
+    wl = make_workload("filter_8b")
+    pre = ctx.set_prefix(wl.prefix)
+    _check_filter(ctx, orc, wl, pre, _sample(wl, 5, 2), "filter_8b")
+    ctx.release_prefix(pre)
+
+
+def test_map_int_8b_dedup_and_sampled_rows(m8b, L):
+    w, ctx, orc = m8b
+    wl = make_workload("map_int_8b")
+    pre = ctx.set_prefix(wl.prefix)
+    _log(f"map_int_8b: full table ({wl.n_rows} rows)")
+    full, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, eos=wl.eos,
+                            max_tokens=wl.max_tokens, prefix=pre)
+    assert_typed(full, wl.kind, 10, wl.allowed, wl.eos, wl.max_tokens)
+    # early dedup: every duplicate gets its representative's result, bit for bit
+    rep, n_unique = L.lmop_dedup_rows(wl.tokens, wl.offsets)
+    assert 2300 < n_unique < 3000
+    assert np.array_equal(full, full[rep])
+    # a sample of distinct suffixes, each with two of its duplicate rows
+    rng = np.random.default_rng(3)
+    reps = rng.choice(np.unique(rep), 5, replace=False)
+    rows, uniq = [], []
+    for r in reps:
+        dup = np.nonzero(rep == r)[0]
+        uniq.append(len(rows))
+        rows.extend(dup[:2].tolist())
+    sub = wl.subset(rows)
+    out, dbg = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, eos=wl.eos,
+                             max_tokens=wl.max_tokens, prefix=pre, debug_logits=True)
+    _same_rows(full, out, rows, "map_int_8b")
+    sub_u = wl.subset([rows[j] for j in uniq])
+    _log(f"map_int_8b: oracle on {len(uniq)} rows")
+    ref = orc.eval_workload(sub_u, keep_logits=True)
+    forced = None
+    toks = [out["tokens"][j][: out["n_tokens"][j]] for j in uniq]
+    if any(list(t) != list(ref["tokens"][k][: ref["n_tokens"][k]]) for k, t in enumerate(toks)):
+        forced = orc.eval_workload(sub_u, keep_logits=True, forced=toks)
+    st = compare(ref, out[uniq], dbg[uniq], "map_int_8b", orc_forced=forced)
+    _log("map_int_8b", st)
+    ctx.release_prefix(pre)
+
+
+def test_join_8b_sampled_pairs(m8b):
+    w, ctx, orc = m8b
+    wl = make_workload("join_8b")
+    root = ctx.set_prefix(wl.prefix)
+    kids = [ctx.set_prefix(c, parent=root) for c in wl.children]
+    row_prefix = [kids[int(i)] for i in wl.row_child]
+    _log(f"join_8b: full table ({wl.n_rows} pairs)")
+    full, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, row_prefix=row_prefix)
+    assert_typed(full, wl.kind, 2, wl.allowed)
+    rows = [0, 199, 200 * 57 + 3, 200 * 57 + 150, 200 * 199 + 7, 200 * 199 + 199]
+    sub = wl.subset(rows)
+    out, dbg = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed,
+                             row_prefix=[row_prefix[r] for r in rows], debug_logits=True)
+    _same_rows(full, out, rows, "join_8b")
+    _log(f"join_8b: oracle on {len(rows)} pairs")
+    ref = orc.eval_workload(sub, keep_logits=True)
+    st = compare(ref, out, dbg, "join_8b")
+    _log("join_8b", st)
+    for k in kids:
+        ctx.release_prefix(k)
+    ctx.release_prefix(root)
