@@ -90,6 +90,9 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
     seg[2] = Seg{base, base + (size_t)p.own_cap * kvdim, p.own_cap, row.own_slot,
                  row.own_q0 + t_last + 1};
   }
+  // own keys visible to every valid query of the workgroup (first token's count)
+  int t_first = (wk.y * QT) / G;
+  const int vis_min = row.own_q0 + t_first + 1;
   const int nb0 = (seg[0].n + KB - 1) / KB, nb1 = (seg[1].n + KB - 1) / KB;
   const int nb2 = (seg[2].n + KB - 1) / KB;
   const int NB = nb0 + nb1 + nb2;
@@ -195,37 +198,50 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
         for (int ks = 0; ks < NS; ++ks) st[qs][kt] = mfma16x16x32(a[ks], qf[qs][ks], st[qs][kt]);
       }
     }
+    // online softmax; scores stay unscaled, p = 2^(s*c - m*c) with c = log2(e)/sqrt(hd).
+    // Blocks whose every key is visible to every query of the workgroup skip
+    // the mask; the running output is rescaled only when some maximum moved.
+    const bool need_mask = kb + KB > seg_n || (s == 2 && kb + KB > vis_min);
     f16x8 pb[2][2];
 #pragma unroll
     for (int qs = 0; qs < 2; ++qs) {
       float mb = -INFINITY;
+      if (need_mask) {
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int kk = kb + 32 * (kt >> 1) + 8 * g + 4 * (kt & 1) + r;
+            const bool vis = kk < seg_n && (s < 2 || kk < n_vis[qs]);
+            st[qs][kt][r] = vis ? st[qs][kt][r] : -INFINITY;
+          }
+      }
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int kk = kb + 32 * (kt >> 1) + 8 * g + 4 * (kt & 1) + r;
-          const bool vis = kk < seg_n && (s < 2 || kk < n_vis[qs]);
-          const float sc = vis ? st[qs][kt][r] * scale_log2 : -INFINITY;
-          st[qs][kt][r] = sc;
-          mb = fmaxf(mb, sc);
-        }
+        for (int r = 0; r < 4; ++r) mb = fmaxf(mb, st[qs][kt][r]);
       mb = fmaxf(mb, shfl_xor(mb, 16));
       mb = fmaxf(mb, shfl_xor(mb, 32));
       const float m_new = fmaxf(m_run[qs], mb);
-      const float alpha = exp2f(m_run[qs] - m_new);
-      m_run[qs] = m_new;
+      const float nmc = -m_new * scale_log2;
       float ps = 0.f;
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float e = exp2f(st[qs][kt][r] - m_new);
+          const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(st[qs][kt][r], scale_log2, nmc));
           ps += e;
           pb[qs][kt >> 1][(kt & 1) * 4 + r] = (f16)e;
         }
-      l_run[qs] = l_run[qs] * alpha + ps;
+      if (__all(m_new == m_run[qs])) {
+        l_run[qs] += ps;
+      } else {
+        const float alpha = __builtin_amdgcn_exp2f((m_run[qs] - m_new) * scale_log2);
+        l_run[qs] = l_run[qs] * alpha + ps;
 #pragma unroll
-      for (int i = 0; i < NT; ++i) o[qs][i] *= alpha;
+        for (int i = 0; i < NT; ++i) o[qs][i] *= alpha;
+      }
+      m_run[qs] = m_new;
     }
     // O^T += V^T P^T over two 32-key chunks; lane group g's operand is keys
     // 32kc + 8g .. +7 of V^T row `dim`, one 16-byte chunk

@@ -58,6 +58,22 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
   }
 }
 
+// --------------------------------------------------------------- row gather
+// Copies the residual row and the attention-output row of each selected token
+// (the last token of every row, before the last layer's O-projection and MLP).
+__global__ __launch_bounds__(256) void gather_rows_kernel(const int32_t* __restrict__ idx,
+                                                          const float* __restrict__ x, int d,
+                                                          float* __restrict__ x_out,
+                                                          const f16* __restrict__ a, int da,
+                                                          f16* __restrict__ a_out) {
+  const int i = blockIdx.x;
+  const size_t t = (size_t)idx[i];
+  for (int j = threadIdx.x * 4; j < d; j += 256 * 4)
+    *(float4*)(x_out + (size_t)i * d + j) = *(const float4*)(x + t * d + j);
+  for (int j = threadIdx.x * 8; j < da; j += 256 * 8)
+    *(f16x8*)(a_out + (size_t)i * da + j) = *(const f16x8*)(a + t * da + j);
+}
+
 // --------------------------------------------------------------- int4 repack
 // One thread per (64-column block, group, lane, word): gathers the 8 codes of
 // column nb*64 + 16f + c, features kg*32 + 8g .. +7, from its source row and
@@ -170,6 +186,15 @@ hipError_t launch_embed(hipStream_t s, const int32_t* tok, int T, const half_bit
                         float* x) {
   if (T == 0) return hipSuccess;
   hipLaunchKernelGGL(embed_kernel, dim3(T), dim3(256), 0, s, tok, (const f16*)emb, d, x);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(hipStream_t s, const int32_t* idx, int R, const float* x, int d,
+                              float* x_out, const half_bits* a, int da, half_bits* a_out) {
+  if (R == 0) return hipSuccess;
+  if (d % 4 != 0 || da % 8 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(R), dim3(256), 0, s, idx, x, d, x_out,
+                     (const f16*)a, da, (f16*)a_out);
   return hipGetLastError();
 }
 

@@ -85,6 +85,9 @@ hipError_t launch_repack_w4(hipStream_t s, const RepackSrc& src, const int32_t* 
 // ---------------------------------------------------------------- elementwise
 hipError_t launch_embed(hipStream_t s, const int32_t* tok, int T, const half_bits* emb, int d,
                         float* x);
+// x_out[i] = x[idx[i]] (fp32, d), a_out[i] = a[idx[i]] (fp16, da)
+hipError_t launch_gather_rows(hipStream_t s, const int32_t* idx, int R, const float* x, int d,
+                              float* x_out, const half_bits* a, int da, half_bits* a_out);
 // out[i] = fp16(rows[i] / rms(rows[i]) * gamma); rows[i] = x + i*ldx, or rowptr[i] if given
 hipError_t launch_rmsnorm(hipStream_t s, const float* x, int ldx, const float* const* rowptr,
                           int R, const float* gamma, int d, float eps, half_bits* out, int ldo);

@@ -414,6 +414,10 @@ struct Batch {
   int n_work = 0;   // attention work items
   uint16_t* own_kv = nullptr;
   int own_cap = 0;
+  // Tokens whose final hidden state is needed (ws "last"), or 0 = all tokens.
+  // With n_last > 0 the last layer's O-projection and MLP run on those tokens
+  // only, and their final hidden states land in ws "xlast" [n_last][d].
+  int n_last = 0;
 };
 
 // One pass of all layers over the T tokens whose ids/positions/slots and row
@@ -448,26 +452,6 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
     LMOP_TRY(timed(c, "rmsnorm", 0, nbytes_norm, [&] {
       return launch_rmsnorm(c->stream, x, d, nullptr, T, L.attn_norm, d, cf.rms_eps, h, d);
     }));
-    auto gemm = [&](const char* name, const void* A, int lda, const PackedW4& W, int epi,
-                    void* C, int ldc, int n_out) {
-      GemmArgs ga{};
-      ga.A = A;
-      ga.lda = lda;
-      ga.M = T;
-      ga.N = W.np;
-      ga.K = W.kp;
-      ga.bq = W.qpack;
-      ga.bs = W.spack;
-      ga.C = C;
-      ga.ldc = ldc;
-      ga.n_out = n_out;
-      ga.X = x;
-      ga.ldx = d;
-      const double flops = 2.0 * T * W.n * W.k;
-      const double bytes = (double)T * W.k * 2 + (double)W.n * W.k * 0.5625 +
-                           (double)T * W.n * (epi == EPI_ADD_F32 ? 8 : 2);
-      return timed(c, name, flops, bytes, [&] { return launch_gemm_w4(c->stream, ga, epi); });
-    };
     uint16_t* kc = b.own_kv + l * kv_layer;
     uint16_t* vt = kc + (size_t)b.own_cap * c->nkv_dim;
     {
@@ -510,12 +494,46 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
     aa.nkv = cf.n_kv_heads;
     aa.hd = hd;
     LMOP_TRY(timed(c, "attention", 0, 0, [&] { return launch_attention(c->stream, aa); }));
-    LMOP_TRY(gemm("gemm_w4a16_o", att, c->nq_dim, L.o, EPI_ADD_F32, nullptr, 0, d));
-    LMOP_TRY(timed(c, "rmsnorm", 0, nbytes_norm, [&] {
-      return launch_rmsnorm(c->stream, x, d, nullptr, T, L.mlp_norm, d, cf.rms_eps, h, d);
+    // in the last layer only the selected tokens continue (their K/V are written above)
+    int M = T;
+    float* xr = x;
+    uint16_t* ar = att;
+    if (l == cf.n_layers - 1 && b.n_last > 0) {
+      int32_t* last;
+      LMOP_TRY(ws_get(c, "last", b.n_last, &last));
+      LMOP_TRY(ws_get(c, "xlast", (size_t)b.n_last * d, &xr));
+      LMOP_TRY(ws_get(c, "attlast", (size_t)b.n_last * c->nq_dim, &ar));
+      LMOP_TRY(timed(c, "gather_rows", 0, (double)b.n_last * (d * 8 + c->nq_dim * 4), [&] {
+        return launch_gather_rows(c->stream, last, b.n_last, x, d, xr, att, c->nq_dim, ar);
+      }));
+      M = b.n_last;
+    }
+    auto gemm2 = [&](const char* name, const void* A, int lda, const PackedW4& W, int epi,
+                     void* C, int ldc, int n_out) {
+      GemmArgs ga{};
+      ga.A = A;
+      ga.lda = lda;
+      ga.M = M;
+      ga.N = W.np;
+      ga.K = W.kp;
+      ga.bq = W.qpack;
+      ga.bs = W.spack;
+      ga.C = C;
+      ga.ldc = ldc;
+      ga.n_out = n_out;
+      ga.X = xr;
+      ga.ldx = d;
+      const double flops = 2.0 * M * W.n * W.k;
+      const double bytes = (double)M * W.k * 2 + (double)W.n * W.k * 0.5625 +
+                           (double)M * W.n * (epi == EPI_ADD_F32 ? 8 : 2);
+      return timed(c, name, flops, bytes, [&] { return launch_gemm_w4(c->stream, ga, epi); });
+    };
+    LMOP_TRY(gemm2("gemm_w4a16_o", ar, c->nq_dim, L.o, EPI_ADD_F32, nullptr, 0, d));
+    LMOP_TRY(timed(c, "rmsnorm", 0, (double)M * d * 6, [&] {
+      return launch_rmsnorm(c->stream, xr, d, nullptr, M, L.mlp_norm, d, cf.rms_eps, h, d);
     }));
-    LMOP_TRY(gemm("gemm_w4a16_gateup", h, d, L.gu, EPI_SWIGLU, act, c->f64, c->f64));
-    LMOP_TRY(gemm("gemm_w4a16_down", act, c->f64, L.down, EPI_ADD_F32, nullptr, 0, d));
+    LMOP_TRY(gemm2("gemm_w4a16_gateup", h, d, L.gu, EPI_SWIGLU, act, c->f64, c->f64));
+    LMOP_TRY(gemm2("gemm_w4a16_down", act, c->f64, L.down, EPI_ADD_F32, nullptr, 0, d));
   }
   return LMOP_OK;
 }
@@ -523,7 +541,13 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
 // Uploads host-built per-token and per-row arrays for one forward pass.
 lmop_status upload_batch(lmop_ctx* c, const std::vector<int32_t>& tok,
                          const std::vector<int32_t>& pos, const std::vector<int32_t>& slot,
-                         const std::vector<AttnRow>& rows, const std::vector<int2>& work) {
+                         const std::vector<AttnRow>& rows, const std::vector<int2>& work,
+                         const std::vector<int32_t>& last = {}) {
+  if (!last.empty()) {
+    int32_t* dl;
+    LMOP_TRY(ws_get(c, "last", last.size(), &dl));
+    HIP_OK(c, hipMemcpyAsync(dl, last.data(), last.size() * 4, hipMemcpyHostToDevice, c->stream));
+  }
   int32_t *dt, *dp, *ds;
   AttnRow* dr;
   int2* dw;
@@ -917,21 +941,25 @@ lmop_status lmop_set_prefix(lmop_ctx* ctx, const lmop_prefix* parent, const int3
     rows[0].own_q0 = 0;
     std::vector<int2> work;
     add_work(work, 0, n_tokens, cf.n_heads / cf.n_kv_heads);
-    lmop_status st = upload_batch(ctx, tok, pos, slot, rows, work);
+    const std::vector<int32_t> last = {n_tokens - 1};
+    lmop_status st = upload_batch(ctx, tok, pos, slot, rows, work, last);
     Batch b;
     b.T = n_tokens;
     b.R = 1;
     b.n_work = (int)work.size();
     b.own_kv = p->kv;
     b.own_cap = p->cap;
+    b.n_last = 1;
     if (st == LMOP_OK) st = forward(ctx, b);
     if (st == LMOP_OK) {
-      float* x = nullptr;
-      st = ws_get(ctx, "x", (size_t)n_tokens * cf.d_model, &x);
+      // the final hidden state of the last token (the whole model when L = 0)
+      float* src = nullptr;
+      st = cf.n_layers > 0 ? ws_get(ctx, "xlast", (size_t)cf.d_model, &src)
+                           : ws_get(ctx, "x", (size_t)n_tokens * cf.d_model, &src);
+      if (cf.n_layers == 0) src += (size_t)(n_tokens - 1) * cf.d_model;
       if (st == LMOP_OK) {
-        hipError_t e = hipMemcpyAsync(p->hidden, x + (size_t)(n_tokens - 1) * cf.d_model,
-                                      (size_t)cf.d_model * 4, hipMemcpyDeviceToDevice,
-                                      ctx->stream);
+        hipError_t e = hipMemcpyAsync(p->hidden, src, (size_t)cf.d_model * 4,
+                                      hipMemcpyDeviceToDevice, ctx->stream);
         if (e != hipSuccess) st = fail(ctx, LMOP_ERR_DEVICE, "copy of prefix hidden failed");
       }
     }
@@ -1112,20 +1140,35 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
     cap = own_store_cap(cap);
     uint16_t* own_kv;
     LMOP_TRY(ws_get(ctx, "own_kv", (size_t)cf.n_layers * 2 * cap * ctx->nkv_dim, &own_kv, true));
-    LMOP_TRY(upload_batch(ctx, tok, pos, slot, rows, work));
+    // each row's last token (rows with suffix tokens only)
+    std::vector<int32_t> last;
+    std::vector<int> last_of(R, -1);
+    for (int i = 0; i < R; ++i)
+      if (len[i] > 0) {
+        last_of[i] = (int)last.size();
+        last.push_back(qs[i] + len[i] - 1);
+      }
+    LMOP_TRY(upload_batch(ctx, tok, pos, slot, rows, work, last));
     Batch b;
     b.T = T;
     b.R = R;
     b.n_work = (int)work.size();
     b.own_kv = own_kv;
     b.own_cap = cap;
+    b.n_last = cf.n_layers > 0 ? (int)last.size() : 0;
     LMOP_TRY(forward(ctx, b));
     float* x;
-    LMOP_TRY(ws_get(ctx, "x", (size_t)std::max(T, 1) * d, &x));
+    if (b.n_last > 0)
+      LMOP_TRY(ws_get(ctx, "xlast", (size_t)b.n_last * d, &x));
+    else
+      LMOP_TRY(ws_get(ctx, "x", (size_t)std::max(T, 1) * d, &x));
     std::vector<const float*> rowptr(R);
     for (int i = 0; i < R; ++i) {
       const int r = uniq[u0 + i];
-      rowptr[i] = len[i] > 0 ? x + (size_t)(qs[i] + len[i] - 1) * d : pf[r]->hidden;
+      if (len[i] == 0)
+        rowptr[i] = pf[r]->hidden;
+      else
+        rowptr[i] = x + (size_t)(b.n_last > 0 ? last_of[i] : qs[i] + len[i] - 1) * d;
     }
     float* dump = nullptr;
     if (dbg) LMOP_TRY(ws_get(ctx, "dump", (size_t)R * V, &dump));
