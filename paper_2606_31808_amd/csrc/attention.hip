@@ -67,7 +67,8 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
   constexpr int KCH = HD / 8;  // 16-byte chunks per K row
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int g = lane >> 4, c = lane & 15;
   const int2 wk = p.work[blockIdx.x];
   const AttnRow row = p.rows[wk.x];
