@@ -25,6 +25,9 @@ if ROOT not in sys.path:
 
 PEAK_F16_TFLOPS = 2500.0   # MI355X dense fp16/bf16 MFMA
 PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
+GEMM_SRC = os.path.join(ROOT, "paper_2606_31808_amd", "csrc", "gemm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_w4a16_hbm_traffic.json")
+COPY_BYTES = 1 << 30       # plain copy used to calibrate the HBM byte counters
 
 
 def log(*a):
@@ -40,10 +43,63 @@ def gemm_roofline(stats):
     if ms <= 0:
         return None
     ach = fl / (ms * 1e-3) / 1e12
+    algo_bytes = sum(stats[n]["bytes"] for n in names) / launches
     return {"bound": "mfma", "kernel": "gemm_w4a16 (qkv, o, gate/up, down)", "achieved": ach,
             "peak": PEAK_F16_TFLOPS, "unit": "TFLOP/s", "frac": ach / PEAK_F16_TFLOPS,
-            "traffic": None, "launches": launches, "avg_launch_ms": ms / launches,
-            "flops_per_launch": fl / launches}
+            "traffic": measured_traffic(), "algorithmic_bytes_per_launch": algo_bytes,
+            "launches": launches, "avg_launch_ms": ms / launches, "flops_per_launch": fl / launches}
+
+
+def _src_hash():
+    import hashlib
+    with open(GEMM_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per W4A16 GEMM launch from the committed PMC summary, if it was
+    taken on the current kernel source; otherwise None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    return t["bytes_per_launch"] if t.get("gemm_src_sha256_16") == _src_hash() else None
+
+
+def pmc_summary(root):
+    """Turns four rocprofv3 --pmc runs (GEMM FETCH_SIZE / WRITE_SIZE, plain copy
+    FETCH_SIZE / WRITE_SIZE, under `root`) into the traffic summary."""
+    import csv
+    import glob
+
+    def per_kernel(d, counter, pred):
+        tot, n = 0.0, 0
+        for fn in glob.glob(os.path.join(root, d, "*counter_collection.csv")):
+            for r in csv.DictReader(open(fn)):
+                if r["Counter_Name"] == counter and pred(r["Kernel_Name"]):
+                    tot += float(r["Counter_Value"])
+                    n += 1
+        return tot, n
+
+    gemm = lambda k: "gemm_kernel<" in k and ", true," in k
+    copy = lambda k: "copy" in k.lower()
+    f_tot, f_n = per_kernel("pmc_fetch", "FETCH_SIZE", gemm)
+    w_tot, w_n = per_kernel("pmc_write", "WRITE_SIZE", gemm)
+    cf, cfn = per_kernel("pmc_copy_fetch", "FETCH_SIZE", copy)
+    cw, cwn = per_kernel("pmc_copy_write", "WRITE_SIZE", copy)
+    # KiB as counted for a copy that moves COPY_BYTES each way -> bytes per counted KiB
+    kf = COPY_BYTES / (cf / cfn * 1024.0)
+    kw = COPY_BYTES / (cw / cwn * 1024.0)
+    fetch_b = f_tot / f_n * 1024.0 * kf
+    write_b = w_tot / w_n * 1024.0 * kw
+    out = {"gemm_src_sha256_16": _src_hash(), "launches": f_n, "fetch_bytes_per_launch": fetch_b,
+           "write_bytes_per_launch": write_b, "bytes_per_launch": fetch_b + write_b,
+           "copy_scale_fetch": kf, "copy_scale_write": kw,
+           "copy_fetch_kib": cf / cfn, "copy_write_kib": cw / cwn}
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
 
 
 def head_roofline(stats):
@@ -84,7 +140,23 @@ def main():
     ap.add_argument("--batch-tokens", type=int, default=0)
     ap.add_argument("--cpu-rows", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run one plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--pmc-summary", metavar="DIR",
+                    help="summarise the rocprofv3 --pmc runs under DIR and exit")
     args = ap.parse_args()
+    if args.pmc_summary:
+        pmc_summary(args.pmc_summary)
+        return
+    if args.calibrate_copy:
+        import torch
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copied_bytes": COPY_BYTES}))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
         sys.exit(2)
