@@ -211,6 +211,8 @@ __global__ __launch_bounds__(256, Occ<MI>::value) void gemm_kernel(const GemmArg
           w = dequant8(f == 0 ? codes.x : f == 1 ? codes.y : f == 2 ? codes.z : codes.w, s4[f],
                        dq_mask, dq_magic);
         } else {
+          // the head's token tiles can be ragged: skip sub-tiles with no valid token
+          if (n0 + wave * 64 + 16 * f >= p.N) continue;
           const int r = wave * 64 + 16 * f + c;
           w = *(const f16x8*)(sB + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
         }
@@ -325,41 +327,39 @@ __global__ __launch_bounds__(256, Occ<MI>::value) void gemm_kernel(const GemmArg
         }
       }
     }
-  } else {  // EPI_HEAD: per token and 64-column block: (max, sum exp), allowed logits
-    const int n_chunks = (p.N + 63) / 64;
-    const int blk = (n0 >> 6) + wave;
+  } else {  // EPI_HEAD: rows of A are vocabulary entries, rows of B are tokens
+    // per token n and this workgroup's 16*MI-entry vocabulary slice (chunk mt):
+    // (max, sum exp(z - max)), plus the logits of the allowed tokens
+    const int n_chunks = (p.M + BM - 1) / BM;
 #pragma unroll
-    for (int i = 0; i < MI; ++i) {
-      const int m = mrow + 16 * i;
-      float mx = -INFINITY;
+    for (int f = 0; f < 4; ++f)
 #pragma unroll
-      for (int f = 0; f < 4; ++f)
+      for (int r = 0; r < 4; ++r) {
+        const int n = ncol + 16 * f + r;  // token
+        float mx = -INFINITY;
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (ncol + 16 * f + r < p.N) mx = fmaxf(mx, acc[f][i][r]);
-      mx = fmaxf(mx, shfl_xor(mx, 16));
-      mx = fmaxf(mx, shfl_xor(mx, 32));
-      float sm = 0.f;
+        for (int i = 0; i < MI; ++i)
+          if (mrow + 16 * i < p.M) mx = fmaxf(mx, acc[f][i][r]);
 #pragma unroll
-      for (int f = 0; f < 4; ++f)
+        for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, shfl_xor(mx, o));
+        float sm = 0.f;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int n = ncol + 16 * f + r;
-          if (n < p.N) {
+        for (int i = 0; i < MI; ++i) {
+          const int v = mrow + 16 * i;  // vocabulary entry
+          if (v < p.M) {
             const float z = acc[f][i][r];
             sm += __expf(z - mx);
-            if (m < p.M) {
-              const int si = p.sel[n];
-              if (si >= 0) p.zsel[(size_t)m * p.n_sel + si] = z;
-              if (p.dump) p.dump[(size_t)m * p.ld_dump + n] = z;
+            if (n < p.N) {
+              const int si = p.sel[v];
+              if (si >= 0) p.zsel[(size_t)n * p.n_sel + si] = z;
+              if (p.dump) p.dump[(size_t)n * p.ld_dump + v] = z;
             }
           }
         }
-      sm += shfl_xor(sm, 16);
-      sm += shfl_xor(sm, 32);
-      if (g == 0 && m < p.M && blk < n_chunks)
-        p.part[(size_t)m * n_chunks + blk] = make_float2(mx, sm);
-    }
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) sm += shfl_xor(sm, o);
+        if (c == 0 && n < p.N) p.part[(size_t)n * n_chunks + mt] = make_float2(mx, sm);
+      }
   }
 }
 
@@ -403,7 +403,10 @@ hipError_t launch_gemm_w4(hipStream_t s, const GemmArgs& a, int epi) {
 
 hipError_t launch_gemm_f16(hipStream_t s, const GemmArgs& a, int epi) {
   if (a.K % BK != 0 || epi != EPI_HEAD || a.ldb % 8 != 0) return hipErrorInvalidValue;
-  return launch_epi<false, EPI_HEAD>(s, a);
+  // vocabulary along M in 128-entry tiles, tokens in 256-row column tiles; the
+  // column tiles of one vocabulary tile run side by side on one XCD, so the
+  // LM head weight streams from HBM about once
+  return launch_cfg<8, false, EPI_HEAD>(s, a);
 }
 
 }  // namespace lmop

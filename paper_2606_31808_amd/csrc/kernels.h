@@ -27,7 +27,8 @@ enum Epilogue : int {
   EPI_STORE_F16 = 0,  // C[m][n] = fp16(acc)
   EPI_ADD_F32 = 1,    // X[m][n] += acc (residual stream)
   EPI_SWIGLU = 2,     // fused [gate|up] blocks of 32: C[m][j] = fp16(silu(gate_j) * up_j)
-  EPI_HEAD = 3,       // LM head: per-64-column (max, sum exp), allowed-token logits, debug dump
+  EPI_HEAD = 3,       // LM head (A = head weight, B = hidden rows): per token and 128-entry
+                      // vocabulary slice (max, sum exp), allowed-token logits, debug dump
   EPI_QKV = 4         // fused q|k|v: RoPE on q, k; q -> qout, k -> K store, v -> V^T store
 };
 
@@ -47,12 +48,12 @@ struct GemmArgs {
   int n_out;      // EPI_STORE_F16: valid columns; EPI_SWIGLU: output columns written
   float* X;       // fp32 [M][ldx]
   int ldx;
-  // head epilogue
-  float2* part;          // [M][ceil(N/64)] (max, sum exp(z - max))
-  const int32_t* sel;    // [N]: index of the column in the allowed list, or -1
-  float* zsel;           // [M][n_sel]
+  // head epilogue (M = vocabulary, N = tokens)
+  float2* part;          // [N][ceil(M/128)] (max, sum exp(z - max))
+  const int32_t* sel;    // [M]: index of the vocabulary entry in the allowed list, or -1
+  float* zsel;           // [N][n_sel]
   int n_sel;
-  float* dump;           // NULL or fp32 [M][ld_dump]
+  float* dump;           // NULL or fp32 [N][ld_dump]
   int ld_dump;
   // qkv epilogue.  Packed column order: q heads, k heads, v heads; every head
   // is hd/64 blocks of 64 columns; in a q/k block b of a head the columns are

@@ -602,7 +602,8 @@ lmop_status run_head(lmop_ctx* c, int R, const std::vector<const float*>& rowptr
                      std::vector<HeadPick>& picks, float* dump_dev) {
   const lmop_config& cf = c->cfg;
   const int d = cf.d_model, V = cf.vocab;
-  const int n_chunks = (V + 63) / 64;
+  constexpr int kVocabTile = 128;
+  const int n_chunks = (V + kVocabTile - 1) / kVocabTile;
   const float** drp;
   uint16_t* hn;
   float2* part;
@@ -619,23 +620,25 @@ lmop_status run_head(lmop_ctx* c, int R, const std::vector<const float*>& rowptr
   LMOP_TRY(timed(c, "rmsnorm_final", 0, (double)R * d * 6, [&] {
     return launch_rmsnorm(c->stream, nullptr, 0, drp, R, c->final_norm, d, cf.rms_eps, hn, d);
   }));
-  GemmArgs ga{};
-  ga.A = hn;
-  ga.lda = d;
-  ga.M = R;
-  ga.N = V;
-  ga.K = d;
-  ga.bh = c->head;
-  ga.ldb = d;
-  ga.part = part;
-  ga.sel = d_sel;
-  ga.zsel = zsel;
-  ga.n_sel = n_sel;
-  ga.dump = dump_dev;
-  ga.ld_dump = V;
-  LMOP_TRY(timed(c, "head_gemm", 2.0 * R * V * d, (double)V * d * 2 + (double)R * d * 2, [&] {
-    return launch_gemm_f16(c->stream, ga, EPI_HEAD);
-  }));
+  {
+    GemmArgs ga{};
+    ga.A = c->head;
+    ga.lda = d;
+    ga.M = V;
+    ga.N = R;
+    ga.K = d;
+    ga.bh = hn;
+    ga.ldb = d;
+    ga.part = part;
+    ga.sel = d_sel;
+    ga.zsel = zsel;
+    ga.n_sel = n_sel;
+    ga.dump = dump_dev;
+    ga.ld_dump = V;
+    LMOP_TRY(timed(c, "head_gemm", 2.0 * R * V * d, (double)V * d * 2 + (double)R * d * 2, [&] {
+      return launch_gemm_f16(c->stream, ga, EPI_HEAD);
+    }));
+  }
   LMOP_TRY(timed(c, "head_finalize", 0, 0, [&] {
     return launch_head_finalize(c->stream, part, n_chunks, zsel, n_sel, n_allowed, d_allowed, R,
                                 dpk);
