@@ -17,7 +17,9 @@
 // Each wave dequantises its own weight fragments in registers (nibble |
 // 0x6400 = 1024 + u in fp16, minus 1032 gives the exact code, times the fp16
 // scale: one rounding), once per workgroup, and reuses each for all MI token
-// sub-tiles.
+// sub-tiles.  Explicit scheduling groups interleave that dequantisation with
+// the MFMAs (two VALU per MFMA) so the matrix core is not left idle while a
+// wave converts its next fragment.
 //
 // The MFMA takes the weight fragment as its A operand and the activations
 // as its B operand, so the accumulator holds C^T: every lane owns 4
@@ -36,24 +38,28 @@ namespace lmop {
 
 namespace {
 
-// Dequantises the 8 biased codes of one word: nibble pair j (bits 4j and
-// 16+4j) | 0x6400 is fp16 1024 + u; minus 1032 gives the exact code; times
-// the scale gives one rounding.  `mask` and `magic` arrive in registers the
-// compiler cannot see through, so (x & mask) | (magic & ~mask) becomes a
-// single v_bitop3; the four pairs are independent chains the scheduler can
-// interleave with MFMAs.
+// Dequantises the 8 biased codes of one word (nibble p holds feature 2p for
+// p < 4 and 2(p-4)+1 otherwise).  Masking nibbles p and p+4 and or-ing in
+// 0x6400 makes fp16 1024 + u, minus 1032 gives the exact code; masking the
+// next nibble pair in place makes 1024 + 16u, and one fma by 1/16 with -72
+// gives the exact code as well, so one shift by 8 serves all four pairs.
+// Times the scale: one rounding.  `mask` and `magic` arrive in registers the
+// compiler cannot see through, so (x & mask) | magic becomes one v_and_or.
 LMOP_DEVICE f16x8 dequant8(uint32_t w, f16 s, uint32_t mask, uint32_t magic) {
   const f16x2 bias = {(f16)1032.0f, (f16)1032.0f};
+  const f16x2 sixteenth = {(f16)0.0625f, (f16)0.0625f};
+  const f16x2 bias_hi = {(f16)-72.0f, (f16)-72.0f};
   const f16x2 s2 = {s, s};
-  const uint32_t nm = magic & ~mask;
-  const uint32_t t0 = (w & mask) | nm;
-  const uint32_t t1 = ((w >> 4) & mask) | nm;
-  const uint32_t t2 = ((w >> 8) & mask) | nm;
-  const uint32_t t3 = ((w >> 12) & mask) | nm;
+  const uint32_t mask_hi = mask << 4;
+  const uint32_t w8 = w >> 8;
+  const uint32_t t0 = (w & mask) | magic;
+  const uint32_t t1 = (w & mask_hi) | magic;
+  const uint32_t t2 = (w8 & mask) | magic;
+  const uint32_t t3 = (w8 & mask_hi) | magic;
   const f16x2 h0 = (__builtin_bit_cast(f16x2, t0) - bias) * s2;
-  const f16x2 h1 = (__builtin_bit_cast(f16x2, t1) - bias) * s2;
+  const f16x2 h1 = __builtin_elementwise_fma(__builtin_bit_cast(f16x2, t1), sixteenth, bias_hi) * s2;
   const f16x2 h2 = (__builtin_bit_cast(f16x2, t2) - bias) * s2;
-  const f16x2 h3 = (__builtin_bit_cast(f16x2, t3) - bias) * s2;
+  const f16x2 h3 = __builtin_elementwise_fma(__builtin_bit_cast(f16x2, t3), sixteenth, bias_hi) * s2;
   return f16x8{h0.x, h0.y, h1.x, h1.y, h2.x, h2.y, h3.x, h3.y};
 }
 
@@ -187,37 +193,62 @@ __global__ __launch_bounds__(256, Occ<MI>::value) void gemm_kernel(const GemmArg
     const char* sA = smem + (kt % NSTAGE) * C::STAGE;
     const char* sB = sA + C::A_BYTES;
     const char* sS = sB + C::B_BYTES;
+    if constexpr (INT4) {
+      // both 32-feature groups' activation fragments, codes and scales are
+      // read up front; then one weight fragment at a time
+      f16x8 a[2][MI];
+      uint4 codes[2];
+      f16x4 s4[2];
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      // all MI activation fragments of this 32-feature group, then one
-      // weight fragment at a time: its MI MFMAs overlap the next dequant
-      f16x8 a[MI];
+      for (int kk = 0; kk < 2; ++kk) {
 #pragma unroll
-      for (int i = 0; i < MI; ++i) {
-        const int r = 16 * i + c;
-        a[i] = *(const f16x8*)(sA + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
-      }
-      uint4 codes;
-      f16x4 s4;
-      if constexpr (INT4) {
+        for (int i = 0; i < MI; ++i) {
+          const int r = 16 * i + c;
+          a[kk][i] = *(const f16x8*)(sA + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
+        }
         const int q = wave * 2 + kk;
-        codes = *(const uint4*)(sB + q * 1024 + lane * 16);
-        s4 = *(const f16x4*)(sS + q * 128 + c * 8);
+        codes[kk] = *(const uint4*)(sB + q * 1024 + lane * 16);
+        s4[kk] = *(const f16x4*)(sS + q * 128 + c * 8);
       }
 #pragma unroll
-      for (int f = 0; f < 4; ++f) {
-        f16x8 w;
-        if constexpr (INT4) {
-          w = dequant8(f == 0 ? codes.x : f == 1 ? codes.y : f == 2 ? codes.z : codes.w, s4[f],
-                       dq_mask, dq_magic);
-        } else {
+      for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+        for (int f = 0; f < 4; ++f) {
+          const uint32_t cw = f == 0 ? codes[kk].x : f == 1 ? codes[kk].y : f == 2 ? codes[kk].z : codes[kk].w;
+          const f16x8 w = dequant8(cw, s4[kk][f], dq_mask, dq_magic);
+#pragma unroll
+          for (int i = 0; i < MI; ++i) acc[f][i] = mfma16x16x32(w, a[kk][i], acc[f][i]);
+        }
+      }
+      // Schedule: the LDS reads first, then the first fragment's dequant (13
+      // VALU), then every MFMA followed by up to two VALU, so the remaining
+      // dequant work issues while earlier MFMAs run instead of in VALU-only
+      // stretches that leave the matrix core idle.
+      __builtin_amdgcn_sched_group_barrier(0x100, 2 * MI + 4, 0);  // DS reads
+      __builtin_amdgcn_sched_group_barrier(0x002, 13, 0);          // VALU
+#pragma unroll
+      for (int j = 0; j < 8 * MI; ++j) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // VALU
+      }
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        f16x8 a[MI];
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+          const int r = 16 * i + c;
+          a[i] = *(const f16x8*)(sA + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
+        }
+#pragma unroll
+        for (int f = 0; f < 4; ++f) {
           // the head's token tiles can be ragged: skip sub-tiles with no valid token
           if (n0 + wave * 64 + 16 * f >= p.N) continue;
           const int r = wave * 64 + 16 * f + c;
-          w = *(const f16x8*)(sB + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
-        }
+          const f16x8 w = *(const f16x8*)(sB + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
 #pragma unroll
-        for (int i = 0; i < MI; ++i) acc[f][i] = mfma16x16x32(w, a[i], acc[f][i]);
+          for (int i = 0; i < MI; ++i) acc[f][i] = mfma16x16x32(w, a[i], acc[f][i]);
+        }
       }
     }
   }
