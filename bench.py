@@ -67,39 +67,88 @@ def measured_traffic():
     return t["bytes_per_launch"] if t.get("gemm_src_sha256_16") == _src_hash() else None
 
 
+def _bench_line(log_path):
+    """The JSON line a bench run printed (its stdout went to log_path)."""
+    with open(log_path) as f:
+        lines = [l for l in f if l.startswith("{")]
+    return json.loads(lines[-1])
+
+
+def _is_w4_gemm(name):
+    return "gemm_kernel<" in name and ", true," in name
+
+
+def _timed_gemm_rows(rows, n_timed):
+    """The last n_timed W4A16 GEMM dispatches: the timed steps come after the
+    shared-prefix pass and the warmup, so these are exactly the timed launches."""
+    g = sorted((r for r in rows if _is_w4_gemm(r["Kernel_Name"])), key=lambda r: int(r["Dispatch_Id"]))
+    return g[-n_timed:]
+
+
 def pmc_summary(root):
-    """Turns four rocprofv3 --pmc runs (GEMM FETCH_SIZE / WRITE_SIZE, plain copy
-    FETCH_SIZE / WRITE_SIZE, under `root`) into the traffic summary."""
+    """Turns four rocprofv3 --pmc runs (GEMM FETCH_SIZE / WRITE_SIZE over one
+    timed step, plain copy FETCH_SIZE / WRITE_SIZE, under `root`) into the
+    traffic summary."""
     import csv
     import glob
 
-    def per_kernel(d, counter, pred):
-        tot, n = 0.0, 0
+    def rows(d):
+        out = []
         for fn in glob.glob(os.path.join(root, d, "*counter_collection.csv")):
-            for r in csv.DictReader(open(fn)):
-                if r["Counter_Name"] == counter and pred(r["Kernel_Name"]):
-                    tot += float(r["Counter_Value"])
-                    n += 1
-        return tot, n
+            out.extend(csv.DictReader(open(fn)))
+        return out
 
-    gemm = lambda k: "gemm_kernel<" in k and ", true," in k
-    copy = lambda k: "copy" in k.lower()
-    f_tot, f_n = per_kernel("pmc_fetch", "FETCH_SIZE", gemm)
-    w_tot, w_n = per_kernel("pmc_write", "WRITE_SIZE", gemm)
-    cf, cfn = per_kernel("pmc_copy_fetch", "FETCH_SIZE", copy)
-    cw, cwn = per_kernel("pmc_copy_write", "WRITE_SIZE", copy)
+    def gemm_mean(d, counter):
+        n = _bench_line(os.path.join(root, d + ".log"))["roofline"]["launches"]
+        sel = _timed_gemm_rows([r for r in rows(d) if r["Counter_Name"] == counter], n)
+        assert len(sel) == n, (d, len(sel), n)
+        return sum(float(r["Counter_Value"]) for r in sel) / n, n
+
+    def copy_mean(d, counter):
+        v = [float(r["Counter_Value"]) for r in rows(d)
+             if r["Counter_Name"] == counter and "copy" in r["Kernel_Name"].lower()]
+        return sum(v) / len(v)
+
+    f_kib, f_n = gemm_mean("pmc_fetch", "FETCH_SIZE")
+    w_kib, _ = gemm_mean("pmc_write", "WRITE_SIZE")
+    cf = copy_mean("pmc_copy_fetch", "FETCH_SIZE")
+    cw = copy_mean("pmc_copy_write", "WRITE_SIZE")
     # KiB as counted for a copy that moves COPY_BYTES each way -> bytes per counted KiB
-    kf = COPY_BYTES / (cf / cfn * 1024.0)
-    kw = COPY_BYTES / (cw / cwn * 1024.0)
-    fetch_b = f_tot / f_n * 1024.0 * kf
-    write_b = w_tot / w_n * 1024.0 * kw
+    kf = COPY_BYTES / (cf * 1024.0)
+    kw = COPY_BYTES / (cw * 1024.0)
+    fetch_b = f_kib * 1024.0 * kf
+    write_b = w_kib * 1024.0 * kw
     out = {"gemm_src_sha256_16": _src_hash(), "launches": f_n, "fetch_bytes_per_launch": fetch_b,
            "write_bytes_per_launch": write_b, "bytes_per_launch": fetch_b + write_b,
            "copy_scale_fetch": kf, "copy_scale_write": kw,
-           "copy_fetch_kib": cf / cfn, "copy_write_kib": cw / cwn}
+           "copy_fetch_kib": cf, "copy_write_kib": cw}
     with open(TRAFFIC_FILE, "w") as f:
         json.dump(out, f, indent=1)
     print(json.dumps(out))
+
+
+def trace_summary(root):
+    """Per-kernel durations of the timed W4A16 GEMM launches from a
+    `rocprofv3 --kernel-trace` run of the default bench command (trace under
+    root/prof_full, the bench line in root/prof_full.json)."""
+    import csv
+    import glob
+    res = _bench_line(os.path.join(root, "prof_full.json"))
+    n = res["roofline"]["launches"]
+    rows = []
+    for fn in glob.glob(os.path.join(root, "prof_full", "*kernel_trace.csv")):
+        rows.extend(csv.DictReader(open(fn)))
+    sel = _timed_gemm_rows(rows, n)
+    dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-6
+    by = {}
+    for r in sel:
+        by.setdefault(r["Kernel_Name"], []).append(dur(r))
+    total = sum(sum(v) for v in by.values())
+    print(f"timed W4A16 GEMM launches: {len(sel)} (bench: {n})")
+    for k, v in sorted(by.items()):
+        print(f"  {k}: {len(v)} launches, avg {sum(v) / len(v):.4f} ms")
+    print(f"family average: trace {total / len(sel):.4f} ms, bench HIP events "
+          f"{res['roofline']['avg_launch_ms']:.4f} ms")
 
 
 def head_roofline(stats):
@@ -144,9 +193,14 @@ def main():
                     help="only run one plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--pmc-summary", metavar="DIR",
                     help="summarise the rocprofv3 --pmc runs under DIR and exit")
+    ap.add_argument("--trace-summary", metavar="DIR",
+                    help="summarise the rocprofv3 --kernel-trace run under DIR and exit")
     args = ap.parse_args()
     if args.pmc_summary:
         pmc_summary(args.pmc_summary)
+        return
+    if args.trace_summary:
+        trace_summary(args.trace_summary)
         return
     if args.calibrate_copy:
         import torch
