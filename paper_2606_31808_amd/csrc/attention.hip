@@ -14,9 +14,12 @@
 // Workgroup = one (row, 128-query-vector tile, kv head); a query vector is
 // a (token, head-in-group) pair, so the G heads sharing a kv head share all
 // K/V tile reads.  Keys are walked segment by segment (root prefix, child
-// prefix, own) in blocks of 64 through a two-stage LDS ring.  Each wave
-// owns 32 query vectors and keeps an online softmax (fp32 running max and
-// sum, base-2 exponent).  Scores are computed transposed, S^T = K Q^T, so
+// prefix, own) in blocks of 64 through a two-stage LDS ring (one barrier per
+// block: the next block's loads are issued right after it).  Each wave owns
+// 32 query vectors and keeps an online softmax (fp32 reference maximum and
+// sum, base-2 exponent); the reference maximum moves only when a score
+// exceeds it by a wide margin, so the running output is rarely rescaled.
+// Waves whose query vectors all lie past the row's end only help load.  Scores are computed transposed, S^T = K Q^T, so
 // the MFMA result layout of P^T is directly the B operand of O^T = V^T P^T
 // and every lane holds values of exactly one query.
 #include "common.h"
@@ -46,13 +49,6 @@ LMOP_DEVICE int kswz(int key) {
 }
 LMOP_DEVICE int vswz(int row) { return row & 7; }
 
-struct Seg {
-  const f16* kbase;  // layer's K [C][nkv][hd]
-  const f16* vbase;  // layer's V^T [nkv][hd][C]
-  int cap;           // C
-  int start;         // first slot of the segment
-  int n;             // keys needed from the segment
-};
 
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float scale_log2) {
@@ -61,7 +57,6 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
   constexpr int STAGE = K_BYTES + V_BYTES;
   constexpr int K_LOADS = K_BYTES / 1024 / 4;  // per wave
   constexpr int V_LOADS = V_BYTES / 1024 / 4;
-  constexpr int LOADS = K_LOADS + V_LOADS;
   constexpr int NS = HD / 32;  // k-steps of the score MFMA
   constexpr int NT = HD / 16;  // 16-dim output tiles
   constexpr int KCH = HD / 8;  // 16-byte chunks per K row
@@ -79,23 +74,35 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
   // segments: root prefix, child prefix, own tokens
   int t_last = (wk.y * QT + QT - 1) / G;
   if (t_last > row.n_q - 1) t_last = row.n_q - 1;
-  Seg seg[3];
+  // segment s: keys [start, start + n) of a store with capacity cap (K at
+  // kb_s, V^T at vb_s).  Kept as separate scalars and chosen with selects: an
+  // array indexed by the runtime segment number would live in scratch memory.
+  const f16* kb_s[3];
+  const f16* vb_s[3];
+  int cap_s[3], start_s[3], n_s[3];
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
     const int cap = row.seg_cap[s];
     const f16* base = (const f16*)row.seg_kv[s] + (size_t)p.layer * 2 * cap * kvdim;
-    seg[s] = Seg{base, base + (size_t)cap * kvdim, cap, 0, row.seg_n[s]};
+    kb_s[s] = base;
+    vb_s[s] = base + (size_t)cap * kvdim;
+    cap_s[s] = cap;
+    start_s[s] = 0;
+    n_s[s] = row.seg_n[s];
   }
   {
     const f16* base = (const f16*)p.own_kv + (size_t)p.layer * 2 * p.own_cap * kvdim;
-    seg[2] = Seg{base, base + (size_t)p.own_cap * kvdim, p.own_cap, row.own_slot,
-                 row.own_q0 + t_last + 1};
+    kb_s[2] = base;
+    vb_s[2] = base + (size_t)p.own_cap * kvdim;
+    cap_s[2] = p.own_cap;
+    start_s[2] = row.own_slot;
+    n_s[2] = row.own_q0 + t_last + 1;
   }
   // own keys visible to every valid query of the workgroup (first token's count)
   int t_first = (wk.y * QT) / G;
   const int vis_min = row.own_q0 + t_first + 1;
-  const int nb0 = (seg[0].n + KB - 1) / KB, nb1 = (seg[1].n + KB - 1) / KB;
-  const int nb2 = (seg[2].n + KB - 1) / KB;
+  const int nb0 = (n_s[0] + KB - 1) / KB, nb1 = (n_s[1] + KB - 1) / KB;
+  const int nb2 = (n_s[2] + KB - 1) / KB;
   const int NB = nb0 + nb1 + nb2;
   const int P = row.seg_n[0] + row.seg_n[1];
 
@@ -116,7 +123,10 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
   auto issue = [&](int st, int b) {
     int s, kb;
     locate(b, s, kb);
-    const Seg& sg = seg[s];
+    const f16* kbase = s == 0 ? kb_s[0] : s == 1 ? kb_s[1] : kb_s[2];
+    const f16* vbase = s == 0 ? vb_s[0] : s == 1 ? vb_s[1] : vb_s[2];
+    const int scap = s == 0 ? cap_s[0] : s == 1 ? cap_s[1] : cap_s[2];
+    const int sstart = s == 0 ? start_s[0] : s == 1 ? start_s[1] : start_s[2];
     char* sK = smem + st * STAGE;
     char* sV = sK + K_BYTES;
 #pragma unroll
@@ -124,7 +134,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
       const int q = wave + 4 * i;                // 1 KB = 1024 / (2*HD) keys
       const int key = q * (512 / HD) + lane / KCH;
       const int chunk = (lane % KCH) ^ kswz<HD>(key);
-      const f16* src = sg.kbase + (size_t)(sg.start + kb + key) * kvdim + h * HD + chunk * 8;
+      const f16* src = kbase + (size_t)(sstart + kb + key) * kvdim + h * HD + chunk * 8;
       g2l16(src, sK + q * 1024);
     }
 #pragma unroll
@@ -132,7 +142,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
       const int q = wave + 4 * i;  // 8 dim rows of 128 bytes
       const int dim = q * 8 + (lane >> 3);
       const int chunk = (lane & 7) ^ vswz(dim);
-      const f16* src = sg.vbase + (size_t)(h * HD + dim) * sg.cap + sg.start + kb + chunk * 8;
+      const f16* src = vbase + (size_t)(h * HD + dim) * scap + sstart + kb + chunk * 8;
       g2l16(src, sV + q * 1024);
     }
   };
@@ -166,21 +176,23 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
 #pragma unroll
     for (int i = 0; i < NT; ++i) o[qs][i] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run[2] = {-1e30f, -1e30f}, l_run[2] = {0.f, 0.f};
+  const float thr = 8.0f / scale_log2;
 
+  // a wave whose query vectors all lie past the row's end only helps load
+  const bool wave_active = wk.y * QT + wave * QW < row.n_q * G;
   issue(0, 0);
   for (int b = 0; b < NB; ++b) {
-    if (b + 1 < NB) {
-      issue((b + 1) & 1, b + 1);
-      wait_vmcnt<LOADS>();
-    } else {
-      wait_vmcnt<0>();
-    }
+    // block b is in LDS for every wave, and every wave is done with block
+    // b-1, whose stage the next issue refills
+    wait_vmcnt<0>();
     barrier();
+    if (b + 1 < NB) issue((b + 1) & 1, b + 1);
+    if (!wave_active) continue;
     int s, kb;
     locate(b, s, kb);
     const char* sK = smem + (b & 1) * STAGE;
     const char* sV = sK + K_BYTES;
-    const int seg_n = seg[s].n;
+    const int seg_n = s == 0 ? n_s[0] : s == 1 ? n_s[1] : n_s[2];
 
     // S^T tiles kt = 2*kc + hf: register r of lane group g holds key
     // kb + 32*kc + 8g + 4hf + r, query (qs, c)
@@ -201,7 +213,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
     }
     // online softmax; scores stay unscaled, p = 2^(s*c - m*c) with c = log2(e)/sqrt(hd).
     // Blocks whose every key is visible to every query of the workgroup skip
-    // the mask; the running output is rescaled only when some maximum moved.
+    // the mask.
     const bool need_mask = kb + KB > seg_n || (s == 2 && kb + KB > vis_min);
     f16x8 pb[2][2];
 #pragma unroll
@@ -223,8 +235,19 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
         for (int r = 0; r < 4; ++r) mb = fmaxf(mb, st[qs][kt][r]);
       mb = fmaxf(mb, shfl_xor(mb, 16));
       mb = fmaxf(mb, shfl_xor(mb, 32));
-      const float m_new = fmaxf(m_run[qs], mb);
-      const float nmc = -m_new * scale_log2;
+      // The reference maximum moves only where a score exceeds it by more than
+      // 8 / c, so p = 2^(s*c - m*c) stays below 2^8 and the running output is
+      // rescaled only on such (rare) blocks.
+      const bool grow = mb > m_run[qs] + thr;
+      if (__any(grow)) {
+        const float m_new = grow ? mb : m_run[qs];
+        const float alpha = __builtin_amdgcn_exp2f((m_run[qs] - m_new) * scale_log2);
+        l_run[qs] *= alpha;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) o[qs][i] *= alpha;
+        m_run[qs] = m_new;
+      }
+      const float nmc = -m_run[qs] * scale_log2;
       float ps = 0.f;
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
@@ -234,15 +257,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
           ps += e;
           pb[qs][kt >> 1][(kt & 1) * 4 + r] = (f16)e;
         }
-      if (__all(m_new == m_run[qs])) {
-        l_run[qs] += ps;
-      } else {
-        const float alpha = __builtin_amdgcn_exp2f((m_run[qs] - m_new) * scale_log2);
-        l_run[qs] = l_run[qs] * alpha + ps;
-#pragma unroll
-        for (int i = 0; i < NT; ++i) o[qs][i] *= alpha;
-      }
-      m_run[qs] = m_new;
+      l_run[qs] += ps;
     }
     // O^T += V^T P^T over two 32-key chunks; lane group g's operand is keys
     // 32kc + 8g .. +7 of V^T row `dim`, one 16-byte chunk
@@ -256,7 +271,6 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
         for (int qs = 0; qs < 2; ++qs) o[qs][i] = mfma16x16x32(a, pb[qs][kc], o[qs][i]);
       }
     }
-    barrier();  // the next issue overwrites this stage
   }
 
 #pragma unroll
