@@ -26,6 +26,10 @@
 // consecutive output columns of one token, which makes the epilogue's
 // stores 8-byte (fp16) or 16-byte (fp32) vectors.
 //
+// The LM head (fp16 weight, M = vocabulary, N = tokens) has 4 or 8 waves (8:
+// one LDS tile of the head weight serves up to 512 token rows); its token
+// rows are private to a wave and go from global memory straight to registers.
+//
 // Workgroups are mapped to tiles XCD-aware: the hardware deals workgroups to
 // the 8 XCDs round-robin, so each XCD is given one contiguous range of
 // tiles, ordered in groups of GM token tiles so that concurrently running
@@ -71,21 +75,28 @@ LMOP_DEVICE float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf
 LMOP_DEVICE int swz(int row) { return row & 7; }
 
 constexpr int BK = 64;
-constexpr int BN = 256;    // 4 waves x 64 columns
+constexpr int BN4 = 256;   // int4 GEMMs: 4 waves x 64 columns
 constexpr int GM = 8;      // token tiles per L2 group
 constexpr int NSTAGE = 3;  // LDS ring depth
 
-template <int MI, bool INT4>
+template <int MI, bool INT4, int NW_ = 4>
 struct Cfg {
+  // waves per workgroup, side by side along N (64 columns each): 4 for the
+  // int4 GEMMs; 4 or 8 for the LM head (8: up to 512 token rows share each
+  // LDS tile of the head weight)
+  static constexpr int NW = NW_;
+  static constexpr int BN = 64 * NW;
   static constexpr int BM = 16 * MI;
   static constexpr int A_BYTES = BM * 128;
-  static constexpr int B_BYTES = INT4 ? BN * 32 : BN * 128;
+  // the fp16 operand of the LM head is private to each wave and goes from
+  // global memory straight to registers, so it takes no LDS
+  static constexpr int B_BYTES = INT4 ? BN * 32 : 0;
   static constexpr int S_BYTES = INT4 ? 1024 : 0;
   static constexpr int STAGE = A_BYTES + B_BYTES + S_BYTES;
   static constexpr int LDS = NSTAGE * STAGE;
   // global->LDS instructions one wave issues per K step (A rows, weight tile, scales)
-  static constexpr int A_LOADS = (BM / 8 + 3) / 4;
-  static constexpr int B_LOADS = INT4 ? BN / 32 / 4 : BN / 8 / 4;
+  static constexpr int A_LOADS = (BM / 8 + NW - 1) / NW;
+  static constexpr int B_LOADS = INT4 ? BN / 32 / NW : 0;
   static constexpr int LOADS = A_LOADS + B_LOADS + (INT4 ? 1 : 0);
 };
 
@@ -98,10 +109,11 @@ struct Occ {
   static constexpr int value = MI >= 16 ? 1 : 2;
 };
 
-template <int MI, bool INT4, int EPI>
-__global__ __launch_bounds__(256, Occ<MI>::value) void gemm_kernel(const GemmArgs p) {
-  using C = Cfg<MI, INT4>;
-  constexpr int BM = C::BM;
+template <int MI, bool INT4, int EPI, int NW_ = 4>
+__global__ __launch_bounds__((64 * NW_), (NW_ == 4 ? Occ<MI>::value : 1)) void gemm_kernel(
+    const GemmArgs p) {
+  using C = Cfg<MI, INT4, NW_>;
+  constexpr int BM = C::BM, BN = C::BN, NW = C::NW;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -135,7 +147,7 @@ __global__ __launch_bounds__(256, Occ<MI>::value) void gemm_kernel(const GemmArg
     char* sS = sB + C::B_BYTES;
 #pragma unroll
     for (int i = 0; i < C::A_LOADS; ++i) {
-      int q = wave + 4 * i;  // 8 rows per instruction
+      int q = wave + NW * i;  // 8 rows per instruction
       if (q >= BM / 8) q = BM / 8 - 1;  // surplus waves repeat the last rows
       const int r = q * 8 + (lane >> 3);
       const int chunk = (lane & 7) ^ swz(r);
@@ -147,7 +159,7 @@ __global__ __launch_bounds__(256, Occ<MI>::value) void gemm_kernel(const GemmArg
       const size_t nb0 = (size_t)(n0 >> 6);
 #pragma unroll
       for (int i = 0; i < C::B_LOADS; ++i) {  // (64-column block, group) pairs
-        const int q = wave + 4 * i;
+        const int q = wave + NW * i;
         const size_t blk = (nb0 + (q >> 1)) * KG + kt * 2 + (q & 1);
         g2l16((const char*)p.bq + blk * 1024 + lane * 16, sB + q * 1024);
       }
@@ -155,16 +167,6 @@ __global__ __launch_bounds__(256, Occ<MI>::value) void gemm_kernel(const GemmArg
         const int pi = lane >> 3;
         const size_t blk = (nb0 + (pi >> 1)) * KG + kt * 2 + (pi & 1);
         if ((lane >> 4) == wave) g2l16((const char*)p.bs + blk * 128 + (lane & 7) * 16, sS);
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < C::B_LOADS; ++i) {
-        const int q = wave + 4 * i;
-        const int r = q * 8 + (lane >> 3);
-        const int chunk = (lane & 7) ^ swz(r);
-        int gn = n0 + r;
-        gn = gn < p.N ? gn : p.N - 1;
-        g2l16((const f16*)p.bh + (size_t)gn * p.ldb + kt * BK + chunk * 8, sB + q * 1024);
       }
     }
   };
@@ -180,58 +182,92 @@ __global__ __launch_bounds__(256, Occ<MI>::value) void gemm_kernel(const GemmArg
 #pragma unroll
     for (int i = 0; i < MI; ++i) acc[f][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  issue(0, 0);
-  if (KT > 1) issue(1, 1);
-  for (int kt = 0; kt < KT; ++kt) {
-    // this step's stage is complete once at most the next step's loads are in flight
-    if (kt + 1 < KT)
-      wait_vmcnt<C::LOADS>();
-    else
-      wait_vmcnt<0>();
-    barrier();
-    if (kt + 2 < KT) issue((kt + 2) % NSTAGE, kt + 2);
-    const char* sA = smem + (kt % NSTAGE) * C::STAGE;
-    const char* sB = sA + C::A_BYTES;
-    const char* sS = sB + C::B_BYTES;
-    if constexpr (INT4) {
-      // both 32-feature groups' activation fragments, codes and scales are
-      // read up front; then one weight fragment at a time
-      f16x8 a[2][MI];
-      uint4 codes[2];
-      f16x4 s4[2];
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-#pragma unroll
-        for (int i = 0; i < MI; ++i) {
-          const int r = 16 * i + c;
-          a[kk][i] = *(const f16x8*)(sA + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
+  if constexpr (INT4) {
+    issue(0, 0);
+    if (KT > 1) issue(1, 1);
+    for (int kt = 0; kt < KT; ++kt) {
+      // this step's stage is complete once at most the next step's loads are in flight
+      if (kt + 1 < KT)
+        wait_vmcnt<C::LOADS>();
+      else
+        wait_vmcnt<0>();
+      barrier();
+      if (kt + 2 < KT) issue((kt + 2) % NSTAGE, kt + 2);
+      const char* sA = smem + (kt % NSTAGE) * C::STAGE;
+      const char* sB = sA + C::A_BYTES;
+      const char* sS = sB + C::B_BYTES;
+        // both 32-feature groups' activation fragments, codes and scales are
+        // read up front; then one weight fragment at a time
+        f16x8 a[2][MI];
+        uint4 codes[2];
+        f16x4 s4[2];
+  #pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+  #pragma unroll
+          for (int i = 0; i < MI; ++i) {
+            const int r = 16 * i + c;
+            a[kk][i] = *(const f16x8*)(sA + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
+          }
+          const int q = wave * 2 + kk;
+          codes[kk] = *(const uint4*)(sB + q * 1024 + lane * 16);
+          s4[kk] = *(const f16x4*)(sS + q * 128 + c * 8);
         }
-        const int q = wave * 2 + kk;
-        codes[kk] = *(const uint4*)(sB + q * 1024 + lane * 16);
-        s4[kk] = *(const f16x4*)(sS + q * 128 + c * 8);
-      }
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-#pragma unroll
-        for (int f = 0; f < 4; ++f) {
-          const uint32_t cw = f == 0 ? codes[kk].x : f == 1 ? codes[kk].y : f == 2 ? codes[kk].z : codes[kk].w;
-          const f16x8 w = dequant8(cw, s4[kk][f], dq_mask, dq_magic);
-#pragma unroll
-          for (int i = 0; i < MI; ++i) acc[f][i] = mfma16x16x32(w, a[kk][i], acc[f][i]);
+  #pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+  #pragma unroll
+          for (int f = 0; f < 4; ++f) {
+            const uint32_t cw = f == 0 ? codes[kk].x : f == 1 ? codes[kk].y : f == 2 ? codes[kk].z : codes[kk].w;
+            const f16x8 w = dequant8(cw, s4[kk][f], dq_mask, dq_magic);
+  #pragma unroll
+            for (int i = 0; i < MI; ++i) acc[f][i] = mfma16x16x32(w, a[kk][i], acc[f][i]);
+          }
         }
-      }
-      // Schedule: the LDS reads first, then the first fragment's dequant (13
-      // VALU), then every MFMA followed by up to two VALU, so the remaining
-      // dequant work issues while earlier MFMAs run instead of in VALU-only
-      // stretches that leave the matrix core idle.
-      __builtin_amdgcn_sched_group_barrier(0x100, 2 * MI + 4, 0);  // DS reads
-      __builtin_amdgcn_sched_group_barrier(0x002, 13, 0);          // VALU
+        // Schedule: the LDS reads first, then the first fragment's dequant (13
+        // VALU), then every MFMA followed by up to two VALU, so the remaining
+        // dequant work issues while earlier MFMAs run instead of in VALU-only
+        // stretches that leave the matrix core idle.
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * MI + 4, 0);  // DS reads
+        __builtin_amdgcn_sched_group_barrier(0x002, 13, 0);          // VALU
+  #pragma unroll
+        for (int j = 0; j < 8 * MI; ++j) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // VALU
+        }
+    }
+  } else {
+    // LM head: the vocabulary tile (A) streams through the LDS ring; each
+    // wave's 64 token rows (B) are loaded from global memory into registers
+    // one K step ahead.  Within a step the token loads are issued before the
+    // next stage's LDS loads, so the same vmcnt wait covers both.  Rows past
+    // the last token load the last token (their results are never stored).
+    const f16* brow[4];
 #pragma unroll
-      for (int j = 0; j < 8 * MI; ++j) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // VALU
-      }
-    } else {
+    for (int f = 0; f < 4; ++f) {
+      int r = n0 + wave * 64 + 16 * f + c;
+      r = r < p.N ? r : p.N - 1;
+      brow[f] = (const f16*)p.bh + (size_t)r * p.ldb + 8 * g;
+    }
+    // a wave whose 64 token rows all lie past the last token only helps load
+    // the shared vocabulary tile (the vmcnt waits count that tile's loads
+    // only, so skipping the token loads keeps them valid)
+    const bool wave_active = n0 + wave * 64 < p.N;
+    auto load_b = [&](f16x8(&bb)[2][4], int kt) {
+      if (!wave_active) return;
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int f = 0; f < 4; ++f) bb[kk][f] = *(const f16x8*)(brow[f] + kt * BK + kk * 32);
+    };
+    auto step = [&](int kt, const f16x8(&bc)[2][4], f16x8(&bn)[2][4]) {
+      if (kt + 1 < KT)
+        wait_vmcnt<C::LOADS>();
+      else
+        wait_vmcnt<0>();
+      barrier();
+      if (kt + 1 < KT) load_b(bn, kt + 1);
+      if (kt + 2 < KT) issue((kt + 2) % NSTAGE, kt + 2);
+      if (!wave_active) return;
+      const char* sA = smem + (kt % NSTAGE) * C::STAGE;
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
         f16x8 a[MI];
@@ -242,14 +278,20 @@ __global__ __launch_bounds__(256, Occ<MI>::value) void gemm_kernel(const GemmArg
         }
 #pragma unroll
         for (int f = 0; f < 4; ++f) {
-          // the head's token tiles can be ragged: skip sub-tiles with no valid token
+          // ragged token tiles: skip sub-tiles with no valid token
           if (n0 + wave * 64 + 16 * f >= p.N) continue;
-          const int r = wave * 64 + 16 * f + c;
-          const f16x8 w = *(const f16x8*)(sB + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
 #pragma unroll
-          for (int i = 0; i < MI; ++i) acc[f][i] = mfma16x16x32(w, a[i], acc[f][i]);
+          for (int i = 0; i < MI; ++i) acc[f][i] = mfma16x16x32(bc[kk][f], a[i], acc[f][i]);
         }
       }
+    };
+    f16x8 b0[2][4], b1[2][4];
+    issue(0, 0);
+    load_b(b0, 0);
+    if (KT > 1) issue(1, 1);
+    for (int kt = 0; kt < KT; kt += 2) {
+      step(kt, b0, b1);
+      if (kt + 1 < KT) step(kt + 1, b1, b0);
     }
   }
 
@@ -394,19 +436,18 @@ __global__ __launch_bounds__(256, Occ<MI>::value) void gemm_kernel(const GemmArg
   }
 }
 
-template <int MI, bool INT4, int EPI>
+template <int MI, bool INT4, int EPI, int NW = 4>
 hipError_t launch_cfg(hipStream_t s, const GemmArgs& a) {
-  using C = Cfg<MI, INT4>;
-  const int tiles = ((a.M + C::BM - 1) / C::BM) * ((a.N + BN - 1) / BN);
+  using C = Cfg<MI, INT4, NW>;
+  const int tiles = ((a.M + C::BM - 1) / C::BM) * ((a.N + C::BN - 1) / C::BN);
   if (tiles == 0) return hipSuccess;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<MI, INT4, EPI>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  hipLaunchKernelGGL((gemm_kernel<MI, INT4, EPI>), dim3(tiles), dim3(256), C::LDS, s, a);
+  // set once per instantiation (a function-local static is initialised once,
+  // also when several threads launch)
+  static const hipError_t attr = hipFuncSetAttribute(
+      (const void*)gemm_kernel<MI, INT4, EPI, NW>, hipFuncAttributeMaxDynamicSharedMemorySize,
+      C::LDS);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((gemm_kernel<MI, INT4, EPI, NW>), dim3(tiles), dim3(64 * NW), C::LDS, s, a);
   return hipGetLastError();
 }
 
@@ -434,10 +475,13 @@ hipError_t launch_gemm_w4(hipStream_t s, const GemmArgs& a, int epi) {
 
 hipError_t launch_gemm_f16(hipStream_t s, const GemmArgs& a, int epi) {
   if (a.K % BK != 0 || epi != EPI_HEAD || a.ldb % 8 != 0) return hipErrorInvalidValue;
-  // vocabulary along M in 128-entry tiles, tokens in 256-row column tiles; the
-  // column tiles of one vocabulary tile run side by side on one XCD, so the
-  // LM head weight streams from HBM about once
-  return launch_cfg<8, false, EPI_HEAD>(s, a);
+  // vocabulary along M in 128-entry tiles, tokens in 256- or 512-row column
+  // tiles; the column tiles of one vocabulary tile run side by side on one
+  // XCD, so the LM head weight streams from HBM about once
+  // up to 256 token rows: 4 waves (two workgroups per CU stream the weight);
+  // more: 8 waves, so up to 512 rows share each weight tile
+  if (a.N <= 256) return launch_cfg<8, false, EPI_HEAD, 4>(s, a);
+  return launch_cfg<8, false, EPI_HEAD, 8>(s, a);
 }
 
 }  // namespace lmop
