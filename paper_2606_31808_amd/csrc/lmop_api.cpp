@@ -15,6 +15,7 @@
 #include <memory>
 #include <set>
 #include <string>
+#include <type_traits>
 #include <unordered_map>
 #include <vector>
 
@@ -96,6 +97,17 @@ struct lmop_ctx {
 
   std::set<lmop_prefix*> prefixes;
 
+  // pinned host staging for batch uploads and result readback: two slots, so
+  // that one batch's host-side packing overlaps the previous batch on the GPU
+  struct Staging {
+    char* p = nullptr;
+    size_t bytes = 0;
+    size_t used = 0;            // bump offset within the current use
+    hipEvent_t done = nullptr;  // recorded after the slot's last device access
+    bool pending = false;
+  };
+  Staging stage[2];
+
   // profiling
   bool prof = false;
   std::vector<hipEvent_t> ev_free;
@@ -163,6 +175,58 @@ lmop_status ws_get(lmop_ctx* c, const char* name, size_t count, T** out, bool ze
   }
   *out = (T*)slot.first;
   return LMOP_OK;
+}
+
+// ---------------------------------------------------------------- staging
+// Makes slot `k` ready for a new batch of at most `need` bytes: waits until
+// the device is done with its previous contents, grows it if needed.
+lmop_status stage_begin(lmop_ctx* c, int k, size_t need) {
+  auto& st = c->stage[k];
+  if (st.pending) {
+    HIP_OK(c, hipEventSynchronize(st.done));
+    st.pending = false;
+  }
+  if (!st.done) HIP_OK(c, hipEventCreateWithFlags(&st.done, hipEventDisableTiming));
+  if (st.bytes < need) {
+    if (st.p) HIP_OK(c, hipHostFree(st.p));
+    st.p = nullptr;
+    st.bytes = 0;
+    const size_t want = need + need / 4;
+    void* q = nullptr;
+    HIP_OK(c, hipHostMalloc(&q, want, hipHostMallocDefault));
+    st.p = (char*)q;
+    st.bytes = want;
+  }
+  st.used = 0;
+  return LMOP_OK;
+}
+
+// Copies n elements into slot k (16-byte aligned) and returns the pinned copy.
+template <typename T>
+lmop_status stage_put(lmop_ctx* c, int k, const T* src, size_t n, T** out) {
+  auto& st = c->stage[k];
+  const size_t off = (st.used + 15) & ~(size_t)15;
+  if (off + n * sizeof(T) > st.bytes)
+    return fail(c, LMOP_ERR_STATE, "internal: staging slot overflow (%zu + %zu > %zu)", off,
+                n * sizeof(T), st.bytes);
+  *out = (T*)(st.p + off);
+  if (src && n) std::memcpy(*out, src, n * sizeof(T));
+  st.used = off + n * sizeof(T);
+  return LMOP_OK;
+}
+
+// The device has been handed everything that reads or writes slot k.
+lmop_status stage_mark(lmop_ctx* c, int k) {
+  auto& st = c->stage[k];
+  HIP_OK(c, hipEventRecord(st.done, c->stream));
+  st.pending = true;
+  return LMOP_OK;
+}
+
+// Upper bound of the staging bytes one batch of T tokens and R rows needs.
+size_t stage_need(int T, int R, size_t n_work) {
+  return (size_t)T * 12 + (size_t)R * (sizeof(AttnRow) + 4 + sizeof(void*) + sizeof(HeadPick)) +
+         n_work * sizeof(int2) + 16 * 16;
 }
 
 // ---------------------------------------------------------------- profiling
@@ -538,37 +602,29 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
   return LMOP_OK;
 }
 
-// Uploads host-built per-token and per-row arrays for one forward pass.
-lmop_status upload_batch(lmop_ctx* c, const std::vector<int32_t>& tok,
+// Uploads host-built per-token and per-row arrays for one forward pass
+// through staging slot k (which stage_begin has sized); does not wait.
+lmop_status upload_batch(lmop_ctx* c, int k, const std::vector<int32_t>& tok,
                          const std::vector<int32_t>& pos, const std::vector<int32_t>& slot,
                          const std::vector<AttnRow>& rows, const std::vector<int2>& work,
                          const std::vector<int32_t>& last = {}) {
-  if (!last.empty()) {
-    int32_t* dl;
-    LMOP_TRY(ws_get(c, "last", last.size(), &dl));
-    HIP_OK(c, hipMemcpyAsync(dl, last.data(), last.size() * 4, hipMemcpyHostToDevice, c->stream));
-  }
-  int32_t *dt, *dp, *ds;
-  AttnRow* dr;
-  int2* dw;
-  LMOP_TRY(ws_get(c, "tok", tok.size(), &dt));
-  LMOP_TRY(ws_get(c, "pos", pos.size(), &dp));
-  LMOP_TRY(ws_get(c, "slot", slot.size(), &ds));
-  LMOP_TRY(ws_get(c, "rows", rows.size(), &dr));
-  LMOP_TRY(ws_get(c, "work", work.size(), &dw));
-  if (!tok.empty()) {
-    HIP_OK(c, hipMemcpyAsync(dt, tok.data(), tok.size() * 4, hipMemcpyHostToDevice, c->stream));
-    HIP_OK(c, hipMemcpyAsync(dp, pos.data(), pos.size() * 4, hipMemcpyHostToDevice, c->stream));
-    HIP_OK(c, hipMemcpyAsync(ds, slot.data(), slot.size() * 4, hipMemcpyHostToDevice, c->stream));
-  }
-  if (!rows.empty())
-    HIP_OK(c, hipMemcpyAsync(dr, rows.data(), rows.size() * sizeof(AttnRow),
-                             hipMemcpyHostToDevice, c->stream));
-  if (!work.empty())
-    HIP_OK(c, hipMemcpyAsync(dw, work.data(), work.size() * sizeof(int2), hipMemcpyHostToDevice,
-                             c->stream));
-  // the host vectors die with the caller's scope: finish the copies now
-  HIP_OK(c, hipStreamSynchronize(c->stream));
+  c->stage[k].used = 0;
+  auto put = [&](const char* name, const auto& v) -> lmop_status {
+    using T = typename std::decay_t<decltype(v)>::value_type;
+    T* d;
+    T* h;
+    LMOP_TRY(ws_get(c, name, v.size(), &d));
+    if (v.empty()) return LMOP_OK;
+    LMOP_TRY(stage_put(c, k, v.data(), v.size(), &h));
+    HIP_OK(c, hipMemcpyAsync(d, h, v.size() * sizeof(T), hipMemcpyHostToDevice, c->stream));
+    return LMOP_OK;
+  };
+  if (!last.empty()) LMOP_TRY(put("last", last));
+  LMOP_TRY(put("tok", tok));
+  LMOP_TRY(put("pos", pos));
+  LMOP_TRY(put("slot", slot));
+  LMOP_TRY(put("rows", rows));
+  LMOP_TRY(put("work", work));
   return LMOP_OK;
 }
 
@@ -597,9 +653,11 @@ void add_work(std::vector<int2>& work, int row, int n_q, int G) {
 
 // Runs the constrained head over R rows whose final hidden states are at
 // d_rowptr[i]; picks -> host.  dump_host (optional) receives [R][V] logits.
-lmop_status run_head(lmop_ctx* c, int R, const std::vector<const float*>& rowptr,
+// Enqueues the head over R rows; the picks land in staging slot k (*picks),
+// valid once the stream has passed this point.
+lmop_status run_head(lmop_ctx* c, int k, int R, const std::vector<const float*>& rowptr,
                      const int32_t* d_sel, const int32_t* d_allowed, int n_sel, int n_allowed,
-                     std::vector<HeadPick>& picks, float* dump_dev) {
+                     HeadPick** picks, float* dump_dev) {
   const lmop_config& cf = c->cfg;
   const int d = cf.d_model, V = cf.vocab;
   constexpr int kVocabTile = 128;
@@ -614,9 +672,9 @@ lmop_status run_head(lmop_ctx* c, int R, const std::vector<const float*>& rowptr
   LMOP_TRY(ws_get(c, "head_part", (size_t)R * n_chunks, &part));
   LMOP_TRY(ws_get(c, "head_zsel", (size_t)R * n_sel, &zsel));
   LMOP_TRY(ws_get(c, "head_pick", R, &dpk));
-  HIP_OK(c, hipMemcpyAsync(drp, rowptr.data(), R * sizeof(float*), hipMemcpyHostToDevice,
-                           c->stream));
-  HIP_OK(c, hipStreamSynchronize(c->stream));
+  const float** hrp;
+  LMOP_TRY(stage_put(c, k, rowptr.data(), (size_t)R, &hrp));
+  HIP_OK(c, hipMemcpyAsync(drp, hrp, R * sizeof(float*), hipMemcpyHostToDevice, c->stream));
   LMOP_TRY(timed(c, "rmsnorm_final", 0, (double)R * d * 6, [&] {
     return launch_rmsnorm(c->stream, nullptr, 0, drp, R, c->final_norm, d, cf.rms_eps, hn, d);
   }));
@@ -643,9 +701,8 @@ lmop_status run_head(lmop_ctx* c, int R, const std::vector<const float*>& rowptr
     return launch_head_finalize(c->stream, part, n_chunks, zsel, n_sel, n_allowed, d_allowed, R,
                                 dpk);
   }));
-  picks.resize(R);
-  HIP_OK(c, hipMemcpyAsync(picks.data(), dpk, R * sizeof(HeadPick), hipMemcpyDeviceToHost,
-                           c->stream));
+  LMOP_TRY(stage_put(c, k, (const HeadPick*)nullptr, (size_t)R, picks));
+  HIP_OK(c, hipMemcpyAsync(*picks, dpk, R * sizeof(HeadPick), hipMemcpyDeviceToHost, c->stream));
   return LMOP_OK;
 }
 
@@ -764,6 +821,10 @@ void lmop_destroy(lmop_ctx* ctx) {
       (void)hipEventDestroy(s.b);
     }
     for (hipEvent_t e : ctx->ev_free) (void)hipEventDestroy(e);
+    for (auto& st : ctx->stage) {
+      if (st.p) (void)hipHostFree(st.p);
+      if (st.done) (void)hipEventDestroy(st.done);
+    }
     if (ctx->own_stream && ctx->stream) (void)hipStreamDestroy(ctx->stream);
   }
   delete ctx;
@@ -945,7 +1006,8 @@ lmop_status lmop_set_prefix(lmop_ctx* ctx, const lmop_prefix* parent, const int3
     std::vector<int2> work;
     add_work(work, 0, n_tokens, cf.n_heads / cf.n_kv_heads);
     const std::vector<int32_t> last = {n_tokens - 1};
-    lmop_status st = upload_batch(ctx, tok, pos, slot, rows, work, last);
+    lmop_status st = stage_begin(ctx, 0, stage_need(n_tokens, 1, work.size()));
+    if (st == LMOP_OK) st = upload_batch(ctx, 0, tok, pos, slot, rows, work, last);
     Batch b;
     b.T = n_tokens;
     b.R = 1;
@@ -966,6 +1028,7 @@ lmop_status lmop_set_prefix(lmop_ctx* ctx, const lmop_prefix* parent, const int3
         if (e != hipSuccess) st = fail(ctx, LMOP_ERR_DEVICE, "copy of prefix hidden failed");
       }
     }
+    if (st == LMOP_OK) st = stage_mark(ctx, 0);
     if (st == LMOP_OK) st = sync(ctx);
     if (st != LMOP_OK) {
       destroy_prefix_storage(p.get());
@@ -1101,9 +1164,9 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
   const int G = cf.n_heads / cf.n_kv_heads;
   const int d = cf.d_model;
   std::vector<lmop_result> res(n_rows);
-  size_t u0 = 0;
-  while (u0 < uniq.size()) {
-    // ---- pack one batch
+  // batches: consecutive runs of distinct rows within the token budget
+  std::vector<std::pair<size_t, size_t>> batches;
+  for (size_t u0 = 0; u0 < uniq.size();) {
     size_t u1 = u0;
     int T = 0;
     while (u1 < uniq.size() && (int)(u1 - u0) < kMaxBatchRows) {
@@ -1112,7 +1175,28 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
       T += len;
       ++u1;
     }
+    batches.emplace_back(u0, u1);
+    u0 = u1;
+  }
+
+  // A batch between enqueue and finish: what its constrained steps need.
+  struct InFlight {
+    size_t u0 = 0;
+    int R = 0;
+    int k = 0;  // staging slot
+    std::vector<int> len, own;
+    int own_cap = 0;
+    uint16_t* own_kv = nullptr;
+    HeadPick* picks = nullptr;
+    float* dump = nullptr;
+  };
+
+  // Packs and uploads one batch, runs its prefill and its first head step;
+  // nothing here waits for the GPU.
+  auto enqueue = [&](size_t u0, size_t u1, int k, InFlight& B) -> lmop_status {
     const int R = (int)(u1 - u0);
+    int T = 0;
+    for (size_t u = u0; u < u1; ++u) T += (int)(offsets[uniq[u] + 1] - offsets[uniq[u]]);
     std::vector<int32_t> tok(T), pos(T), slot(T);
     std::vector<AttnRow> rows(R);
     std::vector<int2> work;
@@ -1141,8 +1225,6 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
       cap = round_up(cap + len[i] + dec, 8);
     }
     cap = own_store_cap(cap);
-    uint16_t* own_kv;
-    LMOP_TRY(ws_get(ctx, "own_kv", (size_t)cf.n_layers * 2 * cap * ctx->nkv_dim, &own_kv, true));
     // each row's last token (rows with suffix tokens only)
     std::vector<int32_t> last;
     std::vector<int> last_of(R, -1);
@@ -1151,7 +1233,10 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
         last_of[i] = (int)last.size();
         last.push_back(qs[i] + len[i] - 1);
       }
-    LMOP_TRY(upload_batch(ctx, tok, pos, slot, rows, work, last));
+    LMOP_TRY(stage_begin(ctx, k, stage_need(T, R, work.size())));
+    uint16_t* own_kv;
+    LMOP_TRY(ws_get(ctx, "own_kv", (size_t)cf.n_layers * 2 * cap * ctx->nkv_dim, &own_kv, true));
+    LMOP_TRY(upload_batch(ctx, k, tok, pos, slot, rows, work, last));
     Batch b;
     b.T = T;
     b.R = R;
@@ -1173,10 +1258,26 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
       else
         rowptr[i] = x + (size_t)(b.n_last > 0 ? last_of[i] : qs[i] + len[i] - 1) * d;
     }
-    float* dump = nullptr;
-    if (dbg) LMOP_TRY(ws_get(ctx, "dump", (size_t)R * V, &dump));
+    B.dump = nullptr;
+    if (dbg) LMOP_TRY(ws_get(ctx, "dump", (size_t)R * V, &B.dump));
+    LMOP_TRY(run_head(ctx, k, R, rowptr, d_sel, d_allowed, n_sel, n_allowed0, &B.picks, B.dump));
+    LMOP_TRY(stage_mark(ctx, k));
+    B.u0 = u0;
+    B.R = R;
+    B.k = k;
+    B.len = std::move(len);
+    B.own = std::move(own);
+    B.own_cap = cap;
+    B.own_kv = own_kv;
+    return LMOP_OK;
+  };
 
-    // ---- constrained steps
+  // Waits for a batch's first step, then runs its further (integer) steps.
+  auto finish = [&](InFlight& B) -> lmop_status {
+    const size_t u0 = B.u0;
+    const int R = B.R, k = B.k;
+    HIP_OK(ctx, hipEventSynchronize(ctx->stage[k].done));
+    ctx->stage[k].pending = false;
     std::vector<int> live(R);
     for (int i = 0; i < R; ++i) live[i] = i;
     std::vector<int> last_tok(R, -1);
@@ -1186,12 +1287,13 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
       o.logprob = 0.f;
       o.logprob_full = 0.f;
       o.n_tokens = 0;
-      for (int k = 0; k < 8; ++k) o.tokens[k] = -1;
+      for (int q = 0; q < 8; ++q) o.tokens[q] = -1;
     }
     if (dbg)
       for (int i = 0; i < R; ++i)
         std::fill(dbg + (size_t)uniq[u0 + i] * steps * V,
                   dbg + (size_t)(uniq[u0 + i] + 1) * steps * V, NAN);
+    HeadPick* picks = B.picks;
     for (int step = 0; step < steps && !live.empty(); ++step) {
       const int nl = (int)live.size();
       if (step > 0) {
@@ -1199,48 +1301,50 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
         std::vector<int32_t> st(nl), sp(nl), ss(nl);
         std::vector<AttnRow> sr(nl);
         std::vector<int2> sw;
-        for (int k = 0; k < nl; ++k) {
-          const int i = live[k];
+        for (int q = 0; q < nl; ++q) {
+          const int i = live[q];
           const int r = uniq[u0 + i];
-          const int own_idx = len[i] + step - 1;
-          st[k] = last_tok[i];
-          sp[k] = prefix_total(pf[r]) + own_idx;
-          ss[k] = own[i] + own_idx;
-          fill_segments(pf[r], sr[k]);
-          sr[k].q_start = k;
-          sr[k].n_q = 1;
-          sr[k].own_slot = own[i];
-          sr[k].own_q0 = own_idx;
-          add_work(sw, k, 1, G);
+          const int own_idx = B.len[i] + step - 1;
+          st[q] = last_tok[i];
+          sp[q] = prefix_total(pf[r]) + own_idx;
+          ss[q] = B.own[i] + own_idx;
+          fill_segments(pf[r], sr[q]);
+          sr[q].q_start = q;
+          sr[q].n_q = 1;
+          sr[q].own_slot = B.own[i];
+          sr[q].own_q0 = own_idx;
+          add_work(sw, q, 1, G);
         }
-        LMOP_TRY(upload_batch(ctx, st, sp, ss, sr, sw));
+        LMOP_TRY(stage_begin(ctx, k, stage_need(nl, nl, sw.size())));
+        LMOP_TRY(upload_batch(ctx, k, st, sp, ss, sr, sw));
         Batch sb;
         sb.T = nl;
         sb.R = nl;
         sb.n_work = (int)sw.size();
-        sb.own_kv = own_kv;
-        sb.own_cap = b.own_cap;
+        sb.own_kv = B.own_kv;
+        sb.own_cap = B.own_cap;
         LMOP_TRY(forward(ctx, sb));
+        float* x;
         LMOP_TRY(ws_get(ctx, "x", (size_t)nl * d, &x));
-        rowptr.resize(nl);
-        for (int k = 0; k < nl; ++k) rowptr[k] = x + (size_t)k * d;
+        std::vector<const float*> rowptr(nl);
+        for (int q = 0; q < nl; ++q) rowptr[q] = x + (size_t)q * d;
+        LMOP_TRY(run_head(ctx, k, nl, rowptr, d_sel, d_allowed, n_sel, n_sel, &picks, B.dump));
+        LMOP_TRY(stage_mark(ctx, k));
+        HIP_OK(ctx, hipEventSynchronize(ctx->stage[k].done));
+        ctx->stage[k].pending = false;
       }
-      const int n_allowed = (type->kind == LMOP_INT && step > 0) ? n_sel : n_allowed0;
-      std::vector<HeadPick> picks;
-      LMOP_TRY(run_head(ctx, nl, rowptr, d_sel, d_allowed, n_sel, n_allowed, picks, dump));
-      LMOP_TRY(sync(ctx));
       if (dbg) {
-        for (int k = 0; k < nl; ++k) {
-          const int r = uniq[u0 + live[k]];
-          HIP_OK(ctx, hipMemcpy(dbg + ((size_t)r * steps + step) * V, dump + (size_t)k * V,
+        for (int q = 0; q < nl; ++q) {
+          const int r = uniq[u0 + live[q]];
+          HIP_OK(ctx, hipMemcpy(dbg + ((size_t)r * steps + step) * V, B.dump + (size_t)q * V,
                                 (size_t)V * 4, hipMemcpyDeviceToHost));
         }
       }
       std::vector<int> next;
-      for (int k = 0; k < nl; ++k) {
-        const int i = live[k];
+      for (int q = 0; q < nl; ++q) {
+        const int i = live[q];
         lmop_result& o = res[uniq[u0 + i]];
-        const HeadPick& hp = picks[k];
+        const HeadPick& hp = picks[q];
         o.logprob += hp.logprob;
         o.logprob_full += hp.logprob_full;
         o.tokens[o.n_tokens++] = hp.token;
@@ -1255,8 +1359,26 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
       }
       live.swap(next);
     }
-    u0 = u1;
+    return LMOP_OK;
+  };
+
+  // With one constrained step and no logit dump, a batch's results come only
+  // from its pinned picks: the next batch is enqueued before this one is
+  // finished, so the GPU does not wait while the host packs and reads back.
+  // Integer decode and logit dumps reuse device buffers of the batch, so they
+  // finish each batch before the next starts.
+  const bool ahead = steps == 1 && !dbg;
+  InFlight slots[2];
+  for (size_t bi = 0; bi < batches.size(); ++bi) {
+    InFlight& cur = slots[bi & 1];
+    if (!ahead || bi == 0)
+      LMOP_TRY(enqueue(batches[bi].first, batches[bi].second, (int)(bi & 1), cur));
+    if (ahead && bi + 1 < batches.size())
+      LMOP_TRY(enqueue(batches[bi + 1].first, batches[bi + 1].second, (int)((bi + 1) & 1),
+                       slots[(bi + 1) & 1]));
+    LMOP_TRY(finish(cur));
   }
+  LMOP_TRY(sync(ctx));
   for (int r = 0; r < n_rows; ++r) {
     out[r] = res[rep[r]];
     if (dbg && rep[r] != r)
