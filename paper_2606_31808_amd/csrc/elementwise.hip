@@ -58,6 +58,45 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
   }
 }
 
+// The same with one wave per row and the row held in registers (NV float4
+// per lane, d = 256 * NV), four rows per workgroup: every load of a row is in
+// flight at once and the sum needs no LDS or barrier.  The sum of squares is
+// reduced in a fixed order (lane order, then a butterfly over the wave).
+template <int NV>
+__global__ __launch_bounds__(256) void rmsnorm_wave_kernel(const float* __restrict__ x, int ldx,
+                                                           const float* const* __restrict__ rowptr,
+                                                           int R, const float* __restrict__ gamma,
+                                                           float eps, f16* __restrict__ out,
+                                                           int ldo) {
+  constexpr int D = 256 * NV;
+  const int lane = threadIdx.x & 63;
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= R) return;
+  const float* row = rowptr ? rowptr[i] : x + (size_t)i * ldx;
+  float4 v[NV];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) v[j] = *(const float4*)(row + (j * 64 + lane) * 4);
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    ss += v[j].x * v[j].x;
+    ss += v[j].y * v[j].y;
+    ss += v[j].z * v[j].z;
+    ss += v[j].w * v[j].w;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) ss += shfl_xor(ss, o);
+  const float rstd = 1.0f / sqrtf(ss / (float)D + eps);
+  f16* o = out + (size_t)i * ldo;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int cix = (j * 64 + lane) * 4;
+    const float4 gm = *(const float4*)(gamma + cix);
+    *(f16x4*)(o + cix) = f16x4{(f16)(v[j].x * rstd * gm.x), (f16)(v[j].y * rstd * gm.y),
+                              (f16)(v[j].z * rstd * gm.z), (f16)(v[j].w * rstd * gm.w)};
+  }
+}
+
 // --------------------------------------------------------------- row gather
 // Copies the residual row and the attention-output row of each selected token
 // (the last token of every row, before the last layer's O-projection and MLP).
@@ -201,8 +240,24 @@ hipError_t launch_gather_rows(hipStream_t s, const int32_t* idx, int R, const fl
 hipError_t launch_rmsnorm(hipStream_t s, const float* x, int ldx, const float* const* rowptr,
                           int R, const float* gamma, int d, float eps, half_bits* out, int ldo) {
   if (R == 0) return hipSuccess;
-  hipLaunchKernelGGL(rmsnorm_kernel, dim3(R), dim3(256), 0, s, x, ldx, rowptr, gamma, d, eps,
-                     (f16*)out, ldo);
+  const dim3 g4((R + 3) / 4);
+  switch (d) {  // the model widths this build meets; others take the workgroup-per-row kernel
+    case 256:
+      hipLaunchKernelGGL(rmsnorm_wave_kernel<1>, g4, dim3(256), 0, s, x, ldx, rowptr, R, gamma, eps,
+                         (f16*)out, ldo);
+      break;
+    case 2048:
+      hipLaunchKernelGGL(rmsnorm_wave_kernel<8>, g4, dim3(256), 0, s, x, ldx, rowptr, R, gamma, eps,
+                         (f16*)out, ldo);
+      break;
+    case 4096:
+      hipLaunchKernelGGL(rmsnorm_wave_kernel<16>, g4, dim3(256), 0, s, x, ldx, rowptr, R, gamma,
+                         eps, (f16*)out, ldo);
+      break;
+    default:
+      hipLaunchKernelGGL(rmsnorm_kernel, dim3(R), dim3(256), 0, s, x, ldx, rowptr, gamma, d, eps,
+                         (f16*)out, ldo);
+  }
   return hipGetLastError();
 }
 
