@@ -141,15 +141,22 @@ typedef struct {
 typedef struct {
   int64_t value;      /* BOOL 0/1; ENUM option index; INT decimal value                     */
   float logprob;      /* sum over steps of log-softmax over that step's allowed tokens       */
-  float logprob_full; /* sum over steps of log-softmax over the whole vocabulary            */
+  float logprob_full; /* sum over steps of log-softmax over the whole vocabulary; NaN with
+                         LMOP_HEAD_RESTRICTED                                              */
   int32_t n_tokens;   /* tokens generated (INT: EOS included)                               */
   int32_t tokens[8];  /* generated token ids; unused entries are -1                         */
 } lmop_result;
 
 #define LMOP_NO_DEDUP 1u /* evaluate duplicate rows separately (results are identical) */
+/* Restricted head: the constrained step (Sec. 2.3, "Constrained Decoding")
+ * needs only the logits of the type's allowed tokens for its value and for
+ * `logprob`; with this flag the library computes just those (|A| dot
+ * products per row instead of the full vocabulary), `logprob_full` is NaN,
+ * and debug_logits holds the allowed tokens' logits with NaN elsewhere. */
+#define LMOP_HEAD_RESTRICTED 2u
 
 typedef struct {
-  uint32_t flags;           /* LMOP_NO_DEDUP                                              */
+  uint32_t flags;           /* LMOP_NO_DEDUP | LMOP_HEAD_RESTRICTED                       */
   int32_t max_batch_tokens; /* suffix tokens per device batch; 0 = library default        */
   float* debug_logits;      /* NULL or host fp32 [n_rows][max_steps][vocab]: the logits of
                                each step (max_steps = max_tokens for INT, else 1); steps a

@@ -153,6 +153,36 @@ __global__ void repack_kernel(RepackSrc src, const int32_t* __restrict__ colsrc,
   if (g == 0) spack[blk * 64 + c * 4 + f] = scale;
 }
 
+// --------------------------------------------------------------- restricted head
+// Logits of the allowed tokens only: one workgroup per row, one wave per
+// allowed token at a time; each lane sums 8-feature runs with a stride of
+// 512 features, then the wave adds the lanes in a fixed order.
+__global__ __launch_bounds__(256) void head_restricted_kernel(const f16* __restrict__ hn, int d,
+                                                              const f16* __restrict__ W,
+                                                              const int32_t* __restrict__ allowed,
+                                                              int n_sel, float* __restrict__ zsel,
+                                                              float* __restrict__ dump,
+                                                              int ld_dump) {
+  const int r = blockIdx.x, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const f16* h = hn + (size_t)r * d;
+  for (int i = wave; i < n_sel; i += 4) {
+    const int tok = allowed[i];
+    const f16* w = W + (size_t)tok * d;
+    float acc = 0.f;
+    for (int k = lane * 8; k < d; k += 512) {
+      const f16x8 a = *(const f16x8*)(h + k), b = *(const f16x8*)(w + k);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc += (float)a[j] * (float)b[j];
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) acc += shfl_xor(acc, o);
+    if (lane == 0) {
+      zsel[(size_t)r * n_sel + i] = acc;
+      if (dump) dump[(size_t)r * ld_dump + tok] = acc;
+    }
+  }
+}
+
 // --------------------------------------------------------------- head finish
 // One wave per row: LSE over the vocabulary from the per-slice partials, then
 // the first maximum among the allowed tokens and the allowed-set LSE.
@@ -212,7 +242,7 @@ __global__ __launch_bounds__(64) void head_finalize_kernel(const float2* __restr
     hp.index = bi;
     hp.token = allowed_tok[bi];
     hp.logprob = -logf(sa);
-    hp.logprob_full = best - lse_full;
+    hp.logprob_full = n_chunks > 0 ? best - lse_full : NAN;
     hp.margin = n_allowed > 1 ? best - second : INFINITY;
     hp.pad[0] = hp.pad[1] = hp.pad[2] = 0.f;
     out[r] = hp;
@@ -268,6 +298,16 @@ hipError_t launch_repack_w4(hipStream_t s, const RepackSrc& src, const int32_t* 
   const int blocks = (int)((total + 255) / 256);
   hipLaunchKernelGGL(repack_kernel, dim3(blocks), dim3(256), 0, s, src, colsrc, dst.np, kg_n,
                      dst.qpack, (f16*)dst.spack);
+  return hipGetLastError();
+}
+
+hipError_t launch_head_restricted(hipStream_t s, const half_bits* hn, int R, int d,
+                                  const half_bits* W, const int32_t* allowed, int n_sel,
+                                  float* zsel, float* dump, int ld_dump) {
+  if (R == 0 || n_sel == 0) return hipSuccess;
+  if (d % 8 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(head_restricted_kernel, dim3(R), dim3(256), 0, s, (const f16*)hn, d,
+                     (const f16*)W, allowed, n_sel, zsel, dump, ld_dump);
   return hipGetLastError();
 }
 

@@ -132,6 +132,12 @@ struct HeadPick {
   float pad[3];
 };
 // per row: combine partials -> LSE over V; pick among zsel[:n_allowed]
+// zsel[r][i] = hn[r] . W[allowed[i]] (fp16 rows of width d, fp32 sums) for
+// the n_sel allowed tokens only; with dump, also dump[r][allowed[i]]
+hipError_t launch_head_restricted(hipStream_t s, const half_bits* hn, int R, int d,
+                                  const half_bits* W, const int32_t* allowed, int n_sel,
+                                  float* zsel, float* dump, int ld_dump);
+// n_chunks = 0: no vocabulary partials (restricted head), logprob_full = NaN
 hipError_t launch_head_finalize(hipStream_t s, const float2* part, int n_chunks,
                                 const float* zsel, int n_sel, int n_allowed,
                                 const int32_t* allowed_tok, int R, HeadPick* out);

@@ -657,7 +657,7 @@ void add_work(std::vector<int2>& work, int row, int n_q, int G) {
 // valid once the stream has passed this point.
 lmop_status run_head(lmop_ctx* c, int k, int R, const std::vector<const float*>& rowptr,
                      const int32_t* d_sel, const int32_t* d_allowed, int n_sel, int n_allowed,
-                     HeadPick** picks, float* dump_dev) {
+                     bool restricted, HeadPick** picks, float* dump_dev) {
   const lmop_config& cf = c->cfg;
   const int d = cf.d_model, V = cf.vocab;
   constexpr int kVocabTile = 128;
@@ -669,7 +669,7 @@ lmop_status run_head(lmop_ctx* c, int k, int R, const std::vector<const float*>&
   HeadPick* dpk;
   LMOP_TRY(ws_get(c, "head_rowptr", R, &drp));
   LMOP_TRY(ws_get(c, "head_hn", (size_t)R * d, &hn));
-  LMOP_TRY(ws_get(c, "head_part", (size_t)R * n_chunks, &part));
+  LMOP_TRY(ws_get(c, "head_part", restricted ? 1 : (size_t)R * n_chunks, &part));
   LMOP_TRY(ws_get(c, "head_zsel", (size_t)R * n_sel, &zsel));
   LMOP_TRY(ws_get(c, "head_pick", R, &dpk));
   const float** hrp;
@@ -678,28 +678,38 @@ lmop_status run_head(lmop_ctx* c, int k, int R, const std::vector<const float*>&
   LMOP_TRY(timed(c, "rmsnorm_final", 0, (double)R * d * 6, [&] {
     return launch_rmsnorm(c->stream, nullptr, 0, drp, R, c->final_norm, d, cf.rms_eps, hn, d);
   }));
-  {
-    GemmArgs ga{};
-    ga.A = c->head;
-    ga.lda = d;
-    ga.M = V;
-    ga.N = R;
-    ga.K = d;
-    ga.bh = hn;
-    ga.ldb = d;
-    ga.part = part;
-    ga.sel = d_sel;
-    ga.zsel = zsel;
-    ga.n_sel = n_sel;
-    ga.dump = dump_dev;
-    ga.ld_dump = V;
-    LMOP_TRY(timed(c, "head_gemm", 2.0 * R * V * d, (double)V * d * 2 + (double)R * d * 2, [&] {
-      return launch_gemm_f16(c->stream, ga, EPI_HEAD);
-    }));
+  if (restricted) {
+    // only the allowed tokens' logits; the dump's other entries stay NaN
+    if (dump_dev) HIP_OK(c, hipMemsetAsync(dump_dev, 0xFF, (size_t)R * V * 4, c->stream));
+    LMOP_TRY(timed(c, "head_restricted", 2.0 * R * n_sel * d,
+                   (double)R * d * 2 + (double)n_sel * d * 2 + (double)R * n_sel * 4, [&] {
+                     return launch_head_restricted(c->stream, hn, R, d, c->head, d_allowed, n_sel,
+                                                   zsel, dump_dev, V);
+                   }));
+  } else {
+    {
+      GemmArgs ga{};
+      ga.A = c->head;
+      ga.lda = d;
+      ga.M = V;
+      ga.N = R;
+      ga.K = d;
+      ga.bh = hn;
+      ga.ldb = d;
+      ga.part = part;
+      ga.sel = d_sel;
+      ga.zsel = zsel;
+      ga.n_sel = n_sel;
+      ga.dump = dump_dev;
+      ga.ld_dump = V;
+      LMOP_TRY(timed(c, "head_gemm", 2.0 * R * V * d, (double)V * d * 2 + (double)R * d * 2, [&] {
+        return launch_gemm_f16(c->stream, ga, EPI_HEAD);
+      }));
+    }
   }
   LMOP_TRY(timed(c, "head_finalize", 0, 0, [&] {
-    return launch_head_finalize(c->stream, part, n_chunks, zsel, n_sel, n_allowed, d_allowed, R,
-                                dpk);
+    return launch_head_finalize(c->stream, part, restricted ? 0 : n_chunks, zsel, n_sel,
+                                n_allowed, d_allowed, R, dpk);
   }));
   LMOP_TRY(stage_put(c, k, (const HeadPick*)nullptr, (size_t)R, picks));
   HIP_OK(c, hipMemcpyAsync(*picks, dpk, R * sizeof(HeadPick), hipMemcpyDeviceToHost, c->stream));
@@ -1117,10 +1127,15 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
                   r, (long long)(prefix_total(p) + len + dec), cf.max_seq);
     pf[r] = p;
   }
+  const uint32_t flags = opts ? opts->flags : 0u;
+  if (flags & ~(LMOP_NO_DEDUP | LMOP_HEAD_RESTRICTED))
+    return fail(ctx, LMOP_ERR_INVALID_ARG, "unknown flags 0x%x", (unsigned)flags);
+  if (opts && opts->max_batch_tokens < 0)
+    return fail(ctx, LMOP_ERR_INVALID_ARG, "max_batch_tokens < 0");
   if (ctx->host_only)
     return fail(ctx, LMOP_ERR_UNSUPPORTED, "host-only ctx: arguments are valid, no device to run");
 
-  const uint32_t flags = opts ? opts->flags : 0u;
+  const bool restricted = (flags & LMOP_HEAD_RESTRICTED) != 0;
   int budget = opts && opts->max_batch_tokens > 0 ? opts->max_batch_tokens : kDefaultBatchTokens;
   float* dbg = opts ? opts->debug_logits : nullptr;
   const int V = cf.vocab;
@@ -1260,7 +1275,8 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
     }
     B.dump = nullptr;
     if (dbg) LMOP_TRY(ws_get(ctx, "dump", (size_t)R * V, &B.dump));
-    LMOP_TRY(run_head(ctx, k, R, rowptr, d_sel, d_allowed, n_sel, n_allowed0, &B.picks, B.dump));
+    LMOP_TRY(run_head(ctx, k, R, rowptr, d_sel, d_allowed, n_sel, n_allowed0, restricted, &B.picks,
+                      B.dump));
     LMOP_TRY(stage_mark(ctx, k));
     B.u0 = u0;
     B.R = R;
@@ -1328,7 +1344,8 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
         LMOP_TRY(ws_get(ctx, "x", (size_t)nl * d, &x));
         std::vector<const float*> rowptr(nl);
         for (int q = 0; q < nl; ++q) rowptr[q] = x + (size_t)q * d;
-        LMOP_TRY(run_head(ctx, k, nl, rowptr, d_sel, d_allowed, n_sel, n_sel, &picks, B.dump));
+        LMOP_TRY(run_head(ctx, k, nl, rowptr, d_sel, d_allowed, n_sel, n_sel, restricted, &picks,
+                          B.dump));
         LMOP_TRY(stage_mark(ctx, k));
         HIP_OK(ctx, hipEventSynchronize(ctx->stage[k].done));
         ctx->stage[k].pending = false;

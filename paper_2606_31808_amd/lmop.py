@@ -21,6 +21,7 @@ LMOP_OK, LMOP_ERR_INVALID_ARG, LMOP_ERR_STATE, LMOP_ERR_OOM, LMOP_ERR_DEVICE, \
     LMOP_ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 LMOP_BOOL, LMOP_ENUM, LMOP_INT = 0, 1, 2
 LMOP_NO_DEDUP = 1
+LMOP_HEAD_RESTRICTED = 2
 
 EXPORTED = (
     "lmop_create", "lmop_destroy", "lmop_last_error", "lmop_status_string", "lmop_load_weights",
@@ -299,10 +300,11 @@ class Context:
         lmop_release_prefix(self.ctx, p)
 
     def eval_rows(self, tokens, offsets, kind, allowed, eos=-1, max_tokens=1, prefix=None,
-                  row_prefix=None, no_dedup=False, max_batch_tokens=0, debug_logits=False):
+                  row_prefix=None, no_dedup=False, max_batch_tokens=0, debug_logits=False,
+                  head_restricted=False):
+        flags = (LMOP_NO_DEDUP if no_dedup else 0) | (LMOP_HEAD_RESTRICTED if head_restricted else 0)
         return lmop_eval_rows(self.ctx, tokens, offsets, kind, allowed, eos, max_tokens, prefix,
-                              row_prefix, LMOP_NO_DEDUP if no_dedup else 0, max_batch_tokens,
-                              debug_logits, self.vocab)
+                              row_prefix, flags, max_batch_tokens, debug_logits, self.vocab)
 
     def set_profiling(self, on: bool):
         lmop_set_profiling(self.ctx, on)

@@ -15,10 +15,24 @@ TOL_REL = 0.05
 MARGIN = 0.1
 
 
-def compare(orc, out, dbg, label="", orc_forced=None):
+def compare(orc, out, dbg, label="", orc_forced=None, cols=None):
     """orc: oracle eval_rows dict (keep_logits=True); out: library results;
     dbg: library logits [R][steps][V]; orc_forced: oracle re-run with
-    forced = library tokens (needed only if some row's path diverged)."""
+    forced = library tokens (needed only if some row's path diverged).
+    cols: the allowed token ids (INT: EOS included) when the library ran the
+    restricted head; then only those logits exist (the rest must be NaN),
+    the scale is still the std of the oracle's full logits, and
+    logprob_full must be NaN."""
+    if cols is not None:
+        cols = np.asarray(cols)
+        others = np.ones(dbg.shape[-1], bool)
+        others[cols] = False
+
+    def pick(zg, zo):
+        if cols is None:
+            return zg, zo
+        assert np.all(np.isnan(zg[others])), f"{label}: restricted logits outside the allowed set"
+        return zg[cols], zo[cols]
     R = len(out)
     diffs, refs = [], []
     n_exact = n_checked = 0
@@ -30,9 +44,9 @@ def compare(orc, out, dbg, label="", orc_forced=None):
         for s, zo in enumerate(orc["logits"][r]):
             if s > 0 and ot[:s] != gt[:s]:
                 break
-            zg = dbg[r, s]
+            zg, zc = pick(dbg[r, s], zo)
             assert np.all(np.isfinite(zg)), f"{label} row {r} step {s}: non-finite logits"
-            d = np.abs(zg.astype(np.float64) - zo)
+            d = np.abs(zg.astype(np.float64) - zc)
             diffs.append(d.max())
             refs.append(zo)
         if ot != gt:
@@ -46,8 +60,8 @@ def compare(orc, out, dbg, label="", orc_forced=None):
     if diverged and orc_forced is not None:
         for r in diverged:
             for s, zo in enumerate(orc_forced["logits"][r]):
-                zg = dbg[r, s]
-                diffs.append(np.abs(zg.astype(np.float64) - zo).max())
+                zg, zc = pick(dbg[r, s], zo)
+                diffs.append(np.abs(zg.astype(np.float64) - zc).max())
                 refs.append(zo)
     sigma = float(np.concatenate(refs).std())
     worst = float(max(diffs)) if diffs else 0.0
@@ -61,7 +75,10 @@ def compare(orc, out, dbg, label="", orc_forced=None):
         dlpf = np.abs(out["logprob_full"][same] - orc["logprob_full"][same])
         bound = 2 * worst * steps + 1e-3 * steps
         assert np.all(dlp <= bound), f"{label}: logprob off by {dlp.max():.4g}"
-        assert np.all(dlpf <= bound + 1e-3 * steps), f"{label}: logprob_full off by {dlpf.max():.4g}"
+        if cols is None:
+            assert np.all(dlpf <= bound + 1e-3 * steps), f"{label}: logprob_full off by {dlpf.max():.4g}"
+    if cols is not None:
+        assert np.all(np.isnan(out["logprob_full"])), f"{label}: restricted head gave logprob_full"
     return dict(max_abs=worst, sigma=sigma, ratio=ratio, rows=R, exact_checked=n_checked,
                 diverged=len(diverged))
 
@@ -73,7 +90,8 @@ def assert_typed(out, kind, n_allowed, allowed, eos=-1, max_tokens=1):
         n = int(out["n_tokens"][r])
         toks = out["tokens"][r][:n].tolist()
         assert np.all(out["tokens"][r][n:] == -1)
-        assert out["logprob"][r] <= 1e-6 and out["logprob_full"][r] <= out["logprob"][r] + 1e-5
+        assert out["logprob"][r] <= 1e-6
+        assert np.isnan(out["logprob_full"][r]) or out["logprob_full"][r] <= out["logprob"][r] + 1e-5
         if kind == 2:
             assert 1 <= n <= max_tokens and toks[0] in allowed
             assert all(t in allowed for t in toks[:-1])

@@ -54,8 +54,9 @@ def m8b(L):
 
 
 def _same_rows(full, sub, rows, label):
+    # bit for bit (NaN fields, as in restricted mode, compare equal too)
     for j, r in enumerate(rows):
-        assert np.array_equal(full[r], sub[j]), f"{label}: row {r} differs between calls"
+        assert full[r].tobytes() == sub[j].tobytes(), f"{label}: row {r} differs between calls"
 
 
 def _check_filter(ctx, orc, wl, pre, sample, label):
@@ -98,6 +99,29 @@ def test_filter_8b_sampled_rows(m8b):
     wl = make_workload("filter_8b")
     pre = ctx.set_prefix(wl.prefix)
     _check_filter(ctx, orc, wl, pre, _sample(wl, 5, 2), "filter_8b")
+    ctx.release_prefix(pre)
+
+
+def test_filter_8b_restricted_head(m8b):
+    """The whole table with the restricted head, then sampled rows against
+    the oracle's allowed logits."""
+    w, ctx, orc = m8b
+    wl = make_workload("filter_8b")
+    pre = ctx.set_prefix(wl.prefix)
+    _log(f"filter_8b restricted: full table ({wl.n_rows} rows)")
+    full, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, prefix=pre,
+                            head_restricted=True)
+    assert_typed(full, wl.kind, len(wl.allowed), wl.allowed)
+    assert np.all(np.isnan(full["logprob_full"]))
+    sample = _sample(wl, 4, 5)
+    sub = wl.subset(sample)
+    out, dbg = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, prefix=pre,
+                             debug_logits=True, head_restricted=True)
+    _same_rows(full, out, sample, "filter_8b restricted")
+    _log(f"filter_8b restricted: oracle on {len(sample)} rows")
+    ref = orc.eval_workload(sub, keep_logits=True)
+    st = compare(ref, out, dbg, "filter_8b restricted", cols=wl.allowed)
+    _log("filter_8b restricted", st)
     ctx.release_prefix(pre)
 
 

@@ -159,6 +159,36 @@ def test_tiny_int_decode(L):
     assert_typed(out, KIND_INT, 10, digits, eos, 4)
     lens = set(out["n_tokens"].tolist())
     assert len(lens) >= 2, lens
+    # the same with the restricted head (digits and EOS only)
+    out_r, dbg_r = ctx.eval_rows(np.concatenate(rows), offs, KIND_INT, digits, eos=eos,
+                                 max_tokens=4, prefix=pre, debug_logits=True, head_restricted=True)
+    forced_r = orc.eval_rows(prefix, rows, KIND_INT, digits, eos=eos, max_tokens=4,
+                             forced=[out_r["tokens"][r][: out_r["n_tokens"][r]] for r in range(48)],
+                             keep_logits=True)
+    st_r = compare(ref, out_r, dbg_r, "int restricted", orc_forced=forced_r,
+                   cols=list(digits) + [eos])
+    _log("int decode, restricted head", st_r)
+    assert_typed(out_r, KIND_INT, 10, digits, eos, 4)
+
+
+def test_tiny_restricted_head(tiny, L):
+    """Restricted head: only the allowed tokens' logits are computed; typed
+    outputs and allowed-set log-probabilities match the oracle and the full
+    head, logprob_full is NaN."""
+    w, orc, ctx = tiny
+    wl = make_workload("filter_tiny")
+    pre = ctx.set_prefix(wl.prefix)
+    out, dbg = _run(ctx, wl, pre, head_restricted=True)
+    ref = orc.eval_workload(wl, keep_logits=True)
+    st = compare(ref, out, dbg, "restricted", cols=wl.allowed)
+    _log("restricted head", st)
+    assert st["exact_checked"] >= 32
+    assert_typed(out, wl.kind, 2, wl.allowed)
+    full, _ = _run(ctx, wl, pre)
+    clear = ref["margin"] > 0.1
+    assert np.array_equal(out["value"][clear], full["value"][clear])
+    assert np.allclose(out["logprob"], full["logprob"], atol=1e-3)
+    ctx.release_prefix(pre)
 
 
 def test_tiny_dedup_and_batch_invariance(tiny, L):

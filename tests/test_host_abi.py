@@ -105,6 +105,12 @@ def test_eval_argument_validation(tiny_w):
             max_tokens=9)
     _expect(L.LMOP_ERR_UNSUPPORTED, ctx.eval_rows, [1], [0, 1], L.LMOP_INT, digits, eos=5,
             max_tokens=8)
+    # options: the restricted head is a valid mode; unknown flags and a
+    # negative batch budget are not
+    _expect(L.LMOP_ERR_UNSUPPORTED, ctx.eval_rows, [1, 2, 3], [0, 2, 3], head_restricted=True, **ok)
+    _expect(L.LMOP_ERR_INVALID_ARG, L.lmop_eval_rows, ctx.ctx, [1, 2, 3], [0, 2, 3], L.LMOP_BOOL,
+            [3, 4], flags=4)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [1, 2, 3], [0, 2, 3], max_batch_tokens=-1, **ok)
     # too long for max_seq (4096 by default)
     _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, np.ones(4097, np.int32), [0, 4097], **ok)
     # zero rows is a no-op
@@ -172,3 +178,11 @@ def test_dedup_rejects_bad_csr():
         L.lmop_dedup_rows([1, 2], [1, 2])
     rep, nu = L.lmop_dedup_rows([], [0])
     assert nu == 0 and len(rep) == 0
+
+
+def test_binding_constants_match_header():
+    """The flag values the binding passes are the header's."""
+    hdr = open(os.path.join(ROOT, "include", "lmop.h")).read()
+    defs = dict(re.findall(r"#define\s+(LMOP_\w+)\s+(\d+)u", hdr))
+    assert defs == {"LMOP_NO_DEDUP": "1", "LMOP_HEAD_RESTRICTED": "2"}
+    assert L.LMOP_NO_DEDUP == 1 and L.LMOP_HEAD_RESTRICTED == 2
