@@ -167,6 +167,25 @@ def head_roofline(stats):
             "bytes_per_launch": s["bytes"] / s["launches"]}
 
 
+def pass_rooflines(stats):
+    """The other passes of a step: attention against MFMA (its FLOPs are the
+    visible query-key pairs the host counts), RMSNorm against HBM (fp32 in,
+    fp16 out)."""
+    out = {}
+    a = stats.get("attention")
+    if a and a["ms"] > 0 and a["flops"] > 0:
+        t = a["flops"] / (a["ms"] * 1e-3) / 1e12
+        out["attention"] = {"bound": "mfma", "achieved": t, "peak": PEAK_F16_TFLOPS,
+                            "unit": "TFLOP/s", "frac": t / PEAK_F16_TFLOPS,
+                            "avg_launch_ms": a["ms"] / a["launches"]}
+    r = stats.get("rmsnorm")
+    if r and r["ms"] > 0:
+        g = r["bytes"] / (r["ms"] * 1e-3) / 1e9
+        out["rmsnorm"] = {"bound": "hbm", "achieved": g, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                          "frac": g / PEAK_HBM_GBS, "avg_launch_ms": r["ms"] / r["launches"]}
+    return out
+
+
 def cpu_baseline(weights, shape, wl, n_rows):
     """The oracle (fp32, as it stands) on the first n_rows rows of the table,
     including its pass over the shared prefix and its weight dequantisation."""
@@ -290,6 +309,7 @@ def main():
                    "head": "restricted" if args.head_restricted else "full vocabulary"},
         "roofline": gemm_roofline(stats),
         "head_roofline": head_roofline(stats),
+        "pass_rooflines": pass_rooflines(stats),
         "load_weights_s": t_load, "set_prefix_ms": t_prefix * 1e3,
         "kernels_ms_per_step": {k: v["ms"] / args.steps for k, v in sorted(stats.items())},
     }

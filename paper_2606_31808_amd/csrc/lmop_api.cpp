@@ -482,6 +482,8 @@ struct Batch {
   // With n_last > 0 the last layer's O-projection and MLP run on those tokens
   // only, and their final hidden states land in ws "xlast" [n_last][d].
   int n_last = 0;
+  // keys visible to the batch's query tokens, summed (for the attention FLOP count)
+  double visible_keys = 0;
 };
 
 // One pass of all layers over the T tokens whose ids/positions/slots and row
@@ -557,7 +559,9 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
     aa.nq = cf.n_heads;
     aa.nkv = cf.n_kv_heads;
     aa.hd = hd;
-    LMOP_TRY(timed(c, "attention", 0, 0, [&] { return launch_attention(c->stream, aa); }));
+    // per visible (query token, key) pair and query head: q.k and p.v, 2 FLOP per dim each
+    const double attn_flops = 4.0 * hd * cf.n_heads * b.visible_keys;
+    LMOP_TRY(timed(c, "attention", attn_flops, 0, [&] { return launch_attention(c->stream, aa); }));
     // in the last layer only the selected tokens continue (their K/V are written above)
     int M = T;
     float* xr = x;
@@ -1025,6 +1029,7 @@ lmop_status lmop_set_prefix(lmop_ctx* ctx, const lmop_prefix* parent, const int3
     b.own_kv = p->kv;
     b.own_cap = p->cap;
     b.n_last = 1;
+    b.visible_keys = (double)n_tokens * start + 0.5 * (double)n_tokens * (n_tokens + 1);
     if (st == LMOP_OK) st = forward(ctx, b);
     if (st == LMOP_OK) {
       // the final hidden state of the last token (the whole model when L = 0)
@@ -1259,6 +1264,9 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
     b.own_kv = own_kv;
     b.own_cap = cap;
     b.n_last = cf.n_layers > 0 ? (int)last.size() : 0;
+    for (int i = 0; i < R; ++i)
+      b.visible_keys += (double)len[i] * prefix_total(pf[uniq[u0 + i]]) +
+                        0.5 * (double)len[i] * (len[i] + 1);
     LMOP_TRY(forward(ctx, b));
     float* x;
     if (b.n_last > 0)
@@ -1339,6 +1347,7 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
         sb.n_work = (int)sw.size();
         sb.own_kv = B.own_kv;
         sb.own_cap = B.own_cap;
+        for (int q = 0; q < nl; ++q) sb.visible_keys += sp[q] + 1;  // position + 1 keys
         LMOP_TRY(forward(ctx, sb));
         float* x;
         LMOP_TRY(ws_get(ctx, "x", (size_t)nl * d, &x));
