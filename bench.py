@@ -238,7 +238,7 @@ def main():
         print(json.dumps({"copied_bytes": COPY_BYTES}))
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
+        print(json.dumps({"error": "the library runs on one GPU; --gpus must be 1"}))
         sys.exit(2)
 
     import numpy as np

@@ -46,7 +46,7 @@ typedef enum {
   LMOP_ERR_STATE = -2,       /* call out of order (e.g. eval before load_weights)     */
   LMOP_ERR_OOM = -3,         /* a device or host allocation failed                    */
   LMOP_ERR_DEVICE = -4,      /* a HIP call failed; sticky, the ctx must be destroyed  */
-  LMOP_ERR_UNSUPPORTED = -5  /* a model shape or option this build does not handle    */
+  LMOP_ERR_UNSUPPORTED = -5  /* a model shape or option the library does not handle   */
 } lmop_status;
 
 typedef struct lmop_ctx lmop_ctx;       /* opaque */

@@ -271,7 +271,7 @@ hipError_t launch_rmsnorm(hipStream_t s, const float* x, int ldx, const float* c
                           int R, const float* gamma, int d, float eps, half_bits* out, int ldo) {
   if (R == 0) return hipSuccess;
   const dim3 g4((R + 3) / 4);
-  switch (d) {  // the model widths this build meets; others take the workgroup-per-row kernel
+  switch (d) {  // the common model widths; others take the workgroup-per-row kernel
     case 256:
       hipLaunchKernelGGL(rmsnorm_wave_kernel<1>, g4, dim3(256), 0, s, x, ldx, rowptr, R, gamma, eps,
                          (f16*)out, ldo);
