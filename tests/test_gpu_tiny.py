@@ -191,6 +191,46 @@ def test_tiny_restricted_head(tiny, L):
     ctx.release_prefix(pre)
 
 
+def test_tiny_edge_cases(tiny, L):
+    """A single allowed option (log-probability exactly 0), a one-token
+    integer, a 300-token row beside one-token rows under a batch budget
+    smaller than the long row, and rows with and without a prefix in one call."""
+    w, orc, ctx = tiny
+    V = TINY.vocab
+    rng = np.random.default_rng(11)
+    prefix = rng.integers(0, V, size=130).astype(np.int32)
+    pre = ctx.set_prefix(prefix)
+    rows = [rng.integers(0, V, size=n).astype(np.int32) for n in (300, 1, 1, 17, 64)]
+    toks = np.concatenate(rows)
+    offs = np.concatenate([[0], np.cumsum([len(r) for r in rows])])
+
+    one = [int(rng.integers(0, V))]
+    out, dbg = ctx.eval_rows(toks, offs, KIND_ENUM, one, prefix=pre, debug_logits=True,
+                             max_batch_tokens=100)
+    assert np.all(out["value"] == 0) and np.all(out["logprob"] == 0.0)
+    ref = orc.eval_rows(prefix, rows, KIND_ENUM, one, keep_logits=True)
+    _log("one option", compare(ref, out, dbg, "one option"))
+
+    digits = rng.choice(V, 10, replace=False).astype(np.int32)
+    eos = int(next(t for t in range(V) if t not in digits))
+    out1, dbg1 = ctx.eval_rows(toks, offs, KIND_INT, digits, eos=eos, max_tokens=1, prefix=pre,
+                               debug_logits=True)
+    ref1 = orc.eval_rows(prefix, rows, KIND_INT, digits, eos=eos, max_tokens=1, keep_logits=True)
+    _log("int, one token", compare(ref1, out1, dbg1, "int, one token"))
+    assert np.all(out1["n_tokens"] == 1)
+    assert_typed(out1, KIND_INT, 10, digits, eos, 1)
+
+    allowed = rng.choice(V, 2, replace=False).astype(np.int32)
+    with_p, without_p = [0, 2, 4], [1, 3]
+    rp = [pre if i in with_p else None for i in range(len(rows))]
+    outm, dbgm = ctx.eval_rows(toks, offs, KIND_BOOL, allowed, row_prefix=rp, debug_logits=True)
+    refa = orc.eval_rows(prefix, [rows[i] for i in with_p], KIND_BOOL, allowed, keep_logits=True)
+    refb = orc.eval_rows(None, [rows[i] for i in without_p], KIND_BOOL, allowed, keep_logits=True)
+    _log("mixed, with prefix", compare(refa, outm[with_p], dbgm[with_p], "mixed, with prefix"))
+    _log("mixed, no prefix", compare(refb, outm[without_p], dbgm[without_p], "mixed, no prefix"))
+    ctx.release_prefix(pre)
+
+
 def test_tiny_dedup_and_batch_invariance(tiny, L):
     w, orc, ctx = tiny
     wl = make_workload("filter_tiny")
