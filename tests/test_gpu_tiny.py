@@ -191,6 +191,27 @@ def test_tiny_restricted_head(tiny, L):
     ctx.release_prefix(pre)
 
 
+def test_tiny_prefix_cached_equals_inlined(tiny, L):
+    """Prefix reuse changes nothing but cost: the rows evaluated against a
+    cached prefix agree with the same rows carrying the prefix tokens
+    inline (and with the oracle's full forward)."""
+    w, orc, ctx = tiny
+    wl = make_workload("filter_tiny", n_rows=24)
+    pre = ctx.set_prefix(wl.prefix)
+    cached, dc = _run(ctx, wl, pre)
+    rows = [np.concatenate([wl.prefix, wl.suffix(r)]) for r in range(wl.n_rows)]
+    offs = np.concatenate([[0], np.cumsum([len(r) for r in rows])])
+    inl, di = ctx.eval_rows(np.concatenate(rows), offs, wl.kind, wl.allowed, debug_logits=True)
+    ref = orc.eval_workload(wl, keep_logits=True)
+    _log("cached", compare(ref, cached, dc, "cached"))
+    _log("inlined", compare(ref, inl, di, "inlined"))
+    sigma = float(np.std(dc))
+    assert np.abs(dc - di).max() <= 0.05 * sigma
+    clear = ref["margin"] > 0.1
+    assert np.array_equal(cached["value"][clear], inl["value"][clear])
+    ctx.release_prefix(pre)
+
+
 def test_tiny_edge_cases(tiny, L):
     """A single allowed option (log-probability exactly 0), a one-token
     integer, a 300-token row beside one-token rows under a batch budget
