@@ -264,7 +264,7 @@ def main():
     kids = None
     row_prefix = None
     if wl.children is not None:
-        kids = [ctx.set_prefix(c, parent=root) for c in wl.children]
+        kids = ctx.set_prefixes(wl.children, parent=root)
         row_prefix = [kids[int(i)] for i in wl.row_child]
     t_prefix = time.perf_counter() - t0
     log(f"[bench] load {t_load:.2f} s, prefix {t_prefix * 1e3:.1f} ms")

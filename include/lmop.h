@@ -117,6 +117,17 @@ lmop_status lmop_load_weights(lmop_ctx* ctx, const lmop_weights* w);
  * last child is released). */
 lmop_status lmop_set_prefix(lmop_ctx* ctx, const lmop_prefix* parent, const int32_t* tokens,
                             int32_t n_tokens, lmop_prefix** out);
+
+/* Computes n prefixes with the same parent in one batched pass: prefix i
+ * holds tokens[offsets[i] .. offsets[i+1]) (host CSR, offsets[0] = 0, every
+ * prefix at least one token).  The result equals n calls of
+ * lmop_set_prefix, bit for bit; it is the form a join needs, one child
+ * (instruction + left value) per left value.  The n prefixes share one
+ * device allocation, freed when the last of them is released; each is
+ * released on its own.  n == 0 does nothing.  out: host [n]; on failure no
+ * prefix is created and out is all NULL. */
+lmop_status lmop_set_prefixes(lmop_ctx* ctx, const lmop_prefix* parent, const int32_t* tokens,
+                              const int64_t* offsets, int32_t n, lmop_prefix** out);
 lmop_status lmop_release_prefix(lmop_ctx* ctx, lmop_prefix* prefix);
 /* Total sequence length of a prefix (ancestors included); -1 for NULL. */
 int32_t lmop_prefix_length(const lmop_prefix* prefix);

@@ -87,7 +87,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
     kb_s[s] = base;
     vb_s[s] = base + (size_t)cap * kvdim;
     cap_s[s] = cap;
-    start_s[s] = 0;
+    start_s[s] = row.seg_start[s];
     n_s[s] = row.seg_n[s];
   }
   {

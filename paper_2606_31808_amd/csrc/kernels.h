@@ -100,6 +100,7 @@ struct AttnRow {
   const half_bits* seg_kv[2];  // prefix-chain KV stores (root, child), or NULL
   int seg_n[2];                // tokens of each segment (0 if absent)
   int seg_cap[2];              // slots C of each segment's store
+  int seg_start[2];            // slot of the segment's first token in its store
   int q_start;                 // first query token of the row in the batch buffers
   int n_q;                     // query tokens of the row in this launch
   int own_slot;                // slot of own token 0 in the own-KV store (multiple of 8)

@@ -55,13 +55,25 @@ struct BatchRow {
 
 }  // namespace
 
+namespace {
+// Device storage shared by the prefixes made in one call: their KV store and
+// their final hidden states; freed with the last of those prefixes.
+struct KvStore {
+  uint16_t* kv = nullptr;     // per layer K [cap][nkv][hd], V^T [nkv][hd][cap]
+  float* hidden = nullptr;    // [n][d]
+  int refs = 0;
+};
+}  // namespace
+
 struct lmop_prefix {
   lmop_ctx* ctx = nullptr;
   lmop_prefix* parent = nullptr;
   int n = 0;       // own tokens
   int start = 0;   // tokens of the parent chain
-  int cap = 0;     // slots of the KV store (n rounded up to 64)
-  uint16_t* kv = nullptr;     // device KV store: per layer K [cap][nkv][hd], V^T [nkv][hd][cap]
+  int cap = 0;     // slots of the KV store (a multiple of 64)
+  int slot0 = 0;   // slot of the prefix's first token in the store (a multiple of 8)
+  KvStore* store = nullptr;
+  uint16_t* kv = nullptr;     // = store->kv
   float* hidden = nullptr;    // device [d]: last token's final-layer hidden state
   int children = 0;
   bool released = false;
@@ -636,6 +648,7 @@ void fill_segments(const lmop_prefix* p, AttnRow& r) {
   r.seg_kv[0] = r.seg_kv[1] = nullptr;
   r.seg_n[0] = r.seg_n[1] = 0;
   r.seg_cap[0] = r.seg_cap[1] = 0;
+  r.seg_start[0] = r.seg_start[1] = 0;
   if (!p) return;
   const lmop_prefix* chain[2] = {p->parent ? p->parent : p, p->parent ? p : nullptr};
   for (int s = 0; s < 2; ++s)
@@ -643,6 +656,7 @@ void fill_segments(const lmop_prefix* p, AttnRow& r) {
       r.seg_kv[s] = chain[s]->kv;
       r.seg_n[s] = chain[s]->n;
       r.seg_cap[s] = chain[s]->cap;
+      r.seg_start[s] = chain[s]->slot0;
     }
 }
 
@@ -808,8 +822,12 @@ const char* lmop_last_error(const lmop_ctx* ctx) {
 }
 
 static void destroy_prefix_storage(lmop_prefix* p) {
-  if (p->kv) (void)hipFree(p->kv);
-  if (p->hidden) (void)hipFree(p->hidden);
+  if (p->store && --p->store->refs == 0) {
+    if (p->store->kv) (void)hipFree(p->store->kv);
+    if (p->store->hidden) (void)hipFree(p->store->hidden);
+    delete p->store;
+  }
+  p->store = nullptr;
   p->kv = nullptr;
   p->hidden = nullptr;
 }
@@ -963,97 +981,174 @@ lmop_status lmop_load_weights(lmop_ctx* ctx, const lmop_weights* w) {
 
 int32_t lmop_prefix_length(const lmop_prefix* p) { return p ? p->start + p->n : -1; }
 
+// n prefixes of `parent`, prefix i = tokens[offsets[i] .. offsets[i+1]), all in
+// one KV store: prefix i's slots start at slot0[i] (8-aligned), and the store
+// is wide enough for every prefix's last 64-key attention block.  The
+// forward passes are the batched prefill of row evaluation, so each prefix
+// is bit for bit what a store of its own would hold.
+static lmop_status make_prefixes(lmop_ctx* ctx, const lmop_prefix* parent, const int32_t* tokens,
+                                 const int64_t* offsets, int n, lmop_prefix** out) {
+  const lmop_config& cf = ctx->cfg;
+  const int start = prefix_total(parent);
+  std::vector<int> len(n), slot0(n);
+  int used = 0, need = 0;
+  for (int i = 0; i < n; ++i) {
+    len[i] = (int)(offsets[i + 1] - offsets[i]);
+    slot0[i] = used;
+    need = std::max(need, used + round_up(len[i], 64));
+    used = round_up(used + len[i], 8);
+  }
+  const int cap = round_up(need, 64);
+  KvStore* store = nullptr;
+  if (!ctx->host_only) {
+    store = new KvStore();
+    auto fail_free = [&](lmop_status st) {
+      if (store->kv) (void)hipFree(store->kv);
+      if (store->hidden) (void)hipFree(store->hidden);
+      delete store;
+      return st;
+    };
+    void* kv = nullptr;
+    void* hid = nullptr;
+    const size_t kv_bytes = (size_t)cf.n_layers * 2 * cap * ctx->nkv_dim * 2;
+    lmop_status st = dev_alloc(ctx, &kv, kv_bytes);
+    if (st != LMOP_OK) return fail_free(st);
+    store->kv = (uint16_t*)kv;
+    st = dev_alloc(ctx, &hid, (size_t)n * cf.d_model * 4);
+    if (st != LMOP_OK) return fail_free(st);
+    store->hidden = (float*)hid;
+    // slots no prefix uses are read (masked) by attention: keep them finite
+    if (hipMemsetAsync(kv, 0, kv_bytes, ctx->stream) != hipSuccess)
+      return fail_free(fail(ctx, LMOP_ERR_DEVICE, "hipMemsetAsync of a prefix KV store failed"));
+    const int G = cf.n_heads / cf.n_kv_heads;
+    for (int i0 = 0; i0 < n && st == LMOP_OK;) {
+      // prefixes [i0, i1) in one forward pass, within the default token budget
+      int i1 = i0, T = 0;
+      while (i1 < n && (i1 == i0 || T + len[i1] <= kDefaultBatchTokens) &&
+             i1 - i0 < kMaxBatchRows)
+        T += len[i1++];
+      const int R = i1 - i0;
+      std::vector<int32_t> tok(T), pos(T), slot(T), last(R);
+      std::vector<AttnRow> rows(R);
+      std::vector<int2> work;
+      Batch b;
+      int t = 0;
+      for (int i = i0; i < i1; ++i) {
+        const int k = i - i0;
+        for (int j = 0; j < len[i]; ++j) {
+          tok[t + j] = tokens[offsets[i] + j];
+          pos[t + j] = start + j;
+          slot[t + j] = slot0[i] + j;
+        }
+        fill_segments(parent, rows[k]);
+        rows[k].q_start = t;
+        rows[k].n_q = len[i];
+        rows[k].own_slot = slot0[i];
+        rows[k].own_q0 = 0;
+        add_work(work, k, len[i], G);
+        last[k] = t + len[i] - 1;
+        b.visible_keys += (double)len[i] * start + 0.5 * (double)len[i] * (len[i] + 1);
+        t += len[i];
+      }
+      st = stage_begin(ctx, 0, stage_need(T, R, work.size()));
+      if (st == LMOP_OK) st = upload_batch(ctx, 0, tok, pos, slot, rows, work, last);
+      b.T = T;
+      b.R = R;
+      b.n_work = (int)work.size();
+      b.own_kv = store->kv;
+      b.own_cap = cap;
+      b.n_last = cf.n_layers > 0 ? R : 0;
+      if (st == LMOP_OK) st = forward(ctx, b);
+      // the final hidden state of each prefix's last token (the whole model when L = 0)
+      float* src = nullptr;
+      if (st == LMOP_OK && cf.n_layers > 0) {
+        st = ws_get(ctx, "xlast", (size_t)R * cf.d_model, &src);
+        if (st == LMOP_OK &&
+            hipMemcpyAsync(store->hidden + (size_t)i0 * cf.d_model, src,
+                           (size_t)R * cf.d_model * 4, hipMemcpyDeviceToDevice,
+                           ctx->stream) != hipSuccess)
+          st = fail(ctx, LMOP_ERR_DEVICE, "copy of prefix hidden states failed");
+      } else if (st == LMOP_OK) {
+        st = ws_get(ctx, "x", (size_t)T * cf.d_model, &src);
+        for (int k = 0; k < R && st == LMOP_OK; ++k)
+          if (hipMemcpyAsync(store->hidden + (size_t)(i0 + k) * cf.d_model,
+                             src + (size_t)last[k] * cf.d_model, (size_t)cf.d_model * 4,
+                             hipMemcpyDeviceToDevice, ctx->stream) != hipSuccess)
+            st = fail(ctx, LMOP_ERR_DEVICE, "copy of prefix hidden states failed");
+      }
+      if (st == LMOP_OK) st = stage_mark(ctx, 0);
+      if (st == LMOP_OK) st = sync(ctx);
+      i0 = i1;
+    }
+    if (st != LMOP_OK) return fail_free(st);
+    store->refs = n;
+  }
+  for (int i = 0; i < n; ++i) {
+    lmop_prefix* p = new lmop_prefix();
+    p->ctx = ctx;
+    p->parent = const_cast<lmop_prefix*>(parent);
+    p->n = len[i];
+    p->start = start;
+    p->cap = cap;
+    p->slot0 = slot0[i];
+    p->store = store;
+    p->kv = store ? store->kv : nullptr;
+    p->hidden = store ? store->hidden + (size_t)i * cf.d_model : nullptr;
+    p->generation = ctx->generation;
+    p->id = ctx->next_prefix_id++;
+    ctx->prefixes.insert(p);
+    out[i] = p;
+  }
+  if (parent) const_cast<lmop_prefix*>(parent)->children += n;
+  return LMOP_OK;
+}
+
+// checks shared by lmop_set_prefix and lmop_set_prefixes
+static lmop_status check_prefix_parent(lmop_ctx* ctx, const lmop_prefix* parent) {
+  if (!ctx->loaded) return fail(ctx, LMOP_ERR_STATE, "lmop_load_weights has not succeeded");
+  if (parent && !prefix_live(ctx, parent))
+    return fail(ctx, LMOP_ERR_INVALID_ARG, "parent prefix is released or from another ctx");
+  if (parent && parent->parent)
+    return fail(ctx, LMOP_ERR_UNSUPPORTED, "a child prefix cannot have children");
+  return LMOP_OK;
+}
+
 lmop_status lmop_set_prefix(lmop_ctx* ctx, const lmop_prefix* parent, const int32_t* tokens,
                             int32_t n_tokens, lmop_prefix** out) {
   if (out) *out = nullptr;
   LMOP_TRY(enter(ctx));
   if (!out) return fail(ctx, LMOP_ERR_INVALID_ARG, "out is NULL");
-  if (!ctx->loaded) return fail(ctx, LMOP_ERR_STATE, "lmop_load_weights has not succeeded");
+  LMOP_TRY(check_prefix_parent(ctx, parent));
   if (n_tokens < 1 || !tokens)
     return fail(ctx, LMOP_ERR_INVALID_ARG, "a prefix needs at least one token");
-  if (parent && !prefix_live(ctx, parent))
-    return fail(ctx, LMOP_ERR_INVALID_ARG, "parent prefix is released or from another ctx");
-  if (parent && parent->parent)
-    return fail(ctx, LMOP_ERR_UNSUPPORTED, "a child prefix cannot have children");
   LMOP_TRY(check_tokens(ctx, tokens, n_tokens, "prefix"));
-  const lmop_config& cf = ctx->cfg;
-  const int start = prefix_total(parent);
-  if (start + n_tokens >= cf.max_seq)
+  if (prefix_total(parent) + n_tokens >= ctx->cfg.max_seq)
     return fail(ctx, LMOP_ERR_INVALID_ARG, "prefix length %d exceeds max_seq %d",
-                start + n_tokens, cf.max_seq);
+                prefix_total(parent) + n_tokens, ctx->cfg.max_seq);
+  const int64_t offs[2] = {0, n_tokens};
+  return make_prefixes(ctx, parent, tokens, offs, 1, out);
+}
 
-  std::unique_ptr<lmop_prefix> p(new lmop_prefix());
-  p->ctx = ctx;
-  p->parent = const_cast<lmop_prefix*>(parent);
-  p->n = n_tokens;
-  p->start = start;
-  p->generation = ctx->generation;
-  p->id = ctx->next_prefix_id++;
-  p->cap = round_up(n_tokens, 64);
-  if (!ctx->host_only) {
-    void* kv = nullptr;
-    void* hid = nullptr;
-    const size_t kv_bytes = (size_t)cf.n_layers * 2 * p->cap * ctx->nkv_dim * 2;
-    LMOP_TRY(dev_alloc(ctx, &kv, kv_bytes));
-    p->kv = (uint16_t*)kv;
-    // pad slots are read (masked) by attention: keep them finite
-    if (hipMemsetAsync(kv, 0, kv_bytes, ctx->stream) != hipSuccess) {
-      destroy_prefix_storage(p.get());
-      return fail(ctx, LMOP_ERR_DEVICE, "hipMemsetAsync of a prefix KV store failed");
-    }
-    if (dev_alloc(ctx, &hid, (size_t)cf.d_model * 4) != LMOP_OK) {
-      destroy_prefix_storage(p.get());
-      return LMOP_ERR_OOM;
-    }
-    p->hidden = (float*)hid;
-    std::vector<int32_t> tok(tokens, tokens + n_tokens), pos(n_tokens), slot(n_tokens);
-    for (int j = 0; j < n_tokens; ++j) {
-      pos[j] = start + j;
-      slot[j] = j;
-    }
-    std::vector<AttnRow> rows(1);
-    fill_segments(parent, rows[0]);
-    rows[0].q_start = 0;
-    rows[0].n_q = n_tokens;
-    rows[0].own_slot = 0;
-    rows[0].own_q0 = 0;
-    std::vector<int2> work;
-    add_work(work, 0, n_tokens, cf.n_heads / cf.n_kv_heads);
-    const std::vector<int32_t> last = {n_tokens - 1};
-    lmop_status st = stage_begin(ctx, 0, stage_need(n_tokens, 1, work.size()));
-    if (st == LMOP_OK) st = upload_batch(ctx, 0, tok, pos, slot, rows, work, last);
-    Batch b;
-    b.T = n_tokens;
-    b.R = 1;
-    b.n_work = (int)work.size();
-    b.own_kv = p->kv;
-    b.own_cap = p->cap;
-    b.n_last = 1;
-    b.visible_keys = (double)n_tokens * start + 0.5 * (double)n_tokens * (n_tokens + 1);
-    if (st == LMOP_OK) st = forward(ctx, b);
-    if (st == LMOP_OK) {
-      // the final hidden state of the last token (the whole model when L = 0)
-      float* src = nullptr;
-      st = cf.n_layers > 0 ? ws_get(ctx, "xlast", (size_t)cf.d_model, &src)
-                           : ws_get(ctx, "x", (size_t)n_tokens * cf.d_model, &src);
-      if (cf.n_layers == 0) src += (size_t)(n_tokens - 1) * cf.d_model;
-      if (st == LMOP_OK) {
-        hipError_t e = hipMemcpyAsync(p->hidden, src, (size_t)cf.d_model * 4,
-                                      hipMemcpyDeviceToDevice, ctx->stream);
-        if (e != hipSuccess) st = fail(ctx, LMOP_ERR_DEVICE, "copy of prefix hidden failed");
-      }
-    }
-    if (st == LMOP_OK) st = stage_mark(ctx, 0);
-    if (st == LMOP_OK) st = sync(ctx);
-    if (st != LMOP_OK) {
-      destroy_prefix_storage(p.get());
-      return st;
-    }
+lmop_status lmop_set_prefixes(lmop_ctx* ctx, const lmop_prefix* parent, const int32_t* tokens,
+                              const int64_t* offsets, int32_t n, lmop_prefix** out) {
+  if (out && n > 0)
+    for (int i = 0; i < n; ++i) out[i] = nullptr;
+  LMOP_TRY(enter(ctx));
+  if (n < 0) return fail(ctx, LMOP_ERR_INVALID_ARG, "n < 0");
+  if (n == 0) return LMOP_OK;
+  if (!out || !offsets || !tokens)
+    return fail(ctx, LMOP_ERR_INVALID_ARG, "NULL tokens, offsets or out");
+  LMOP_TRY(check_prefix_parent(ctx, parent));
+  if (offsets[0] != 0) return fail(ctx, LMOP_ERR_INVALID_ARG, "offsets[0] != 0");
+  for (int i = 0; i < n; ++i) {
+    const int64_t len = offsets[i + 1] - offsets[i];
+    if (len < 1) return fail(ctx, LMOP_ERR_INVALID_ARG, "prefix %d has no tokens", i);
+    if (prefix_total(parent) + len >= ctx->cfg.max_seq)
+      return fail(ctx, LMOP_ERR_INVALID_ARG, "prefix %d: length %lld exceeds max_seq %d", i,
+                  (long long)(prefix_total(parent) + len), ctx->cfg.max_seq);
   }
-  if (parent) const_cast<lmop_prefix*>(parent)->children++;
-  ctx->prefixes.insert(p.get());
-  *out = p.release();
-  return LMOP_OK;
+  LMOP_TRY(check_tokens(ctx, tokens, offsets[n], "prefix"));
+  return make_prefixes(ctx, parent, tokens, offsets, n, out);
 }
 
 static void maybe_free_prefix(lmop_ctx* ctx, lmop_prefix* p) {

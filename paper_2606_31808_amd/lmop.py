@@ -25,7 +25,7 @@ LMOP_HEAD_RESTRICTED = 2
 
 EXPORTED = (
     "lmop_create", "lmop_destroy", "lmop_last_error", "lmop_status_string", "lmop_load_weights",
-    "lmop_set_prefix", "lmop_release_prefix", "lmop_prefix_length", "lmop_eval_rows",
+    "lmop_set_prefix", "lmop_set_prefixes", "lmop_release_prefix", "lmop_prefix_length", "lmop_eval_rows",
     "lmop_dedup_rows", "lmop_set_profiling", "lmop_get_kernel_stats",
 )
 
@@ -91,6 +91,8 @@ def _load():
         "lmop_status_string": (C.c_char_p, [st]),
         "lmop_load_weights": (st, [vp, C.POINTER(lmop_weights)]),
         "lmop_set_prefix": (st, [vp, vp, C.POINTER(C.c_int32), i32, C.POINTER(vp)]),
+        "lmop_set_prefixes": (st, [vp, vp, C.POINTER(C.c_int32), C.POINTER(C.c_int64), i32,
+                                   C.POINTER(vp)]),
         "lmop_release_prefix": (st, [vp, vp]),
         "lmop_prefix_length": (i32, [vp]),
         "lmop_eval_rows": (st, [vp, vp, C.POINTER(vp), C.POINTER(C.c_int32),
@@ -194,6 +196,19 @@ def lmop_set_prefix(ctx, tokens, parent=None):
     return out
 
 
+def lmop_set_prefixes(ctx, token_lists, parent=None):
+    lists = [_i32(t) for t in token_lists]
+    n = len(lists)
+    offs = np.zeros(n + 1, dtype=np.int64)
+    offs[1:] = np.cumsum([len(t) for t in lists])
+    t = np.concatenate(lists) if n else np.zeros(0, dtype=np.int32)
+    t = np.ascontiguousarray(t, dtype=np.int32)
+    out = (C.c_void_p * max(n, 1))()
+    _check(_lib.lmop_set_prefixes(ctx, parent, _ptr(t, C.c_int32), _ptr(offs, C.c_int64), n,
+                                  out), ctx)
+    return [C.c_void_p(out[i]) for i in range(n)]
+
+
 def lmop_release_prefix(ctx, prefix) -> None:
     _check(_lib.lmop_release_prefix(ctx, prefix), ctx)
 
@@ -295,6 +310,9 @@ class Context:
 
     def set_prefix(self, tokens, parent=None):
         return lmop_set_prefix(self.ctx, tokens, parent)
+
+    def set_prefixes(self, token_lists, parent=None):
+        return lmop_set_prefixes(self.ctx, token_lists, parent)
 
     def release_prefix(self, p):
         lmop_release_prefix(self.ctx, p)

@@ -165,7 +165,8 @@ def test_join_8b_sampled_pairs(m8b):
     w, ctx, orc = m8b
     wl = make_workload("join_8b")
     root = ctx.set_prefix(wl.prefix)
-    kids = [ctx.set_prefix(c, parent=root) for c in wl.children]
+    _log(f"join_8b: {len(wl.children)} child prefixes in one batched call")
+    kids = ctx.set_prefixes(wl.children, parent=root)
     row_prefix = [kids[int(i)] for i in wl.row_child]
     _log(f"join_8b: full table ({wl.n_rows} pairs)")
     full, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, row_prefix=row_prefix)
@@ -175,6 +176,16 @@ def test_join_8b_sampled_pairs(m8b):
     out, dbg = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed,
                              row_prefix=[row_prefix[r] for r in rows], debug_logits=True)
     _same_rows(full, out, rows, "join_8b")
+    # the sampled pairs against children made one at a time: the same bits
+    single = {int(wl.row_child[r]): None for r in rows}
+    for i in single:
+        single[i] = ctx.set_prefix(wl.children[i], parent=root)
+    out1, dbg1 = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed,
+                               row_prefix=[single[int(wl.row_child[r])] for r in rows],
+                               debug_logits=True)
+    assert out1.tobytes() == out.tobytes() and np.array_equal(dbg1, dbg)
+    for p in single.values():
+        ctx.release_prefix(p)
     _log(f"join_8b: oracle on {len(rows)} pairs")
     ref = orc.eval_workload(sub, keep_logits=True)
     st = compare(ref, out, dbg, "join_8b")

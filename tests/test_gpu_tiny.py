@@ -134,6 +134,50 @@ def test_tiny_join_two_level_prefix(tiny, L):
         ctx.release_prefix(k)
 
 
+def test_tiny_batched_children_equal_single(tiny, L):
+    """Children made in one lmop_set_prefixes call share a KV store at 8-aligned
+    offsets; rows evaluated against them equal, bit for bit, rows evaluated
+    against children made one at a time (also rows with no suffix, which read
+    the child's stored hidden state), and releasing some keeps the rest valid."""
+    w, orc, ctx = tiny
+    rng = np.random.default_rng(41)
+    root_t = rng.integers(0, TINY.vocab, size=45).astype(np.int32)
+    lens = (1, 8, 17, 64, 65, 9, 30)
+    kids_t = [rng.integers(0, TINY.vocab, size=n).astype(np.int32) for n in lens]
+    root = ctx.set_prefix(root_t)
+    single = [ctx.set_prefix(k, parent=root) for k in kids_t]
+    _log("batched children: set_prefixes")
+    batched = ctx.set_prefixes(kids_t, parent=root)
+    rights = [rng.integers(0, TINY.vocab, size=int(n)).astype(np.int32) for n in (0, 7, 23)]
+    rc = [i for i in range(len(lens)) for _ in rights]
+    rows = [r for _ in lens for r in rights]
+    toks = np.concatenate(rows)
+    offs = np.concatenate([[0], np.cumsum([len(r) for r in rows])])
+    allowed = rng.choice(TINY.vocab, 3, replace=False)
+    o1, d1 = ctx.eval_rows(toks, offs, KIND_ENUM, allowed,
+                           row_prefix=[single[i] for i in rc], debug_logits=True)
+    o2, d2 = ctx.eval_rows(toks, offs, KIND_ENUM, allowed,
+                           row_prefix=[batched[i] for i in rc], debug_logits=True)
+    assert o1.tobytes() == o2.tobytes() and np.array_equal(d1, d2)
+    ref = orc.eval_rows(root_t, rows, KIND_ENUM, allowed, children=kids_t, row_child=rc,
+                        keep_logits=True)
+    _log("batched children", compare(ref, o2, d2, "batched children"))
+    for i in (0, 3, 5):
+        ctx.release_prefix(batched[i])
+    keep = [i for i in range(len(lens)) if i not in (0, 3, 5)]
+    sel = [j for j, i in enumerate(rc) if i in keep]
+    rows_k = [rows[j] for j in sel]
+    offs_k = np.concatenate([[0], np.cumsum([len(r) for r in rows_k])])
+    o3, d3 = ctx.eval_rows(np.concatenate(rows_k), offs_k, KIND_ENUM, allowed,
+                           row_prefix=[batched[rc[j]] for j in sel], debug_logits=True)
+    assert o3.tobytes() == o1[sel].tobytes() and np.array_equal(d3, d1[sel])
+    for i in keep:
+        ctx.release_prefix(batched[i])
+    for p in single:
+        ctx.release_prefix(p)
+    ctx.release_prefix(root)
+
+
 def test_tiny_int_decode(L):
     w = make_weights(TINY, seed=1234)
     rng = np.random.default_rng(5)

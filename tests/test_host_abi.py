@@ -150,6 +150,27 @@ def test_prefix_lifetimes(tiny_w):
     _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [7], [0, 1], prefix=p3, **ok)
 
 
+def test_set_prefixes_validation(tiny_w):
+    ctx = _host_ctx()
+    _expect(L.LMOP_ERR_STATE, ctx.set_prefixes, [[1, 2]])
+    ctx.load_weights(tiny_w)
+    assert ctx.set_prefixes([]) == []
+    root = ctx.set_prefix([1, 2, 3])
+    kids = ctx.set_prefixes([[4, 5], [6], [7, 8, 9]], parent=root)
+    assert [L.lmop_prefix_length(k) for k in kids] == [5, 4, 6]
+    assert len({k.value for k in kids}) == 3
+    _expect(L.LMOP_ERR_UNSUPPORTED, ctx.set_prefixes, [[6]], parent=kids[0])
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.set_prefixes, [[1], []], parent=root)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.set_prefixes, [[1], [TINY.vocab]], parent=root)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.set_prefixes, [[1] * 4096], parent=root)
+    # the root outlives its release while batched children exist; children free one by one
+    ctx.release_prefix(root)
+    ctx.release_prefix(kids[1])
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.release_prefix, kids[1])
+    ctx.release_prefix(kids[0])
+    ctx.release_prefix(kids[2])
+
+
 def _py_dedup(rows, keys):
     first = {}
     rep = []
