@@ -27,6 +27,8 @@ namespace {
 
 constexpr int kDefaultBatchTokens = 16384;
 constexpr int kMaxBatchRows = 2048;
+// own-KV bytes of one integer-decode group (also at most half the free memory)
+constexpr size_t kDecodeGroupBytes = size_t(24) << 30;
 
 int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
@@ -45,12 +47,6 @@ struct Span {
   std::string name;
   hipEvent_t a, b;
   double flops, bytes;
-};
-
-struct BatchRow {
-  const lmop_prefix* pfx;
-  const int32_t* toks;
-  int len;
 };
 
 }  // namespace
@@ -1294,37 +1290,85 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
     u0 = u1;
   }
 
-  // A batch between enqueue and finish: what its constrained steps need.
+  // Own-KV placement.  Integer types decode their further tokens for a group
+  // of consecutive batches at once: the group's batches keep their KV in one
+  // store, so each decode step is one forward over all live rows of the
+  // group instead of one small forward per batch.  A group is bounded by the
+  // store's size and by the token budget (a decode step has one token per
+  // live row).  Other types need no KV after the first step: one batch each.
+  const size_t slot_bytes = (size_t)cf.n_layers * 2 * ctx->nkv_dim * 2;
+  size_t group_bytes = kDecodeGroupBytes;
+  if (dec > 0) {
+    size_t free_b = 0, total_b = 0;
+    if (hipMemGetInfo(&free_b, &total_b) == hipSuccess)
+      group_bytes = std::max<size_t>(std::min(group_bytes, free_b / 2), 1);
+  }
+  const int n_batches = (int)batches.size();
+  std::vector<int> base_of(n_batches), group_of(n_batches);
+  std::vector<int> group_cap;
+  for (int b = 0; b < n_batches;) {
+    int b1 = b, used = 0;
+    size_t rows = 0;
+    std::vector<int> base;
+    while (b1 < n_batches) {
+      int slots = 0;
+      for (size_t u = batches[b1].first; u < batches[b1].second; ++u)
+        slots = round_up(slots + (int)(offsets[uniq[u] + 1] - offsets[uniq[u]]) + dec, 8);
+      const size_t r = batches[b1].second - batches[b1].first;
+      if (b1 > b && (dec == 0 || (size_t)own_store_cap(used + slots) * slot_bytes > group_bytes ||
+                     rows + r > (size_t)budget))
+        break;
+      base_of[b1] = used;
+      group_of[b1] = (int)group_cap.size();
+      used += slots;
+      rows += r;
+      ++b1;
+    }
+    group_cap.push_back(own_store_cap(used));
+    b = b1;
+  }
+
+  // per distinct row (index into uniq): own tokens, slot of own token 0 in
+  // its group's store, last chosen token
+  std::vector<int> row_len(uniq.size()), own_slot(uniq.size());
+  std::vector<int32_t> last_tok(uniq.size(), -1);
+  for (size_t u = 0; u < uniq.size(); ++u)
+    row_len[u] = (int)(offsets[uniq[u] + 1] - offsets[uniq[u]]);
+
+  // A batch between enqueue and collect: where its first step's picks land.
   struct InFlight {
     size_t u0 = 0;
     int R = 0;
     int k = 0;  // staging slot
-    std::vector<int> len, own;
-    int own_cap = 0;
-    uint16_t* own_kv = nullptr;
     HeadPick* picks = nullptr;
     float* dump = nullptr;
   };
+  uint16_t* own_kv = nullptr;  // the current group's store
 
   // Packs and uploads one batch, runs its prefill and its first head step;
   // nothing here waits for the GPU.
-  auto enqueue = [&](size_t u0, size_t u1, int k, InFlight& B) -> lmop_status {
-    const int R = (int)(u1 - u0);
+  auto enqueue = [&](int bi, InFlight& B) -> lmop_status {
+    const size_t u0 = batches[bi].first, u1 = batches[bi].second;
+    const int R = (int)(u1 - u0), k = bi & 1;
+    const int cap_g = group_cap[group_of[bi]];
+    if (bi == 0 || group_of[bi] != group_of[bi - 1])
+      LMOP_TRY(ws_get(ctx, "own_kv", (size_t)cap_g * slot_bytes / 2, &own_kv, true));
     int T = 0;
-    for (size_t u = u0; u < u1; ++u) T += (int)(offsets[uniq[u] + 1] - offsets[uniq[u]]);
+    for (size_t u = u0; u < u1; ++u) T += row_len[u];
     std::vector<int32_t> tok(T), pos(T), slot(T);
     std::vector<AttnRow> rows(R);
     std::vector<int2> work;
-    std::vector<int> len(R), own(R), qs(R);
-    int t = 0, cap = 0;
+    std::vector<int> qs(R);
+    int t = 0, cap = base_of[bi];
     for (int i = 0; i < R; ++i) {
-      const int r = uniq[u0 + i];
+      const size_t u = u0 + i;
+      const int r = uniq[u];
       const lmop_prefix* p = pf[r];
-      len[i] = (int)(offsets[r + 1] - offsets[r]);
-      own[i] = cap;
+      const int len = row_len[u];
+      own_slot[u] = cap;
       qs[i] = t;
       const int P = prefix_total(p);
-      for (int j = 0; j < len[i]; ++j) {
+      for (int j = 0; j < len; ++j) {
         tok[t + j] = tokens[offsets[r] + j];
         pos[t + j] = P + j;
         slot[t + j] = cap + j;
@@ -1332,36 +1376,33 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
       AttnRow& ar = rows[i];
       fill_segments(p, ar);
       ar.q_start = t;
-      ar.n_q = len[i];
+      ar.n_q = len;
       ar.own_slot = cap;
       ar.own_q0 = 0;
-      add_work(work, i, len[i], G);
-      t += len[i];
-      cap = round_up(cap + len[i] + dec, 8);
+      add_work(work, i, len, G);
+      t += len;
+      cap = round_up(cap + len + dec, 8);
     }
-    cap = own_store_cap(cap);
     // each row's last token (rows with suffix tokens only)
     std::vector<int32_t> last;
     std::vector<int> last_of(R, -1);
     for (int i = 0; i < R; ++i)
-      if (len[i] > 0) {
+      if (row_len[u0 + i] > 0) {
         last_of[i] = (int)last.size();
-        last.push_back(qs[i] + len[i] - 1);
+        last.push_back(qs[i] + row_len[u0 + i] - 1);
       }
     LMOP_TRY(stage_begin(ctx, k, stage_need(T, R, work.size())));
-    uint16_t* own_kv;
-    LMOP_TRY(ws_get(ctx, "own_kv", (size_t)cf.n_layers * 2 * cap * ctx->nkv_dim, &own_kv, true));
     LMOP_TRY(upload_batch(ctx, k, tok, pos, slot, rows, work, last));
     Batch b;
     b.T = T;
     b.R = R;
     b.n_work = (int)work.size();
     b.own_kv = own_kv;
-    b.own_cap = cap;
+    b.own_cap = cap_g;
     b.n_last = cf.n_layers > 0 ? (int)last.size() : 0;
     for (int i = 0; i < R; ++i)
-      b.visible_keys += (double)len[i] * prefix_total(pf[uniq[u0 + i]]) +
-                        0.5 * (double)len[i] * (len[i] + 1);
+      b.visible_keys += (double)row_len[u0 + i] * prefix_total(pf[uniq[u0 + i]]) +
+                        0.5 * (double)row_len[u0 + i] * (row_len[u0 + i] + 1);
     LMOP_TRY(forward(ctx, b));
     float* x;
     if (b.n_last > 0)
@@ -1371,10 +1412,10 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
     std::vector<const float*> rowptr(R);
     for (int i = 0; i < R; ++i) {
       const int r = uniq[u0 + i];
-      if (len[i] == 0)
+      if (row_len[u0 + i] == 0)
         rowptr[i] = pf[r]->hidden;
       else
-        rowptr[i] = x + (size_t)(b.n_last > 0 ? last_of[i] : qs[i] + len[i] - 1) * d;
+        rowptr[i] = x + (size_t)(b.n_last > 0 ? last_of[i] : qs[i] + row_len[u0 + i] - 1) * d;
     }
     B.dump = nullptr;
     if (dbg) LMOP_TRY(ws_get(ctx, "dump", (size_t)R * V, &B.dump));
@@ -1384,120 +1425,122 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
     B.u0 = u0;
     B.R = R;
     B.k = k;
-    B.len = std::move(len);
-    B.own = std::move(own);
-    B.own_cap = cap;
-    B.own_kv = own_kv;
     return LMOP_OK;
   };
 
-  // Waits for a batch's first step, then runs its further (integer) steps.
-  auto finish = [&](InFlight& B) -> lmop_status {
-    const size_t u0 = B.u0;
-    const int R = B.R, k = B.k;
-    HIP_OK(ctx, hipEventSynchronize(ctx->stage[k].done));
-    ctx->stage[k].pending = false;
-    std::vector<int> live(R);
-    for (int i = 0; i < R; ++i) live[i] = i;
-    std::vector<int> last_tok(R, -1);
-    for (int i = 0; i < R; ++i) {
-      lmop_result& o = res[uniq[u0 + i]];
+  // Adds one step's pick to a row's result; true if the row decodes further.
+  auto apply_pick = [&](size_t u, const HeadPick& hp) {
+    lmop_result& o = res[uniq[u]];
+    o.logprob += hp.logprob;
+    o.logprob_full += hp.logprob_full;
+    o.tokens[o.n_tokens++] = hp.token;
+    if (type->kind != LMOP_INT) {
+      o.value = hp.index;
+      return false;
+    }
+    if (hp.index == n_allowed0) return false;  // EOS
+    o.value = o.value * 10 + hp.index;
+    last_tok[u] = hp.token;
+    return o.n_tokens < steps;
+  };
+
+  // Waits for a batch's first step and takes its picks; rows that decode
+  // further join the group's live list.
+  std::vector<size_t> live;
+  auto collect = [&](InFlight& B) -> lmop_status {
+    HIP_OK(ctx, hipEventSynchronize(ctx->stage[B.k].done));
+    ctx->stage[B.k].pending = false;
+    for (int i = 0; i < B.R; ++i) {
+      const size_t u = B.u0 + i;
+      const int r = uniq[u];
+      lmop_result& o = res[r];
       o.value = 0;
       o.logprob = 0.f;
       o.logprob_full = 0.f;
       o.n_tokens = 0;
       for (int q = 0; q < 8; ++q) o.tokens[q] = -1;
-    }
-    if (dbg)
-      for (int i = 0; i < R; ++i)
-        std::fill(dbg + (size_t)uniq[u0 + i] * steps * V,
-                  dbg + (size_t)(uniq[u0 + i] + 1) * steps * V, NAN);
-    HeadPick* picks = B.picks;
-    for (int step = 0; step < steps && !live.empty(); ++step) {
-      const int nl = (int)live.size();
-      if (step > 0) {
-        // one more token per live row: its id, position and KV slot
-        std::vector<int32_t> st(nl), sp(nl), ss(nl);
-        std::vector<AttnRow> sr(nl);
-        std::vector<int2> sw;
-        for (int q = 0; q < nl; ++q) {
-          const int i = live[q];
-          const int r = uniq[u0 + i];
-          const int own_idx = B.len[i] + step - 1;
-          st[q] = last_tok[i];
-          sp[q] = prefix_total(pf[r]) + own_idx;
-          ss[q] = B.own[i] + own_idx;
-          fill_segments(pf[r], sr[q]);
-          sr[q].q_start = q;
-          sr[q].n_q = 1;
-          sr[q].own_slot = B.own[i];
-          sr[q].own_q0 = own_idx;
-          add_work(sw, q, 1, G);
-        }
-        LMOP_TRY(stage_begin(ctx, k, stage_need(nl, nl, sw.size())));
-        LMOP_TRY(upload_batch(ctx, k, st, sp, ss, sr, sw));
-        Batch sb;
-        sb.T = nl;
-        sb.R = nl;
-        sb.n_work = (int)sw.size();
-        sb.own_kv = B.own_kv;
-        sb.own_cap = B.own_cap;
-        for (int q = 0; q < nl; ++q) sb.visible_keys += sp[q] + 1;  // position + 1 keys
-        LMOP_TRY(forward(ctx, sb));
-        float* x;
-        LMOP_TRY(ws_get(ctx, "x", (size_t)nl * d, &x));
-        std::vector<const float*> rowptr(nl);
-        for (int q = 0; q < nl; ++q) rowptr[q] = x + (size_t)q * d;
-        LMOP_TRY(run_head(ctx, k, nl, rowptr, d_sel, d_allowed, n_sel, n_sel, restricted, &picks,
-                          B.dump));
-        LMOP_TRY(stage_mark(ctx, k));
-        HIP_OK(ctx, hipEventSynchronize(ctx->stage[k].done));
-        ctx->stage[k].pending = false;
-      }
       if (dbg) {
-        for (int q = 0; q < nl; ++q) {
-          const int r = uniq[u0 + live[q]];
-          HIP_OK(ctx, hipMemcpy(dbg + ((size_t)r * steps + step) * V, B.dump + (size_t)q * V,
-                                (size_t)V * 4, hipMemcpyDeviceToHost));
-        }
+        std::fill(dbg + (size_t)r * steps * V, dbg + (size_t)(r + 1) * steps * V, NAN);
+        HIP_OK(ctx, hipMemcpy(dbg + (size_t)r * steps * V, B.dump + (size_t)i * V,
+                              (size_t)V * 4, hipMemcpyDeviceToHost));
       }
-      std::vector<int> next;
-      for (int q = 0; q < nl; ++q) {
-        const int i = live[q];
-        lmop_result& o = res[uniq[u0 + i]];
-        const HeadPick& hp = picks[q];
-        o.logprob += hp.logprob;
-        o.logprob_full += hp.logprob_full;
-        o.tokens[o.n_tokens++] = hp.token;
-        if (type->kind == LMOP_INT) {
-          if (hp.index == n_allowed0) continue;  // EOS
-          o.value = o.value * 10 + hp.index;
-          last_tok[i] = hp.token;
-          if (o.n_tokens < steps) next.push_back(i);
-        } else {
-          o.value = hp.index;
-        }
-      }
-      live.swap(next);
+      if (apply_pick(u, B.picks[i])) live.push_back(u);
     }
     return LMOP_OK;
   };
 
-  // With one constrained step and no logit dump, a batch's results come only
-  // from its pinned picks: the next batch is enqueued before this one is
-  // finished, so the GPU does not wait while the host packs and reads back.
-  // Integer decode and logit dumps reuse device buffers of the batch, so they
-  // finish each batch before the next starts.
-  const bool ahead = steps == 1 && !dbg;
-  InFlight slots[2];
-  for (size_t bi = 0; bi < batches.size(); ++bi) {
-    InFlight& cur = slots[bi & 1];
-    if (!ahead || bi == 0)
-      LMOP_TRY(enqueue(batches[bi].first, batches[bi].second, (int)(bi & 1), cur));
-    if (ahead && bi + 1 < batches.size())
-      LMOP_TRY(enqueue(batches[bi + 1].first, batches[bi + 1].second, (int)((bi + 1) & 1),
-                       slots[(bi + 1) & 1]));
-    LMOP_TRY(finish(cur));
+  // The further (integer) steps of a group: one forward over all live rows
+  // per step, each row adding one token to its own KV.
+  auto decode = [&](int gi) -> lmop_status {
+    for (int step = 1; step < steps && !live.empty(); ++step) {
+      const int nl = (int)live.size();
+      std::vector<int32_t> st(nl), sp(nl), ss(nl);
+      std::vector<AttnRow> sr(nl);
+      std::vector<int2> sw;
+      for (int q = 0; q < nl; ++q) {
+        const size_t u = live[q];
+        const int r = uniq[u];
+        const int own_idx = row_len[u] + step - 1;
+        st[q] = last_tok[u];
+        sp[q] = prefix_total(pf[r]) + own_idx;
+        ss[q] = own_slot[u] + own_idx;
+        fill_segments(pf[r], sr[q]);
+        sr[q].q_start = q;
+        sr[q].n_q = 1;
+        sr[q].own_slot = own_slot[u];
+        sr[q].own_q0 = own_idx;
+        add_work(sw, q, 1, G);
+      }
+      LMOP_TRY(stage_begin(ctx, 0, stage_need(nl, nl, sw.size())));
+      LMOP_TRY(upload_batch(ctx, 0, st, sp, ss, sr, sw));
+      Batch sb;
+      sb.T = nl;
+      sb.R = nl;
+      sb.n_work = (int)sw.size();
+      sb.own_kv = own_kv;
+      sb.own_cap = group_cap[gi];
+      for (int q = 0; q < nl; ++q) sb.visible_keys += sp[q] + 1;  // position + 1 keys
+      LMOP_TRY(forward(ctx, sb));
+      float* x;
+      LMOP_TRY(ws_get(ctx, "x", (size_t)nl * d, &x));
+      std::vector<const float*> rowptr(nl);
+      for (int q = 0; q < nl; ++q) rowptr[q] = x + (size_t)q * d;
+      float* dump = nullptr;
+      if (dbg) LMOP_TRY(ws_get(ctx, "dump", (size_t)nl * V, &dump));
+      HeadPick* picks;
+      LMOP_TRY(run_head(ctx, 0, nl, rowptr, d_sel, d_allowed, n_sel, n_sel, restricted, &picks,
+                        dump));
+      LMOP_TRY(stage_mark(ctx, 0));
+      HIP_OK(ctx, hipEventSynchronize(ctx->stage[0].done));
+      ctx->stage[0].pending = false;
+      std::vector<size_t> next;
+      for (int q = 0; q < nl; ++q) {
+        const size_t u = live[q];
+        if (dbg)
+          HIP_OK(ctx, hipMemcpy(dbg + ((size_t)uniq[u] * steps + step) * V,
+                                dump + (size_t)q * V, (size_t)V * 4, hipMemcpyDeviceToHost));
+        if (apply_pick(u, picks[q])) next.push_back(u);
+      }
+      live.swap(next);
+    }
+    live.clear();
+    return LMOP_OK;
+  };
+
+  // Without a logit dump a batch's first step needs only its pinned picks:
+  // the next batch of the same group (any next batch, for types without
+  // further steps) is enqueued before this one is collected, so the GPU does
+  // not wait while the host packs and reads back.  A logit dump reuses one
+  // device buffer, so then each batch is collected before the next starts.
+  InFlight fl[2];
+  int next_b = 0;
+  for (int bi = 0; bi < n_batches; ++bi) {
+    if (next_b == bi) LMOP_TRY(enqueue(next_b++, fl[bi & 1]));
+    const bool last_of_group = bi + 1 == n_batches || group_of[bi + 1] != group_of[bi];
+    if (!dbg && next_b == bi + 1 && bi + 1 < n_batches && (dec == 0 || !last_of_group))
+      LMOP_TRY(enqueue(next_b++, fl[(bi + 1) & 1]));
+    LMOP_TRY(collect(fl[bi & 1]));
+    if (dec > 0 && last_of_group) LMOP_TRY(decode(group_of[bi]));
   }
   LMOP_TRY(sync(ctx));
   for (int r = 0; r < n_rows; ++r) {

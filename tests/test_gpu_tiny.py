@@ -203,6 +203,18 @@ def test_tiny_int_decode(L):
     assert_typed(out, KIND_INT, 10, digits, eos, 4)
     lens = set(out["n_tokens"].tolist())
     assert len(lens) >= 2, lens
+    # decode steps run per group of batches: the same bits for any batching
+    # (40-token batches: several batches per group and several groups), with
+    # and without the logit dump (the look-ahead path)
+    toks = np.concatenate(rows)
+    out_b, dbg_b = ctx.eval_rows(toks, offs, KIND_INT, digits, eos=eos, max_tokens=4,
+                                 prefix=pre, debug_logits=True, max_batch_tokens=40)
+    assert out_b.tobytes() == out.tobytes()
+    assert np.array_equal(dbg_b, dbg, equal_nan=True)
+    for mbt in (0, 40, 97):
+        out_n, _ = ctx.eval_rows(toks, offs, KIND_INT, digits, eos=eos, max_tokens=4,
+                                 prefix=pre, max_batch_tokens=mbt)
+        assert out_n.tobytes() == out.tobytes(), mbt
     # the same with the restricted head (digits and EOS only)
     out_r, dbg_r = ctx.eval_rows(np.concatenate(rows), offs, KIND_INT, digits, eos=eos,
                                  max_tokens=4, prefix=pre, debug_logits=True, head_restricted=True)
