@@ -58,7 +58,7 @@ typedef struct lmop_prefix lmop_prefix; /* opaque; owned by its ctx */
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff, vocab, group_size;
   float rms_eps, rope_theta;
-  int32_t max_seq; /* longest prefix + suffix + generated tokens; 0 = 4096 */
+  int32_t max_seq; /* longest prefix + suffix + generated tokens; 0 = 4096, at most 2^20 */
 } lmop_config;
 
 /* Creates a ctx on HIP device `device` whose work runs on `hip_stream`
@@ -168,7 +168,8 @@ typedef struct {
 
 typedef struct {
   uint32_t flags;           /* LMOP_NO_DEDUP | LMOP_HEAD_RESTRICTED                       */
-  int32_t max_batch_tokens; /* suffix tokens per device batch; 0 = library default        */
+  int32_t max_batch_tokens; /* suffix tokens per device batch; 0 = library default (16384),
+                               larger values are capped at 2^21                           */
   float* debug_logits;      /* NULL or host fp32 [n_rows][max_steps][vocab]: the logits of
                                each step (max_steps = max_tokens for INT, else 1); steps a
                                row did not take are NaN                                   */

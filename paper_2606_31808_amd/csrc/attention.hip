@@ -50,6 +50,30 @@ LMOP_DEVICE int kswz(int key) {
 LMOP_DEVICE int vswz(int row) { return row & 7; }
 
 
+// max / sum with the lane 16 (32) apart: the gfx950 row-swap instructions
+// exchange 16-lane rows between two registers without going through LDS
+LMOP_DEVICE float vmax(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));  // inputs are never NaN
+  return r;
+}
+LMOP_DEVICE float max_x16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+LMOP_DEVICE float max_x32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+LMOP_DEVICE float sum_x16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+LMOP_DEVICE float sum_x32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float scale_log2) {
   constexpr int K_BYTES = KB * HD * 2;
@@ -120,6 +144,24 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
     }
   };
 
+  // Each load's address = a block base in scalar registers + a per-lane byte
+  // offset.  K offsets do not depend on the block; V^T offsets depend on the
+  // segment's capacity (row stride) only.
+  uint32_t koff[K_LOADS], vdim[V_LOADS], vchunk[V_LOADS];
+#pragma unroll
+  for (int i = 0; i < K_LOADS; ++i) {
+    const int q = wave + 4 * i;  // 1 KB = 1024 / (2*HD) keys
+    const int key = q * (512 / HD) + lane / KCH;
+    const int chunk = (lane % KCH) ^ kswz<HD>(key);
+    koff[i] = (uint32_t)(key * kvdim + h * HD + chunk * 8) * 2u;
+  }
+#pragma unroll
+  for (int i = 0; i < V_LOADS; ++i) {
+    const int q = wave + 4 * i;  // 8 dim rows of 128 bytes
+    const int dim = q * 8 + (lane >> 3);
+    vdim[i] = (uint32_t)dim;
+    vchunk[i] = (uint32_t)(((lane & 7) ^ vswz(dim)) * 16);
+  }
   auto issue = [&](int st, int b) {
     int s, kb;
     locate(b, s, kb);
@@ -129,22 +171,14 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
     const int sstart = s == 0 ? start_s[0] : s == 1 ? start_s[1] : start_s[2];
     char* sK = smem + st * STAGE;
     char* sV = sK + K_BYTES;
+    const f16* kblk = kbase + (size_t)(sstart + kb) * kvdim;
+    const f16* vblk = vbase + (size_t)h * HD * scap + sstart + kb;
+    const uint32_t vrow = (uint32_t)scap * 2u;  // bytes per V^T row
 #pragma unroll
-    for (int i = 0; i < K_LOADS; ++i) {
-      const int q = wave + 4 * i;                // 1 KB = 1024 / (2*HD) keys
-      const int key = q * (512 / HD) + lane / KCH;
-      const int chunk = (lane % KCH) ^ kswz<HD>(key);
-      const f16* src = kbase + (size_t)(sstart + kb + key) * kvdim + h * HD + chunk * 8;
-      g2l16(src, sK + q * 1024);
-    }
+    for (int i = 0; i < K_LOADS; ++i) g2l16_s(kblk, koff[i], sK + (wave + 4 * i) * 1024);
 #pragma unroll
-    for (int i = 0; i < V_LOADS; ++i) {
-      const int q = wave + 4 * i;  // 8 dim rows of 128 bytes
-      const int dim = q * 8 + (lane >> 3);
-      const int chunk = (lane & 7) ^ vswz(dim);
-      const f16* src = vbase + (size_t)(h * HD + dim) * scap + sstart + kb + chunk * 8;
-      g2l16(src, sV + q * 1024);
-    }
+    for (int i = 0; i < V_LOADS; ++i)
+      g2l16_s(vblk, __umul24(vdim[i], vrow) + vchunk[i], sV + (wave + 4 * i) * 1024);
   };
 
   // this lane's query vectors: v = tile*128 + wave*32 + 16*qs + c
@@ -220,21 +254,20 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
     for (int qs = 0; qs < 2; ++qs) {
       float mb = -INFINITY;
       if (need_mask) {
+        // key kb + 8g + j is visible iff j < lim - kb - 8g
+        const int lim = s < 2 ? seg_n : (seg_n < n_vis[qs] ? seg_n : n_vis[qs]);
+        const int dl = lim - kb - 8 * g;
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int kk = kb + 32 * (kt >> 1) + 8 * g + 4 * (kt & 1) + r;
-            const bool vis = kk < seg_n && (s < 2 || kk < n_vis[qs]);
-            st[qs][kt][r] = vis ? st[qs][kt][r] : -INFINITY;
-          }
+          for (int r = 0; r < 4; ++r)
+            st[qs][kt][r] = 32 * (kt >> 1) + 4 * (kt & 1) + r < dl ? st[qs][kt][r] : -INFINITY;
       }
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) mb = fmaxf(mb, st[qs][kt][r]);
-      mb = fmaxf(mb, shfl_xor(mb, 16));
-      mb = fmaxf(mb, shfl_xor(mb, 32));
+      mb = max_x32(max_x16(mb));
       // The reference maximum moves only where a score exceeds it by more than
       // 8 / c, so p = 2^(s*c - m*c) stays below 2^8 and the running output is
       // rescaled only on such (rare) blocks.
@@ -275,8 +308,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
 
 #pragma unroll
   for (int qs = 0; qs < 2; ++qs) {
-    float l_tot = l_run[qs] + shfl_xor(l_run[qs], 16);
-    l_tot += shfl_xor(l_tot, 32);
+    const float l_tot = sum_x32(sum_x16(l_run[qs]));
     if (qvalid[qs]) {
       const float inv = 1.0f / l_tot;
       f16* op = (f16*)p.out + (size_t)(row.q_start + tok[qs]) * p.ldo + hq[qs] * HD;
@@ -294,6 +326,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
 
 hipError_t launch_attention(hipStream_t s, const AttnArgs& a) {
   if (a.n_work == 0) return hipSuccess;
+  if (a.own_cap > kMaxStoreSlots) return hipErrorInvalidValue;
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)a.hd);
   dim3 grid(a.n_work, a.nkv);
   if (a.hd == 128)

@@ -107,6 +107,9 @@ struct AttnRow {
   int own_q0;                  // own index of the first query token
 };
 constexpr int ATTN_QTILE = 128;  // query vectors (token, head-in-group) per workgroup
+// Largest KV store (slots) the attention kernel reads: it forms V^T row
+// offsets with a 24-bit multiply (dim x 2*capacity bytes).
+constexpr int kMaxStoreSlots = 1 << 22;
 
 struct AttnArgs {
   const half_bits* q;  // [T][ldq], post-RoPE

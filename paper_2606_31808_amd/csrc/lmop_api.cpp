@@ -29,8 +29,13 @@ constexpr int kDefaultBatchTokens = 16384;
 constexpr int kMaxBatchRows = 2048;
 // own-KV bytes of one integer-decode group (also at most half the free memory)
 constexpr size_t kDecodeGroupBytes = size_t(24) << 30;
+// longest sequence, and largest token budget of one batch; both keep every
+// KV store within the attention kernel's kMaxStoreSlots
+constexpr int kMaxSeq = 1 << 20;
+constexpr int kMaxBatchBudget = 1 << 21;
 
 int round_up(int x, int m) { return (x + m - 1) / m * m; }
+int64_t round_up64(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 struct LayerW {
   float* attn_norm = nullptr;
@@ -296,6 +301,8 @@ lmop_status check_config(const lmop_config* cfg, lmop_ctx* c) {
       cfg->head_dim <= 0 || cfg->d_ff <= 0 || cfg->vocab <= 1 || !(cfg->rms_eps >= 0.f) ||
       !(cfg->rope_theta > 0.f) || cfg->max_seq < 0)
     return fail(c, LMOP_ERR_INVALID_ARG, "config has a non-positive dimension or parameter");
+  if (cfg->max_seq > kMaxSeq)
+    return fail(c, LMOP_ERR_UNSUPPORTED, "max_seq %d (at most %d)", cfg->max_seq, kMaxSeq);
   if (cfg->head_dim != 64 && cfg->head_dim != 128)
     return fail(c, LMOP_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", cfg->head_dim);
   if (cfg->n_heads % cfg->n_kv_heads != 0)
@@ -987,14 +994,18 @@ static lmop_status make_prefixes(lmop_ctx* ctx, const lmop_prefix* parent, const
   const lmop_config& cf = ctx->cfg;
   const int start = prefix_total(parent);
   std::vector<int> len(n), slot0(n);
-  int used = 0, need = 0;
+  int64_t used = 0, need = 0;
   for (int i = 0; i < n; ++i) {
     len[i] = (int)(offsets[i + 1] - offsets[i]);
-    slot0[i] = used;
-    need = std::max(need, used + round_up(len[i], 64));
-    used = round_up(used + len[i], 8);
+    slot0[i] = (int)std::min<int64_t>(used, kMaxStoreSlots);
+    need = std::max<int64_t>(need, used + round_up(len[i], 64));
+    used = round_up64(used + len[i], 8);
   }
-  const int cap = round_up(need, 64);
+  if (need > kMaxStoreSlots)
+    return fail(ctx, LMOP_ERR_UNSUPPORTED,
+                "%d prefixes of %lld tokens in all need more than %d KV slots: use several calls",
+                n, (long long)offsets[n], kMaxStoreSlots);
+  const int cap = round_up((int)need, 64);
   KvStore* store = nullptr;
   if (!ctx->host_only) {
     store = new KvStore();
@@ -1233,6 +1244,7 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
 
   const bool restricted = (flags & LMOP_HEAD_RESTRICTED) != 0;
   int budget = opts && opts->max_batch_tokens > 0 ? opts->max_batch_tokens : kDefaultBatchTokens;
+  budget = std::min(budget, kMaxBatchBudget);
   float* dbg = opts ? opts->debug_logits : nullptr;
   const int V = cf.vocab;
 
@@ -1316,7 +1328,7 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
         slots = round_up(slots + (int)(offsets[uniq[u] + 1] - offsets[uniq[u]]) + dec, 8);
       const size_t r = batches[b1].second - batches[b1].first;
       if (b1 > b && (dec == 0 || (size_t)own_store_cap(used + slots) * slot_bytes > group_bytes ||
-                     rows + r > (size_t)budget))
+                     own_store_cap(used + slots) > kMaxStoreSlots || rows + r > (size_t)budget))
         break;
       base_of[b1] = used;
       group_of[b1] = (int)group_cap.size();

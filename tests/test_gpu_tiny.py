@@ -308,6 +308,38 @@ def test_tiny_edge_cases(tiny, L):
     ctx.release_prefix(pre)
 
 
+def test_tiny_row_at_max_seq(tiny, L):
+    """A row whose last decode step sits at position max_seq - 1 (the last
+    RoPE table entry and KV slot), under a batch budget smaller than the row."""
+    w, orc, _ = tiny
+    V, max_seq = TINY.vocab, 600
+    ctx = L.Context(TINY, device=0, max_seq=max_seq)
+    ctx.load_weights(w)
+    rng = np.random.default_rng(12)
+    prefix = rng.integers(0, V, size=130).astype(np.int32)
+    pre = ctx.set_prefix(prefix)
+    digits = rng.choice(V, 10, replace=False).astype(np.int32)
+    eos = int(next(t for t in range(V) if t not in digits))
+    rows = [rng.integers(0, V, size=n).astype(np.int32) for n in (max_seq - 130 - 3, 5)]
+    toks = np.concatenate(rows)
+    offs = np.concatenate([[0], np.cumsum([len(r) for r in rows])])
+    _log("max_seq row: eval")
+    out, dbg = ctx.eval_rows(toks, offs, KIND_INT, digits, eos=eos, max_tokens=4, prefix=pre,
+                             debug_logits=True, max_batch_tokens=64)
+    ref = orc.eval_rows(prefix, rows, KIND_INT, digits, eos=eos, max_tokens=4, keep_logits=True)
+    forced = orc.eval_rows(prefix, rows, KIND_INT, digits, eos=eos, max_tokens=4,
+                           forced=[out["tokens"][r][: out["n_tokens"][r]] for r in range(2)],
+                           keep_logits=True)
+    _log("max_seq row", compare(ref, out, dbg, "max_seq row", orc_forced=forced))
+    assert_typed(out, KIND_INT, 10, digits, eos, 4)
+    # one token more does not fit
+    long_row = np.concatenate([rows[0], [1]]).astype(np.int32)
+    with pytest.raises(L.LmopError):
+        ctx.eval_rows(long_row, [0, len(long_row)], KIND_INT, digits, eos=eos, max_tokens=4,
+                      prefix=pre)
+    ctx.release_prefix(pre)
+
+
 def test_tiny_dedup_and_batch_invariance(tiny, L):
     w, orc, ctx = tiny
     wl = make_workload("filter_tiny")

@@ -47,6 +47,8 @@ def test_config_validation():
                            ("n_kv_heads", 3, L.LMOP_ERR_UNSUPPORTED),
                            ("d_model", 200, L.LMOP_ERR_UNSUPPORTED),
                            ("group_size", 64, L.LMOP_ERR_UNSUPPORTED),
+                           ("max_seq", (1 << 20) + 1, L.LMOP_ERR_UNSUPPORTED),
+                           ("max_seq", -1, L.LMOP_ERR_INVALID_ARG),
                            ("vocab", 0, L.LMOP_ERR_INVALID_ARG),
                            ("d_ff", -1, L.LMOP_ERR_INVALID_ARG)]:
         cfg = L.lmop_config.from_buffer_copy(base)
