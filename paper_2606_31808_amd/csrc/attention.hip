@@ -99,50 +99,23 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
   int t_last = (wk.y * QT + QT - 1) / G;
   if (t_last > row.n_q - 1) t_last = row.n_q - 1;
   // segment s: keys [start, start + n) of a store with capacity cap (K at
-  // kb_s, V^T at vb_s).  Kept as separate scalars and chosen with selects: an
+  // kb_s, V^T at vb_s).  Separate named scalars, chosen with selects: an
   // array indexed by the runtime segment number would live in scratch memory.
-  const f16* kb_s[3];
-  const f16* vb_s[3];
-  int cap_s[3], start_s[3], n_s[3];
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    const int cap = row.seg_cap[s];
-    const f16* base = (const f16*)row.seg_kv[s] + (size_t)p.layer * 2 * cap * kvdim;
-    kb_s[s] = base;
-    vb_s[s] = base + (size_t)cap * kvdim;
-    cap_s[s] = cap;
-    start_s[s] = row.seg_start[s];
-    n_s[s] = row.seg_n[s];
-  }
-  {
-    const f16* base = (const f16*)p.own_kv + (size_t)p.layer * 2 * p.own_cap * kvdim;
-    kb_s[2] = base;
-    vb_s[2] = base + (size_t)p.own_cap * kvdim;
-    cap_s[2] = p.own_cap;
-    start_s[2] = row.own_slot;
-    n_s[2] = row.own_q0 + t_last + 1;
-  }
+  const int cap0 = row.seg_cap[0], cap1 = row.seg_cap[1], cap2 = p.own_cap;
+  const f16* kb0 = (const f16*)row.seg_kv[0] + (size_t)p.layer * 2 * cap0 * kvdim;
+  const f16* kb1 = (const f16*)row.seg_kv[1] + (size_t)p.layer * 2 * cap1 * kvdim;
+  const f16* kb2 = (const f16*)p.own_kv + (size_t)p.layer * 2 * cap2 * kvdim;
+  const f16* vb0 = kb0 + (size_t)cap0 * kvdim;
+  const f16* vb1 = kb1 + (size_t)cap1 * kvdim;
+  const f16* vb2 = kb2 + (size_t)cap2 * kvdim;
+  const int start0 = row.seg_start[0], start1 = row.seg_start[1], start2 = row.own_slot;
+  const int n0 = row.seg_n[0], n1 = row.seg_n[1], n2 = row.own_q0 + t_last + 1;
   // own keys visible to every valid query of the workgroup (first token's count)
   int t_first = (wk.y * QT) / G;
   const int vis_min = row.own_q0 + t_first + 1;
-  const int nb0 = (n_s[0] + KB - 1) / KB, nb1 = (n_s[1] + KB - 1) / KB;
-  const int nb2 = (n_s[2] + KB - 1) / KB;
+  const int nb0 = (n0 + KB - 1) / KB, nb1 = (n1 + KB - 1) / KB;
+  const int nb2 = (n2 + KB - 1) / KB;
   const int NB = nb0 + nb1 + nb2;
-  const int P = row.seg_n[0] + row.seg_n[1];
-
-  // block b -> (segment, first key of the block within the segment)
-  auto locate = [&](int b, int& s, int& kb) {
-    if (b < nb0) {
-      s = 0;
-      kb = b * KB;
-    } else if (b < nb0 + nb1) {
-      s = 1;
-      kb = (b - nb0) * KB;
-    } else {
-      s = 2;
-      kb = (b - nb0 - nb1) * KB;
-    }
-  };
 
   // Each load's address = a block base in scalar registers + a per-lane byte
   // offset.  K offsets do not depend on the block; V^T offsets depend on the
@@ -162,23 +135,47 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
     vdim[i] = (uint32_t)dim;
     vchunk[i] = (uint32_t)(((lane & 7) ^ vswz(dim)) * 16);
   }
-  auto issue = [&](int st, int b) {
-    int s, kb;
-    locate(b, s, kb);
-    const f16* kbase = s == 0 ? kb_s[0] : s == 1 ? kb_s[1] : kb_s[2];
-    const f16* vbase = s == 0 ? vb_s[0] : s == 1 ? vb_s[1] : vb_s[2];
-    const int scap = s == 0 ? cap_s[0] : s == 1 ? cap_s[1] : cap_s[2];
-    const int sstart = s == 0 ? start_s[0] : s == 1 ? start_s[1] : start_s[2];
-    char* sK = smem + st * STAGE;
-    char* sV = sK + K_BYTES;
-    const f16* kblk = kbase + (size_t)(sstart + kb) * kvdim;
-    const f16* vblk = vbase + (size_t)h * HD * scap + sstart + kb;
-    const uint32_t vrow = (uint32_t)scap * 2u;  // bytes per V^T row
+  // The non-empty segments in walk order, as up to three slots (a, b, c)
+  // that shift down when a segment is used up: no runtime segment index
+  // (it would turn the selects into a scratch-memory table).  Each slot:
+  // first block's K and V^T bases (bytes), V^T row length (bytes), keys,
+  // whether it is the own segment.
+  struct Seg {
+    const char* k;
+    const char* v;
+    uint32_t vrow;
+    int n;
+    bool own;
+  };
+  auto make_seg = [&](const f16* kb, const f16* vb, int cap, int start, int n, bool own) {
+    return Seg{(const char*)(kb + (size_t)start * kvdim),
+               (const char*)(vb + (size_t)h * HD * cap + start), (uint32_t)cap * 2u, n, own};
+  };
+  const Seg s0 = make_seg(kb0, vb0, cap0, start0, n0, false);
+  const Seg s1 = make_seg(kb1, vb1, cap1, start1, n1, false);
+  const Seg s2 = make_seg(kb2, vb2, cap2, start2, n2, true);  // never empty
+  const Seg none = Seg{nullptr, nullptr, 0u, 0, true};
+  Seg la = n0 > 0 ? s0 : n1 > 0 ? s1 : s2;
+  Seg lb = n0 > 0 ? (n1 > 0 ? s1 : s2) : n1 > 0 ? s2 : none;
+  Seg lc = n0 > 0 && n1 > 0 ? s2 : none;
+  // the loads' walk: slot la holds the next block to load, lkb its first key
+  int lkb = 0;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_ptr_t)smem + (uint32_t)wave * 1024u;
+  auto issue = [&](int st) {
+    const uint32_t mk = lds0 + (uint32_t)(st * STAGE);
 #pragma unroll
-    for (int i = 0; i < K_LOADS; ++i) g2l16_s(kblk, koff[i], sK + (wave + 4 * i) * 1024);
+    for (int i = 0; i < K_LOADS; ++i) g2l16_m0(la.k, koff[i], mk + 4096u * i);
 #pragma unroll
     for (int i = 0; i < V_LOADS; ++i)
-      g2l16_s(vblk, __umul24(vdim[i], vrow) + vchunk[i], sV + (wave + 4 * i) * 1024);
+      g2l16_m0(la.v, __umul24(vdim[i], la.vrow) + vchunk[i], mk + K_BYTES + 4096u * i);
+    lkb += KB;
+    la.k += (size_t)KB * kvdim * 2;
+    la.v += KB * 2;
+    if (lkb >= la.n) {
+      lkb = 0;
+      la = lb;
+      lb = lc;
+    }
   };
 
   // this lane's query vectors: v = tile*128 + wave*32 + 16*qs + c
@@ -214,19 +211,32 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
 
   // a wave whose query vectors all lie past the row's end only helps load
   const bool wave_active = wk.y * QT + wave * QW < row.n_q * G;
-  issue(0, 0);
+  // the computation's walk over the same blocks: keys and kind of the
+  // current segment and of the ones after it, ckb the block's first key
+  int ca_n = la.n, cb_n = lb.n, cc_n = lc.n;
+  bool ca_own = la.own, cb_own = lb.own, cc_own = lc.own;
+  int ckb = 0;
+  issue(0);
   for (int b = 0; b < NB; ++b) {
     // block b is in LDS for every wave, and every wave is done with block
     // b-1, whose stage the next issue refills
     wait_vmcnt<0>();
     barrier();
-    if (b + 1 < NB) issue((b + 1) & 1, b + 1);
+    if (b + 1 < NB) issue((b + 1) & 1);
+    const int seg_n = ca_n;
+    const int kb_cur = ckb;
+    const bool own_cur = ca_own;
+    ckb += KB;
+    if (ckb >= ca_n) {
+      ckb = 0;
+      ca_n = cb_n;
+      ca_own = cb_own;
+      cb_n = cc_n;
+      cb_own = cc_own;
+    }
     if (!wave_active) continue;
-    int s, kb;
-    locate(b, s, kb);
     const char* sK = smem + (b & 1) * STAGE;
     const char* sV = sK + K_BYTES;
-    const int seg_n = s == 0 ? n_s[0] : s == 1 ? n_s[1] : n_s[2];
 
     // S^T tiles kt = 2*kc + hf: register r of lane group g holds key
     // kb + 32*kc + 8g + 4hf + r, query (qs, c)
@@ -248,15 +258,15 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
     // online softmax; scores stay unscaled, p = 2^(s*c - m*c) with c = log2(e)/sqrt(hd).
     // Blocks whose every key is visible to every query of the workgroup skip
     // the mask.
-    const bool need_mask = kb + KB > seg_n || (s == 2 && kb + KB > vis_min);
+    const bool need_mask = kb_cur + KB > seg_n || (own_cur && kb_cur + KB > vis_min);
     f16x8 pb[2][2];
 #pragma unroll
     for (int qs = 0; qs < 2; ++qs) {
       float mb = -INFINITY;
       if (need_mask) {
         // key kb + 8g + j is visible iff j < lim - kb - 8g
-        const int lim = s < 2 ? seg_n : (seg_n < n_vis[qs] ? seg_n : n_vis[qs]);
-        const int dl = lim - kb - 8 * g;
+        const int lim = !own_cur ? seg_n : (seg_n < n_vis[qs] ? seg_n : n_vis[qs]);
+        const int dl = lim - kb_cur - 8 * g;
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll

@@ -27,13 +27,12 @@ LMOP_DEVICE void g2l16(const void* gaddr, void* lds_base) {
 }
 
 // the same with the address split into a wave-uniform base (scalar
-// registers) and a per-lane 32-bit byte offset
-LMOP_DEVICE void g2l16_s(const void* sbase, uint32_t voff, void* lds_base) {
-  const uint32_t m0 =
-      __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_ptr_t)lds_base);
+// registers) plus a per-lane 32-bit byte offset, and the LDS destination
+// given as a wave-uniform LDS address
+LMOP_DEVICE void g2l16_m0(const void* sbase, uint32_t voff, uint32_t lds_addr) {
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
                :
-               : "v"(voff), "s"(sbase), "s"(m0)
+               : "v"(voff), "s"(sbase), "s"(lds_addr)
                : "memory");
 }
 
