@@ -1010,6 +1010,8 @@ static lmop_status make_prefixes(lmop_ctx* ctx, const lmop_prefix* parent, const
   if (!ctx->host_only) {
     store = new KvStore();
     auto fail_free = [&](lmop_status st) {
+      // work already queued may still write the store
+      (void)hipStreamSynchronize(ctx->stream);
       if (store->kv) (void)hipFree(store->kv);
       if (store->hidden) (void)hipFree(store->hidden);
       delete store;
