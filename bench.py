@@ -127,6 +127,62 @@ def pmc_summary(root):
     print(json.dumps(out))
 
 
+def mfma_summary(root):
+    """MFMA utilisation of the timed step's kernels from one rocprofv3 --pmc
+    run of the bench (SQ_VALU_MFMA_BUSY_CYCLES, GRBM_GUI_ACTIVE; under
+    root/pmc_mfma, the bench line in root/pmc_mfma.log).  Utilisation = MFMA
+    busy cycles summed over all SIMDs / (GPU busy cycles of one XCD x 1024
+    SIMDs); GRBM_GUI_ACTIVE comes summed over the 8 XCDs."""
+    import csv
+    import glob
+    xcds, simds = 8, 1024
+    rows = []
+    for fn in glob.glob(os.path.join(root, "pmc_mfma", "*counter_collection.csv")):
+        rows.extend(csv.DictReader(open(fn)))
+    n = _bench_line(os.path.join(root, "pmc_mfma.log"))["roofline"]["launches"]
+    by_id = {}
+    for r in rows:
+        d = by_id.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"]})
+        d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    gemm_ids = sorted(i for i, d in by_id.items() if _is_w4_gemm(d["name"]))[-n:]
+    first = gemm_ids[0]
+
+    def family(name):
+        if _is_w4_gemm(name):
+            epi = name.split("gemm_kernel<")[1].split(",")[2].strip()
+            return {"1": "W4A16 GEMM, residual add (o, down)", "2": "W4A16 GEMM, SwiGLU (gate/up)",
+                    "4": "W4A16 GEMM, QKV + RoPE (qkv)", "0": "W4A16 GEMM, fp16 store"}.get(epi, epi)
+        if "gemm_kernel<" in name:
+            return "LM head GEMM"
+        if "attn_kernel" in name:
+            return "attention"
+        return None
+
+    agg = {}
+    for i, d in by_id.items():
+        if i < first:
+            continue
+        fam = family(d["name"])
+        if fam is None:
+            continue
+        a = agg.setdefault(fam, [0, 0.0, 0.0, 0.0])
+        a[0] += 1
+        a[1] += d.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+        a[2] += d.get("GRBM_GUI_ACTIVE", 0.0) / xcds * simds
+        a[3] += d.get("SQ_INSTS_MFMA", 0.0)
+    print(f"timed step: {n} W4A16 GEMM dispatches (bench: {n})")
+    print("| kernel family | dispatches | MFMA instructions | MFMA busy (of all SIMD cycles) |")
+    print("|---|---|---|---|")
+    tot = [0, 0.0, 0.0, 0.0]
+    for fam in sorted(agg):
+        a = agg[fam]
+        print(f"| {fam} | {a[0]} | {a[3]:.4g} | {100.0 * a[1] / a[2]:.1f}% |")
+        if fam.startswith("W4A16"):
+            for k in range(4):
+                tot[k] += a[k]
+    print(f"| all W4A16 GEMMs | {tot[0]} | {tot[3]:.4g} | {100.0 * tot[1] / tot[2]:.1f}% |")
+
+
 def trace_summary(root):
     """Per-kernel durations of the timed W4A16 GEMM launches from a
     `rocprofv3 --kernel-trace` run of the default bench command (trace under
@@ -219,6 +275,8 @@ def main():
                     help="only run one plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--pmc-summary", metavar="DIR",
                     help="summarise the rocprofv3 --pmc runs under DIR and exit")
+    ap.add_argument("--mfma-summary", metavar="DIR",
+                    help="summarise an SQ_VALU_MFMA_BUSY_CYCLES pass under DIR/pmc_mfma and exit")
     ap.add_argument("--trace-summary", metavar="DIR",
                     help="summarise the rocprofv3 --kernel-trace run under DIR and exit")
     args = ap.parse_args()
@@ -227,6 +285,9 @@ def main():
         return
     if args.trace_summary:
         trace_summary(args.trace_summary)
+        return
+    if args.mfma_summary:
+        mfma_summary(args.mfma_summary)
         return
     if args.calibrate_copy:
         import torch
