@@ -31,6 +31,9 @@ decode follow the readings listed in the design notes: ties go to the first
 allowed token; `logprob` is the log-softmax over the step's allowed set and
 `logprob_full` over the whole vocabulary; an integer is a digit string with
 no EOS at the first step and at most `max_tokens` tokens including EOS.
+Multi-token outputs (option strings, other regular types) follow a token
+automaton: each step allows the current state's edge tokens (and EOS in an
+accepting state), as listed in automaton_steps.
 
 Evaluation with a shared prefix computes the prefix's keys and values once
 and lets each row attend to them.  Causal attention makes that identical to
@@ -45,7 +48,7 @@ from typing import List, Optional, Sequence
 
 import numpy as np
 
-KIND_BOOL, KIND_ENUM, KIND_INT = 0, 1, 2
+KIND_BOOL, KIND_ENUM, KIND_INT, KIND_AUTOMATON = 0, 1, 2, 3
 GROUP = 32
 
 # two's-complement value of every nibble 0..15
@@ -168,6 +171,37 @@ def constrained_pick(z: np.ndarray, allowed: Sequence[int]):
     else:
         margin = float("inf")
     return i, lp, lpf, margin
+
+
+def automaton_steps(aut, eos: int):
+    """The constrained-decoding grammar of a token automaton (multi-token
+    options and other regular output types, Sec. 2.3 "Constrained Decoding").
+
+    `aut` has n_states, edge_offset [n_states + 1], edge_token, edge_next and
+    accepting [n_states]; state 0 is the start.  Returns, per state, the
+    allowed tokens of a step in that state and the state each one leads to
+    (None for EOS).  The allowed tokens are the state's edge tokens ordered by
+    where each token first appears in edge_token (this order breaks ties),
+    followed by EOS when the state is accepting and an EOS token is given.
+    """
+    off = np.asarray(aut.edge_offset)
+    tok = np.asarray(aut.edge_token)
+    nxt = np.asarray(aut.edge_next)
+    acc = np.asarray(aut.accepting)
+    first = {}
+    for t in tok.tolist():
+        first.setdefault(t, len(first))
+    out = []
+    for st in range(int(aut.n_states)):
+        edges = sorted(zip(tok[off[st]:off[st + 1]].tolist(), nxt[off[st]:off[st + 1]].tolist()),
+                       key=lambda e: first[e[0]])
+        allowed = [t for t, _ in edges]
+        to = [int(n) for _, n in edges]
+        if acc[st] and eos >= 0:
+            allowed.append(int(eos))
+            to.append(None)
+        out.append((np.array(allowed, dtype=np.int64), to))
+    return out
 
 
 def _np(t):
@@ -327,12 +361,21 @@ class OracleLM:
         margin (smallest top-two allowed gap over the row's steps) and, with
         keep_logits, logits[r] = list of per-step logit vectors.
 
+        `kind` KIND_AUTOMATON takes a token automaton as `allowed` (see
+        automaton_steps); the value is then the final state.
+
         Sequences are prefix ++ children[row_child[r]] ++ suffixes[r].  The
         prefix (and each child) is run once and its keys/values are reused by
         every row below it.  `forced[r]`, if given, replaces the chosen token
         of each step (teacher forcing) while logits/picks are still reported.
         """
-        allowed = np.asarray(allowed, dtype=np.int64)
+        grammar = None
+        if kind == KIND_AUTOMATON:
+            grammar = automaton_steps(allowed, eos)
+            edge_off = np.asarray(allowed.edge_offset)
+            accepting = np.asarray(allowed.accepting)
+        else:
+            allowed = np.asarray(allowed, dtype=np.int64)
         R = len(suffixes)
         root = _Node(np.asarray(prefix), None) if prefix is not None and len(prefix) else None
         kids = []
@@ -363,7 +406,8 @@ class OracleLM:
         tails = list(rows)
         live = list(range(R))
         digits: List[List[int]] = [[] for _ in range(R)]
-        steps = 1 if kind != KIND_INT else max_tokens
+        state = np.zeros(R, dtype=np.int64)  # automaton state of each row
+        steps = 1 if kind not in (KIND_INT, KIND_AUTOMATON) else max_tokens
         for step in range(steps):
             if not live:
                 break
@@ -371,11 +415,13 @@ class OracleLM:
             z = self.logits(xs)
             if kind == KIND_INT and step > 0:
                 step_allowed = np.concatenate([allowed, [eos]])
-            else:
+            elif kind != KIND_AUTOMATON:
                 step_allowed = allowed
             next_live = []
             for i, r in enumerate(live):
                 zi = z[i]
+                if kind == KIND_AUTOMATON:
+                    step_allowed, step_to = grammar[int(state[r])]
                 if keep_logits:
                     logits_out[r].append(zi.copy())
                 ci, a, b, m = constrained_pick(zi, step_allowed)
@@ -397,9 +443,23 @@ class OracleLM:
                     digits[r].append(ci)
                     if ntok[r] < max_tokens:
                         next_live.append(r)
+                elif kind == KIND_AUTOMATON:
+                    # the output ends with EOS, in an accepting state without
+                    # edges, or after max_tokens; the value is the final state,
+                    # -1 if that state is not accepting
+                    if step_to[ci] is None:
+                        value[r] = state[r]
+                        continue
+                    state[r] = step_to[ci]
+                    s_new = int(state[r])
+                    ends = edge_off[s_new + 1] == edge_off[s_new] or ntok[r] >= max_tokens
+                    if ends:
+                        value[r] = s_new if accepting[s_new] else -1
+                    else:
+                        next_live.append(r)
                 else:
                     value[r] = ci
-            if kind == KIND_INT and next_live:
+            if kind in (KIND_INT, KIND_AUTOMATON) and next_live:
                 new = [_Node(np.array([toks[r, ntok[r] - 1]]), tails[r]) for r in next_live]
                 for r, nd in zip(next_live, new):
                     tails[r] = nd
@@ -422,5 +482,6 @@ class OracleLM:
         idx = range(wl.n_rows) if rows is None else rows
         sufs = [wl.suffix(int(r)) for r in idx]
         rc = None if wl.row_child is None else [int(wl.row_child[int(r)]) for r in idx]
-        return self.eval_rows(wl.prefix, sufs, wl.kind, wl.allowed, eos=wl.eos,
+        allowed = wl.automaton if getattr(wl, "automaton", None) is not None else wl.allowed
+        return self.eval_rows(wl.prefix, sufs, wl.kind, allowed, eos=wl.eos,
                               max_tokens=wl.max_tokens, children=wl.children, row_child=rc, **kw)

@@ -16,4 +16,8 @@ from .workloads import (  # noqa: F401
     make_workload,
     quantize_int4_g32,
     WORKLOADS,
+    Automaton,
+    option_trie,
+    automaton_of_options,
+    KIND_AUTOMATON,
 )

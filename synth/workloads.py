@@ -164,7 +164,68 @@ def make_weights(shape: ModelShape, seed: int = 1234, device="cpu", std: float =
 # Row tables
 # --------------------------------------------------------------------------
 
-KIND_BOOL, KIND_ENUM, KIND_INT = 0, 1, 2
+KIND_BOOL, KIND_ENUM, KIND_INT, KIND_AUTOMATON = 0, 1, 2, 3
+
+
+@dataclasses.dataclass
+class Automaton:
+    """A token automaton (data only): state 0 starts; state s has the edges
+    edge_token[edge_offset[s]:edge_offset[s+1]] -> edge_next[...];
+    accepting[s] != 0 lets an output end in s."""
+    n_states: int
+    edge_offset: np.ndarray   # int32 [n_states + 1]
+    edge_token: np.ndarray    # int32 [n_edges]
+    edge_next: np.ndarray     # int32 [n_edges]
+    accepting: np.ndarray     # uint8 [n_states]
+
+
+def option_trie(options) -> "tuple[Automaton, np.ndarray]":
+    """The prefix tree of token-string options: one state per distinct option
+    prefix (state 0 = empty), edges in order of first use, the state of each
+    whole option accepting.  Returns the automaton and, per option, its
+    final state."""
+    children = [dict()]
+    final = []
+    for opt in options:
+        st = 0
+        for t in (int(x) for x in opt):
+            nxt = children[st].get(t)
+            if nxt is None:
+                nxt = len(children)
+                children[st][t] = nxt
+                children.append(dict())
+            st = nxt
+        final.append(st)
+    n = len(children)
+    off = np.zeros(n + 1, dtype=np.int32)
+    tok, nx = [], []
+    for s in range(n):
+        for t, c in children[s].items():
+            tok.append(t)
+            nx.append(c)
+        off[s + 1] = len(tok)
+    acc = np.zeros(n, dtype=np.uint8)
+    acc[final] = 1
+    aut = Automaton(n, off, np.array(tok, dtype=np.int32), np.array(nx, dtype=np.int32), acc)
+    return aut, np.array(final, dtype=np.int64)
+
+
+def automaton_of_options(n_options: int, V: int, rng, max_len: int = 3, n_heads: int = 8):
+    """Options of 1..max_len tokens whose first tokens come from a pool of
+    n_heads ids (so the options share prefixes), no option a prefix of
+    another: a synthetic multi-token option set and its trie."""
+    heads = rng.choice(V, size=n_heads, replace=False)
+    opts, seen = [], set()
+    while len(opts) < n_options:
+        n = int(rng.integers(1, max_len + 1))
+        o = tuple([int(heads[rng.integers(0, n_heads)])] +
+                  [int(x) for x in rng.integers(0, V, size=n - 1)])
+        clash = any(o == q[:len(o)] or q == o[:len(q)] for q in seen)
+        if not clash:
+            seen.add(o)
+            opts.append(np.array(o, dtype=np.int32))
+    aut, final = option_trie(opts)
+    return opts, aut, final
 
 
 @dataclasses.dataclass
@@ -185,6 +246,8 @@ class Workload:
     max_tokens: int = 1
     children: Optional[List[np.ndarray]] = None   # second-level prefixes (joins)
     row_child: Optional[np.ndarray] = None         # int32 [n_rows]
+    automaton: Optional[Automaton] = None          # KIND_AUTOMATON: the output grammar
+    options: Optional[List[np.ndarray]] = None     # its option strings, if it is a trie
 
     @property
     def n_rows(self) -> int:
@@ -238,6 +301,8 @@ def make_workload(name: str, seed: int = 7, n_rows: Optional[int] = None) -> Wor
                   suffixes of U{24..64} tokens; integer output over 10 digits + EOS, <= 4 tokens
     join_8b       8B shape, instruction 320, 200 left x 200 right values of U{8..32} tokens,
                   all 40,000 pairs left-major; bool; one child prefix per left value
+    options_tiny  as filter_tiny, output one of 24 options of 1..3 tokens (a token trie)
+    options_8b    as filter_8b, output one of 24 options of 1..3 tokens (a token trie)
     `n_rows` truncates the table to its first rows (same draws otherwise).
     """
     cfg = WORKLOADS[name]
@@ -255,6 +320,11 @@ def make_workload(name: str, seed: int = 7, n_rows: Optional[int] = None) -> Wor
                 eos = e
                 break
     children = row_child = None
+    automaton = options = None
+    if cfg["kind"] == KIND_AUTOMATON:
+        options, automaton, _ = automaton_of_options(cfg["n_allowed"], V, rng,
+                                                     max_len=cfg["max_tokens"])
+        allowed = np.zeros(0, dtype=np.int32)
     if name == "map_int_8b":
         n_distinct, n_total = 5000, 20000
         lens = rng.integers(24, 65, size=n_distinct)
@@ -287,7 +357,8 @@ def make_workload(name: str, seed: int = 7, n_rows: Optional[int] = None) -> Wor
     toks, offs = _csr(parts)
     return Workload(name=name, shape=shape, prefix=prefix, tokens=toks, offsets=offs,
                     kind=cfg["kind"], allowed=allowed, eos=eos, max_tokens=cfg["max_tokens"],
-                    children=children, row_child=row_child)
+                    children=children, row_child=row_child, automaton=automaton,
+                    options=options)
 
 
 WORKLOADS = {
@@ -301,4 +372,8 @@ WORKLOADS = {
                        kind=KIND_INT, n_allowed=10, max_tokens=4),
     "join_8b": dict(id=5, shape="8b", rows=40000, prefix=320, len=None,
                     kind=KIND_BOOL, n_allowed=2, max_tokens=1),
+    "options_tiny": dict(id=6, shape="tiny", rows=64, prefix=96, len=("uniform", 16, 48),
+                         kind=KIND_AUTOMATON, n_allowed=24, max_tokens=3),
+    "options_8b": dict(id=7, shape="8b", rows=10000, prefix=512, len=("lognormal", 60, 8, 512),
+                       kind=KIND_AUTOMATON, n_allowed=24, max_tokens=3),
 }

@@ -12,7 +12,9 @@ import torch
 
 from oracle import (KIND_BOOL, KIND_ENUM, KIND_INT, OracleLM, attention, constrained_pick,
                     decode_nibbles, dequant, rms_norm, rope, silu)
-from synth import SHAPES, ModelShape, make_weights, make_workload, quantize_int4_g32
+from oracle.lmop_oracle import KIND_AUTOMATON, automaton_steps
+from synth import (SHAPES, Automaton, ModelShape, make_weights, make_workload, option_trie,
+                   quantize_int4_g32)
 
 GOLD = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -335,6 +337,136 @@ def test_int_decode_matches_full_recompute():
         assert math.isclose(res["logprob"][r], lp, abs_tol=1e-12)
         assert math.isclose(res["logprob_full"][r], lpf, abs_tol=1e-12)
     assert n_eos >= 1 and n_full >= 1
+
+
+def _star(tokens):
+    """ENUM as a token automaton: state 0 -> one leaf per option."""
+    n = len(tokens)
+    off = np.array([0] + [n] * (n + 1), dtype=np.int32)
+    return Automaton(n + 1, off, np.asarray(tokens, dtype=np.int32),
+                     np.arange(1, n + 1, dtype=np.int32),
+                     np.array([0] + [1] * n, dtype=np.uint8))
+
+
+def _int_automaton(digits, max_digits=4):
+    """INT as a token automaton: state k = k digits so far."""
+    n = max_digits + 1
+    off = np.array([10 * min(s, max_digits) for s in range(n + 1)], dtype=np.int32)
+    tok = np.tile(np.asarray(digits, dtype=np.int32), max_digits)
+    nxt = np.repeat(np.arange(1, max_digits + 1, dtype=np.int32), 10)
+    acc = np.array([0] + [1] * max_digits, dtype=np.uint8)
+    return Automaton(n, off, tok, nxt, acc)
+
+
+def test_automaton_steps_hand_example():
+    # state 0: 7 -> 1, 5 -> 2; state 1 (accepting): 5 -> 2, 9 -> 3; 2, 3 accepting leaves
+    aut = Automaton(4, np.array([0, 2, 4, 4, 4], np.int32), np.array([7, 5, 9, 5], np.int32),
+                    np.array([1, 2, 3, 2], np.int32), np.array([0, 1, 1, 1], np.uint8))
+    g = automaton_steps(aut, eos=42)
+    assert g[0][0].tolist() == [7, 5] and g[0][1] == [1, 2]
+    # token order is first appearance in the edge list (7, 5, 9), then EOS
+    assert g[1][0].tolist() == [5, 9, 42] and g[1][1] == [2, 3, None]
+    assert g[2][0].tolist() == [42] and g[3][1] == [None]
+    assert [a.tolist() for a, _ in automaton_steps(aut, eos=-1)][1] == [5, 9]
+
+
+def test_option_trie_hand_example():
+    aut, final = option_trie([np.array([4, 8]), np.array([4, 9, 1]), np.array([6])])
+    # states: 0, [4]=1, [4,8]=2, [4,9]=3, [4,9,1]=4, [6]=5
+    assert aut.n_states == 6
+    assert aut.edge_offset.tolist() == [0, 2, 4, 4, 5, 5, 5]
+    assert aut.edge_token.tolist() == [4, 6, 8, 9, 1]
+    assert aut.edge_next.tolist() == [1, 5, 2, 3, 4]
+    assert aut.accepting.tolist() == [0, 0, 1, 0, 1, 1]
+    assert final.tolist() == [2, 4, 5]
+
+
+def test_automaton_star_equals_enum(micro):
+    _, orc = micro
+    rng = np.random.default_rng(21)
+    prefix = rng.integers(0, MICRO.vocab, size=7)
+    rows = _rand_rows(rng, 9, 1, 6, MICRO.vocab)
+    opts = np.array([30, 5, 61, 12])
+    e = orc.eval_rows(prefix, rows, KIND_ENUM, opts)
+    a = orc.eval_rows(prefix, rows, KIND_AUTOMATON, _star(opts), max_tokens=3)
+    assert np.array_equal(a["value"], e["value"] + 1)
+    for k in ("logprob", "logprob_full", "n_tokens", "tokens", "margin"):
+        assert np.array_equal(a[k], e[k]), k
+
+
+def test_automaton_int_grammar_equals_int():
+    w = make_weights(MICRO, seed=11)
+    eos = 3
+    w.lm_head[eos] *= 4
+    orc = OracleLM(w, MICRO)
+    rng = np.random.default_rng(9)
+    prefix = rng.integers(0, MICRO.vocab, size=6)
+    digits = np.array([10, 11, 12, 13, 14, 15, 16, 17, 18, 19])
+    rows = _rand_rows(rng, 12, 1, 5, MICRO.vocab)
+    i = orc.eval_rows(prefix, rows, KIND_INT, digits, eos=eos, max_tokens=4)
+    a = orc.eval_rows(prefix, rows, KIND_AUTOMATON, _int_automaton(digits), eos=eos, max_tokens=4)
+    for k in ("logprob", "logprob_full", "n_tokens", "tokens", "margin"):
+        assert np.array_equal(a[k], i[k]), k
+    n_digits = np.array([n - (t[n - 1] == eos) for n, t in zip(i["n_tokens"], i["tokens"])])
+    assert np.array_equal(a["value"], n_digits)
+
+
+def test_automaton_trie_decode_matches_full_recompute(micro):
+    _, orc = micro
+    rng = np.random.default_rng(23)
+    prefix = rng.integers(0, MICRO.vocab, size=5)
+    options = [np.array(o) for o in ([40, 2], [40, 7, 9], [40, 7, 1], [66], [21, 2, 2])]
+    aut, final = option_trie(options)
+    g = automaton_steps(aut, eos=-1)
+    rows = _rand_rows(rng, 16, 1, 6, MICRO.vocab)
+    res = orc.eval_rows(prefix, rows, KIND_AUTOMATON, aut, max_tokens=3, keep_logits=True)
+    seen = set()
+    for r in range(16):
+        n = res["n_tokens"][r]
+        toks = res["tokens"][r][:n].tolist()
+        # the output is exactly the option whose final state is the value
+        o = final.tolist().index(res["value"][r])
+        assert toks == options[o].tolist()
+        seen.add(o)
+        st, lp, lpf = 0, 0.0, 0.0
+        for s in range(n):
+            seq = np.concatenate([prefix, rows[r], toks[:s]])
+            z = orc.logits(orc.forward_sequence(seq)[-1])[0]
+            assert np.allclose(res["logits"][r][s], z, atol=1e-11)
+            allowed, to = g[st]
+            ci, a, b, _ = constrained_pick(z, allowed)
+            assert allowed[ci] == toks[s]
+            lp, lpf, st = lp + a, lpf + b, to[ci]
+        assert math.isclose(res["logprob"][r], lp, abs_tol=1e-12)
+        assert math.isclose(res["logprob_full"][r], lpf, abs_tol=1e-12)
+    assert len(seen) >= 2
+
+
+def test_automaton_endings(micro):
+    _, orc = micro
+    rng = np.random.default_rng(25)
+    rows = _rand_rows(rng, 6, 1, 4, MICRO.vocab)
+    # a chain 0 -> 1 -> 2 -> 3 with only state 3 accepting: cut after 2 tokens
+    chain = Automaton(4, np.array([0, 1, 2, 3, 3], np.int32), np.array([5, 6, 7], np.int32),
+                      np.array([1, 2, 3], np.int32), np.array([0, 0, 0, 1], np.uint8))
+    res = orc.eval_rows(None, rows, KIND_AUTOMATON, chain, max_tokens=2)
+    assert np.all(res["value"] == -1) and np.all(res["n_tokens"] == 2)
+    assert np.all(res["tokens"][:, :2] == [5, 6]) and np.all(res["logprob"] == 0.0)
+    res = orc.eval_rows(None, rows, KIND_AUTOMATON, chain, max_tokens=3)
+    assert np.all(res["value"] == 3) and np.all(res["n_tokens"] == 3)
+    # an accepting state with edges ends on EOS or runs on
+    fork = Automaton(3, np.array([0, 1, 2, 2], np.int32), np.array([5, 6], np.int32),
+                     np.array([1, 2], np.int32), np.array([0, 1, 1], np.uint8))
+    w2 = make_weights(MICRO, seed=11)
+    w2.lm_head[9] *= 6
+    o2 = OracleLM(w2, MICRO)
+    res = o2.eval_rows(None, rows, KIND_AUTOMATON, fork, eos=9, max_tokens=3)
+    for r in range(6):
+        toks = res["tokens"][r][:res["n_tokens"][r]].tolist()
+        assert toks in ([5, 9], [5, 6])
+        assert res["value"][r] == (1 if toks == [5, 9] else 2)
+    lp = res["logprob"]
+    assert np.all(lp <= 0.0)
 
 
 def test_batch_and_order_invariance(micro):
