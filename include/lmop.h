@@ -136,25 +136,51 @@ int32_t lmop_prefix_length(const lmop_prefix* prefix);
 typedef enum {
   LMOP_BOOL = 0, /* tokens = {false_token, true_token}; value 0/1                        */
   LMOP_ENUM = 1, /* tokens[i] = single-token option i; value = option index              */
-  LMOP_INT = 2   /* tokens[d] = token of digit d (n_tokens = 10), eos_token ends the
+  LMOP_INT = 2,  /* tokens[d] = token of digit d (n_tokens = 10), eos_token ends the
                     number; a digit string of at most max_tokens tokens (EOS included),
                     no EOS at the first step; value = decimal value of the digits       */
+  LMOP_AUTOMATON = 3 /* multi-token outputs (option strings as a token trie, lists,
+                    other regular types): the steps follow a token automaton            */
 } lmop_kind;
+
+/* A token automaton (Sec. 2.3 "Constrained Decoding": option strings and
+ * other structured return types decoded token by token under a grammar).
+ * State 0 starts.  State s has the edges edge_token[e] -> edge_next[e] for
+ * e in [edge_offset[s], edge_offset[s+1]); accepting[s] != 0 lets an output
+ * end in s.  A step in state s allows s's edge tokens, ordered by where
+ * each token first appears in edge_token (this order breaks ties), and,
+ * when s is accepting and eos_token >= 0, the EOS token last.  The output
+ * ends on EOS, on reaching an accepting state without edges, or after
+ * max_tokens tokens; value = the final state, or -1 if that state is not
+ * accepting.  Limits: n_states in 1..65536; edges in 1..2^20; state 0 and
+ * every non-accepting state have edges; a state's edge tokens are distinct
+ * ids in [0, vocab); EOS is none of the edge tokens; the distinct edge
+ * tokens plus EOS number at most 4096.  All arrays are host memory. */
+typedef struct {
+  int32_t n_states;
+  const int32_t* edge_offset; /* [n_states + 1], edge_offset[0] = 0, non-decreasing */
+  const int32_t* edge_token;  /* [edge_offset[n_states]] */
+  const int32_t* edge_next;   /* [edge_offset[n_states]], in [0, n_states) */
+  const uint8_t* accepting;   /* [n_states] */
+} lmop_automaton;
 
 typedef struct {
   int32_t kind;          /* lmop_kind */
-  const int32_t* tokens; /* host [n_tokens], distinct ids in [0, vocab) */
+  const int32_t* tokens; /* host [n_tokens], distinct ids in [0, vocab); AUTOMATON: unused */
   int32_t n_tokens;      /* BOOL: 2; ENUM: 1..4096; INT: 10 */
-  int32_t eos_token;     /* INT only: not one of the digit tokens */
-  int32_t max_tokens;    /* INT: 1..8; BOOL/ENUM: ignored (1) */
+  int32_t eos_token;     /* INT: not one of the digit tokens; AUTOMATON: -1 (none) or the
+                            token that ends an output in an accepting state */
+  int32_t max_tokens;    /* INT, AUTOMATON: 1..8; BOOL/ENUM: ignored (1) */
+  const lmop_automaton* automaton; /* AUTOMATON only */
 } lmop_type;
 
 typedef struct {
-  int64_t value;      /* BOOL 0/1; ENUM option index; INT decimal value                     */
+  int64_t value;      /* BOOL 0/1; ENUM option index; INT decimal value; AUTOMATON final
+                         state (-1: cut off by max_tokens in a non-accepting state)        */
   float logprob;      /* sum over steps of log-softmax over that step's allowed tokens       */
   float logprob_full; /* sum over steps of log-softmax over the whole vocabulary; NaN with
                          LMOP_HEAD_RESTRICTED                                              */
-  int32_t n_tokens;   /* tokens generated (INT: EOS included)                               */
+  int32_t n_tokens;   /* tokens generated (EOS included)                                   */
   int32_t tokens[8];  /* generated token ids; unused entries are -1                         */
 } lmop_result;
 

@@ -185,14 +185,20 @@ __global__ __launch_bounds__(256) void head_restricted_kernel(const f16* __restr
 
 // --------------------------------------------------------------- head finish
 // One wave per row: LSE over the vocabulary from the per-slice partials, then
-// the first maximum among the allowed tokens and the allowed-set LSE.
+// the first maximum among the allowed tokens and the allowed-set LSE.  With a
+// state mask the row's allowed tokens are the entries its state's mask row
+// marks.
 __global__ __launch_bounds__(64) void head_finalize_kernel(const float2* __restrict__ part,
                                                            int n_chunks,
                                                            const float* __restrict__ zsel,
                                                            int n_sel, int n_allowed,
                                                            const int32_t* __restrict__ allowed_tok,
-                                                           HeadPick* __restrict__ out) {
+                                                           HeadPick* __restrict__ out,
+                                                           const int32_t* __restrict__ row_state,
+                                                           const uint8_t* __restrict__ state_mask) {
   const int r = blockIdx.x, lane = threadIdx.x;
+  const uint8_t* mk = state_mask ? state_mask + (size_t)row_state[r] * n_sel : nullptr;
+  auto ok = [&](int j) { return mk == nullptr || mk[j] != 0; };
   const float2* pr = part + (size_t)r * n_chunks;
   float mx = -INFINITY;
   for (int j = lane; j < n_chunks; j += 64) mx = fmaxf(mx, pr[j].x);
@@ -212,6 +218,7 @@ __global__ __launch_bounds__(64) void head_finalize_kernel(const float2* __restr
   float best = -INFINITY;
   int bi = n_allowed;  // sentinel; stays only if every logit is NaN
   for (int j = lane; j < n_allowed; j += 64) {
+    if (!ok(j)) continue;
     const float z = zr[j];
     if (z > best || (z == best && j < bi)) {
       best = z;
@@ -229,21 +236,29 @@ __global__ __launch_bounds__(64) void head_finalize_kernel(const float2* __restr
   }
   if (bi >= n_allowed) bi = 0;  // keeps the index in bounds whatever the logits hold
   float second = -INFINITY;
+  int n_ok = 0;
   for (int j = lane; j < n_allowed; j += 64)
-    if (j != bi) second = fmaxf(second, zr[j]);
+    if (ok(j)) {
+      ++n_ok;
+      if (j != bi) second = fmaxf(second, zr[j]);
+    }
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) second = fmaxf(second, shfl_xor(second, o));
   float sa = 0.f;
-  for (int j = lane; j < n_allowed; j += 64) sa += expf(zr[j] - best);
+  for (int j = lane; j < n_allowed; j += 64)
+    if (ok(j)) sa += expf(zr[j] - best);
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) sa += shfl_xor(sa, o);
+  for (int o = 32; o >= 1; o >>= 1) {
+    sa += shfl_xor(sa, o);
+    n_ok += shfl_xor(n_ok, o);
+  }
   if (lane == 0) {
     HeadPick hp;
     hp.index = bi;
     hp.token = allowed_tok[bi];
     hp.logprob = -logf(sa);
     hp.logprob_full = n_chunks > 0 ? best - lse_full : NAN;
-    hp.margin = n_allowed > 1 ? best - second : INFINITY;
+    hp.margin = n_ok > 1 ? best - second : INFINITY;
     hp.pad[0] = hp.pad[1] = hp.pad[2] = 0.f;
     out[r] = hp;
   }
@@ -313,10 +328,12 @@ hipError_t launch_head_restricted(hipStream_t s, const half_bits* hn, int R, int
 
 hipError_t launch_head_finalize(hipStream_t s, const float2* part, int n_chunks,
                                 const float* zsel, int n_sel, int n_allowed,
-                                const int32_t* allowed_tok, int R, HeadPick* out) {
+                                const int32_t* allowed_tok, int R, HeadPick* out,
+                                const int32_t* row_state, const uint8_t* state_mask) {
   if (R == 0) return hipSuccess;
+  if (state_mask && !row_state) return hipErrorInvalidValue;
   hipLaunchKernelGGL(head_finalize_kernel, dim3(R), dim3(64), 0, s, part, n_chunks, zsel, n_sel,
-                     n_allowed, allowed_tok, out);
+                     n_allowed, allowed_tok, out, row_state, state_mask);
   return hipGetLastError();
 }
 

@@ -141,9 +141,13 @@ struct HeadPick {
 hipError_t launch_head_restricted(hipStream_t s, const half_bits* hn, int R, int d,
                                   const half_bits* W, const int32_t* allowed, int n_sel,
                                   float* zsel, float* dump, int ld_dump);
-// n_chunks = 0: no vocabulary partials (restricted head), logprob_full = NaN
+// n_chunks = 0: no vocabulary partials (restricted head), logprob_full = NaN.
+// state_mask != NULL: row r picks only among entries j < n_allowed with
+// state_mask[row_state[r] * n_sel + j] != 0 (token-automaton outputs).
 hipError_t launch_head_finalize(hipStream_t s, const float2* part, int n_chunks,
                                 const float* zsel, int n_sel, int n_allowed,
-                                const int32_t* allowed_tok, int R, HeadPick* out);
+                                const int32_t* allowed_tok, int R, HeadPick* out,
+                                const int32_t* row_state = nullptr,
+                                const uint8_t* state_mask = nullptr);
 
 }  // namespace lmop

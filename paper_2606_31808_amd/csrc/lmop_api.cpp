@@ -238,8 +238,10 @@ lmop_status stage_mark(lmop_ctx* c, int k) {
 
 // Upper bound of the staging bytes one batch of T tokens and R rows needs.
 size_t stage_need(int T, int R, size_t n_work) {
-  return (size_t)T * 12 + (size_t)R * (sizeof(AttnRow) + 4 + sizeof(void*) + sizeof(HeadPick)) +
-         n_work * sizeof(int2) + 16 * 16;
+  // tokens, positions, slots; per row: attention row, last-token index,
+  // head row pointer, automaton state, pick; work items; alignment
+  return (size_t)T * 12 + (size_t)R * (sizeof(AttnRow) + 8 + sizeof(void*) + sizeof(HeadPick)) +
+         n_work * sizeof(int2) + 16 * 17;
 }
 
 // ---------------------------------------------------------------- profiling
@@ -341,10 +343,61 @@ lmop_status check_tokens(lmop_ctx* c, const int32_t* t, int64_t n, const char* w
   return LMOP_OK;
 }
 
+// A token automaton's validity (the limits stated with lmop_automaton).
+lmop_status check_automaton(lmop_ctx* c, const lmop_type* ty) {
+  const lmop_automaton* a = ty->automaton;
+  if (!a) return fail(c, LMOP_ERR_INVALID_ARG, "AUTOMATON type without an automaton");
+  if (ty->max_tokens < 1 || ty->max_tokens > 8)
+    return fail(c, LMOP_ERR_INVALID_ARG, "AUTOMATON max_tokens %d outside 1..8", ty->max_tokens);
+  const int S = a->n_states;
+  if (S < 1 || S > 65536)
+    return fail(c, LMOP_ERR_INVALID_ARG, "automaton n_states %d outside 1..65536", S);
+  if (!a->edge_offset || !a->edge_token || !a->edge_next || !a->accepting)
+    return fail(c, LMOP_ERR_INVALID_ARG, "automaton has a NULL array");
+  if (a->edge_offset[0] != 0) return fail(c, LMOP_ERR_INVALID_ARG, "automaton edge_offset[0] != 0");
+  for (int s = 0; s < S; ++s)
+    if (a->edge_offset[s + 1] < a->edge_offset[s])
+      return fail(c, LMOP_ERR_INVALID_ARG, "automaton edge_offset decreases at state %d", s);
+  const int E = a->edge_offset[S];
+  if (E < 1 || E > (1 << 20))
+    return fail(c, LMOP_ERR_INVALID_ARG, "automaton has %d edges (1..2^20)", E);
+  LMOP_TRY(check_tokens(c, a->edge_token, E, "automaton edge"));
+  std::set<int32_t> all;
+  for (int s = 0; s < S; ++s) {
+    const int e0 = a->edge_offset[s], e1 = a->edge_offset[s + 1];
+    if (e0 == e1 && (s == 0 || !a->accepting[s]))
+      return fail(c, LMOP_ERR_INVALID_ARG, "automaton state %d has no edges and %s", s,
+                  s == 0 ? "is the start" : "is not accepting");
+    std::set<int32_t> own;
+    for (int e = e0; e < e1; ++e) {
+      if (a->edge_next[e] < 0 || a->edge_next[e] >= S)
+        return fail(c, LMOP_ERR_INVALID_ARG, "automaton edge %d leads to state %d", e,
+                    a->edge_next[e]);
+      if (!own.insert(a->edge_token[e]).second)
+        return fail(c, LMOP_ERR_INVALID_ARG, "automaton state %d repeats token %d", s,
+                    a->edge_token[e]);
+      all.insert(a->edge_token[e]);
+    }
+  }
+  if (ty->eos_token >= 0) {
+    if (ty->eos_token >= c->cfg.vocab)
+      return fail(c, LMOP_ERR_INVALID_ARG, "eos_token %d outside the vocabulary", ty->eos_token);
+    if (all.count(ty->eos_token))
+      return fail(c, LMOP_ERR_INVALID_ARG, "eos_token %d is an edge token", ty->eos_token);
+  }
+  const size_t n_union = all.size() + (ty->eos_token >= 0 ? 1 : 0);
+  if (n_union > 4096)
+    return fail(c, LMOP_ERR_INVALID_ARG, "automaton uses more than 4096 distinct tokens");
+  if ((size_t)S * n_union > (size_t(1) << 26))
+    return fail(c, LMOP_ERR_INVALID_ARG, "automaton states x distinct tokens exceeds 2^26");
+  return LMOP_OK;
+}
+
 lmop_status check_type(lmop_ctx* c, const lmop_type* ty) {
   if (!ty) return fail(c, LMOP_ERR_INVALID_ARG, "type is NULL");
-  if (ty->kind < LMOP_BOOL || ty->kind > LMOP_INT)
+  if (ty->kind < LMOP_BOOL || ty->kind > LMOP_AUTOMATON)
     return fail(c, LMOP_ERR_INVALID_ARG, "unknown type kind %d", ty->kind);
+  if (ty->kind == LMOP_AUTOMATON) return check_automaton(c, ty);
   if (!ty->tokens) return fail(c, LMOP_ERR_INVALID_ARG, "type tokens is NULL");
   const int n = ty->n_tokens;
   if (ty->kind == LMOP_BOOL && n != 2)
@@ -678,7 +731,9 @@ void add_work(std::vector<int2>& work, int row, int n_q, int G) {
 // valid once the stream has passed this point.
 lmop_status run_head(lmop_ctx* c, int k, int R, const std::vector<const float*>& rowptr,
                      const int32_t* d_sel, const int32_t* d_allowed, int n_sel, int n_allowed,
-                     bool restricted, HeadPick** picks, float* dump_dev) {
+                     bool restricted, HeadPick** picks, float* dump_dev,
+                     const uint8_t* d_state_mask = nullptr,
+                     const std::vector<int32_t>* states = nullptr) {
   const lmop_config& cf = c->cfg;
   const int d = cf.d_model, V = cf.vocab;
   constexpr int kVocabTile = 128;
@@ -728,9 +783,19 @@ lmop_status run_head(lmop_ctx* c, int k, int R, const std::vector<const float*>&
       }));
     }
   }
+  // per-row automaton states: row r picks within state_mask[states[r]]
+  int32_t* d_states = nullptr;
+  if (states) {
+    int32_t* hst;
+    LMOP_TRY(ws_get(c, "head_state", R, &d_states));
+    LMOP_TRY(stage_put(c, k, states->data(), (size_t)R, &hst));
+    HIP_OK(c, hipMemcpyAsync(d_states, hst, R * sizeof(int32_t), hipMemcpyHostToDevice,
+                             c->stream));
+  }
   LMOP_TRY(timed(c, "head_finalize", 0, 0, [&] {
     return launch_head_finalize(c->stream, part, restricted ? 0 : n_chunks, zsel, n_sel,
-                                n_allowed, d_allowed, R, dpk);
+                                n_allowed, d_allowed, R, dpk, d_states,
+                                states ? d_state_mask : nullptr);
   }));
   LMOP_TRY(stage_put(c, k, (const HeadPick*)nullptr, (size_t)R, picks));
   HIP_OK(c, hipMemcpyAsync(*picks, dpk, R * sizeof(HeadPick), hipMemcpyDeviceToHost, c->stream));
@@ -1219,7 +1284,8 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
   if (total > 0 && !tokens) return fail(ctx, LMOP_ERR_INVALID_ARG, "tokens is NULL");
   LMOP_TRY(check_tokens(ctx, tokens, total, "row"));
   const lmop_config& cf = ctx->cfg;
-  const int steps = type->kind == LMOP_INT ? type->max_tokens : 1;
+  const bool is_aut = type->kind == LMOP_AUTOMATON;
+  const int steps = type->kind == LMOP_INT || is_aut ? type->max_tokens : 1;
   const int dec = steps - 1;
   if (prefix && !prefix_live(ctx, prefix))
     return fail(ctx, LMOP_ERR_INVALID_ARG, "prefix is released or from another ctx");
@@ -1271,12 +1337,26 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
     return ia < ib;
   });
 
-  // allowed-token map: sel[token] = position in the allowed list (INT: EOS last)
-  const int n_allowed0 = type->n_tokens;
-  std::vector<int32_t> allowed(type->tokens, type->tokens + n_allowed0);
-  if (type->kind == LMOP_INT) allowed.push_back(type->eos_token);
-  const int n_sel = (int)allowed.size();
+  // allowed-token map: sel[token] = position in the allowed list (INT: EOS
+  // last).  An automaton's list is every edge token in order of first
+  // appearance, then EOS; each state allows a subset of it (a row of the
+  // state mask table), and the head picks within the row's state's subset.
+  const lmop_automaton* aut = type->automaton;
+  std::vector<int32_t> allowed;
   std::vector<int32_t> sel(V, -1);
+  if (is_aut) {
+    for (int e = 0; e < aut->edge_offset[aut->n_states]; ++e)
+      if (sel[aut->edge_token[e]] < 0) {
+        sel[aut->edge_token[e]] = (int)allowed.size();
+        allowed.push_back(aut->edge_token[e]);
+      }
+    if (type->eos_token >= 0) allowed.push_back(type->eos_token);
+  } else {
+    allowed.assign(type->tokens, type->tokens + type->n_tokens);
+    if (type->kind == LMOP_INT) allowed.push_back(type->eos_token);
+  }
+  const int n_sel = (int)allowed.size();
+  const int n_allowed0 = is_aut ? n_sel : type->n_tokens;
   for (int i = 0; i < n_sel; ++i) sel[allowed[i]] = i;
   int32_t *d_sel, *d_allowed;
   LMOP_TRY(ws_get(ctx, "sel", V, &d_sel));
@@ -1284,6 +1364,21 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
   HIP_OK(ctx, hipMemcpyAsync(d_sel, sel.data(), V * 4, hipMemcpyHostToDevice, ctx->stream));
   HIP_OK(ctx, hipMemcpyAsync(d_allowed, allowed.data(), n_sel * 4, hipMemcpyHostToDevice,
                              ctx->stream));
+  uint8_t* d_state_mask = nullptr;
+  std::vector<uint8_t> state_mask;
+  if (is_aut) {
+    const int S = aut->n_states;
+    state_mask.assign((size_t)S * n_sel, 0);
+    for (int st = 0; st < S; ++st) {
+      for (int e = aut->edge_offset[st]; e < aut->edge_offset[st + 1]; ++e)
+        state_mask[(size_t)st * n_sel + sel[aut->edge_token[e]]] = 1;
+      if (aut->accepting[st] && type->eos_token >= 0)
+        state_mask[(size_t)st * n_sel + n_sel - 1] = 1;
+    }
+    LMOP_TRY(ws_get(ctx, "state_mask", state_mask.size(), &d_state_mask));
+    HIP_OK(ctx, hipMemcpyAsync(d_state_mask, state_mask.data(), state_mask.size(),
+                               hipMemcpyHostToDevice, ctx->stream));
+  }
   HIP_OK(ctx, hipStreamSynchronize(ctx->stream));
 
   const int G = cf.n_heads / cf.n_kv_heads;
@@ -1346,6 +1441,7 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
   // its group's store, last chosen token
   std::vector<int> row_len(uniq.size()), own_slot(uniq.size());
   std::vector<int32_t> last_tok(uniq.size(), -1);
+  std::vector<int32_t> row_state(uniq.size(), 0);  // automaton state
   for (size_t u = 0; u < uniq.size(); ++u)
     row_len[u] = (int)(offsets[uniq[u] + 1] - offsets[uniq[u]]);
 
@@ -1433,8 +1529,10 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
     }
     B.dump = nullptr;
     if (dbg) LMOP_TRY(ws_get(ctx, "dump", (size_t)R * V, &B.dump));
+    std::vector<int32_t> st0;
+    if (is_aut) st0.assign(R, 0);
     LMOP_TRY(run_head(ctx, k, R, rowptr, d_sel, d_allowed, n_sel, n_allowed0, restricted, &B.picks,
-                      B.dump));
+                      B.dump, d_state_mask, is_aut ? &st0 : nullptr));
     LMOP_TRY(stage_mark(ctx, k));
     B.u0 = u0;
     B.R = R;
@@ -1448,6 +1546,29 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
     o.logprob += hp.logprob;
     o.logprob_full += hp.logprob_full;
     o.tokens[o.n_tokens++] = hp.token;
+    if (is_aut) {
+      // EOS ends the output in the current (accepting) state
+      int32_t& st = row_state[u];
+      if (type->eos_token >= 0 && hp.index == n_sel - 1) {
+        o.value = st;
+        return false;
+      }
+      int nxt = -1;
+      for (int e = aut->edge_offset[st]; e < aut->edge_offset[st + 1]; ++e)
+        if (aut->edge_token[e] == hp.token) nxt = aut->edge_next[e];
+      if (nxt < 0) {  // not reachable: the state mask allows only edge tokens
+        o.value = -1;
+        return false;
+      }
+      st = nxt;
+      const bool leaf = aut->edge_offset[st + 1] == aut->edge_offset[st];
+      if (leaf || o.n_tokens >= steps) {
+        o.value = aut->accepting[st] ? st : -1;
+        return false;
+      }
+      last_tok[u] = hp.token;
+      return true;
+    }
     if (type->kind != LMOP_INT) {
       o.value = hp.index;
       return false;
@@ -1522,8 +1643,11 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
       float* dump = nullptr;
       if (dbg) LMOP_TRY(ws_get(ctx, "dump", (size_t)nl * V, &dump));
       HeadPick* picks;
+      std::vector<int32_t> st_live;
+      if (is_aut)
+        for (int q = 0; q < nl; ++q) st_live.push_back(row_state[live[q]]);
       LMOP_TRY(run_head(ctx, 0, nl, rowptr, d_sel, d_allowed, n_sel, n_sel, restricted, &picks,
-                        dump));
+                        dump, d_state_mask, is_aut ? &st_live : nullptr));
       LMOP_TRY(stage_mark(ctx, 0));
       HIP_OK(ctx, hipEventSynchronize(ctx->stage[0].done));
       ctx->stage[0].pending = false;

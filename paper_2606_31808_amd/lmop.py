@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "_lib", "liblmop.so")
 
 LMOP_OK, LMOP_ERR_INVALID_ARG, LMOP_ERR_STATE, LMOP_ERR_OOM, LMOP_ERR_DEVICE, \
     LMOP_ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
-LMOP_BOOL, LMOP_ENUM, LMOP_INT = 0, 1, 2
+LMOP_BOOL, LMOP_ENUM, LMOP_INT, LMOP_AUTOMATON = 0, 1, 2, 3
 LMOP_NO_DEDUP = 1
 LMOP_HEAD_RESTRICTED = 2
 
@@ -54,9 +54,16 @@ class lmop_weights(C.Structure):
                 ("n_layers", C.c_int32), ("on_device", C.c_int32)]
 
 
+class lmop_automaton(C.Structure):
+    _fields_ = [("n_states", C.c_int32), ("edge_offset", C.POINTER(C.c_int32)),
+                ("edge_token", C.POINTER(C.c_int32)), ("edge_next", C.POINTER(C.c_int32)),
+                ("accepting", C.POINTER(C.c_uint8))]
+
+
 class lmop_type(C.Structure):
     _fields_ = [("kind", C.c_int32), ("tokens", C.POINTER(C.c_int32)), ("n_tokens", C.c_int32),
-                ("eos_token", C.c_int32), ("max_tokens", C.c_int32)]
+                ("eos_token", C.c_int32), ("max_tokens", C.c_int32),
+                ("automaton", C.POINTER(lmop_automaton))]
 
 
 class lmop_result(C.Structure):
@@ -221,14 +228,26 @@ def lmop_eval_rows(ctx, tokens, offsets, kind: int, allowed: Sequence[int], eos:
                    max_tokens: int = 1, prefix=None, row_prefix=None, flags: int = 0,
                    max_batch_tokens: int = 0, debug_logits: bool = False, vocab: int = 0):
     """Returns a structured numpy array of lmop_result (value, logprob, logprob_full,
-    n_tokens, tokens) and, with debug_logits, fp32 logits [n_rows][steps][vocab]."""
+    n_tokens, tokens) and, with debug_logits, fp32 logits [n_rows][steps][vocab].
+    For LMOP_AUTOMATON, `allowed` is an object with n_states, edge_offset,
+    edge_token, edge_next and accepting arrays."""
     toks = _i32(tokens)
     offs = _i64(offsets)
     n = len(offs) - 1
-    al = _i32(allowed)
-    ty = lmop_type(kind, _ptr(al, C.c_int32), len(al), int(eos), int(max_tokens))
+    keep = []
+    if kind == LMOP_AUTOMATON:
+        eo, et, en = _i32(allowed.edge_offset), _i32(allowed.edge_token), _i32(allowed.edge_next)
+        ac = np.ascontiguousarray(np.asarray(allowed.accepting, dtype=np.uint8))
+        keep = [eo, et, en, ac]
+        aut = lmop_automaton(int(allowed.n_states), _ptr(eo, C.c_int32), _ptr(et, C.c_int32),
+                             _ptr(en, C.c_int32), _ptr(ac, C.c_uint8))
+        ty = lmop_type(kind, None, 0, int(eos), int(max_tokens), C.pointer(aut))
+    else:
+        al = _i32(allowed)
+        keep = [al]
+        ty = lmop_type(kind, _ptr(al, C.c_int32), len(al), int(eos), int(max_tokens), None)
     out = np.zeros(max(n, 0), dtype=RESULT_DTYPE)
-    steps = max_tokens if kind == LMOP_INT else 1
+    steps = max_tokens if kind in (LMOP_INT, LMOP_AUTOMATON) else 1
     dbg = None
     opts = lmop_eval_opts(flags, max_batch_tokens, None)
     if debug_logits:
@@ -242,6 +261,7 @@ def lmop_eval_rows(ctx, tokens, offsets, kind: int, allowed: Sequence[int], eos:
                                         for r in row_prefix])
     _check(_lib.lmop_eval_rows(ctx, prefix, rp, _ptr(toks, C.c_int32), _ptr(offs, C.c_int64), n,
                                C.byref(ty), out.ctypes.data, C.byref(opts)), ctx)
+    del keep
     return out, dbg
 
 

@@ -104,3 +104,33 @@ def assert_typed(out, kind, n_allowed, allowed, eos=-1, max_tokens=1):
             assert n == 1 and toks[0] in allowed
             assert allowed[int(out["value"][r])] == toks[0]
             assert 0 <= out["value"][r] < n_allowed
+
+
+def assert_automaton(out, aut, eos=-1, max_tokens=1):
+    """Every result is a path of the token automaton from state 0 that ends
+    on EOS, at an accepting state without edges or after max_tokens; the
+    value is the final state, -1 if that state is not accepting."""
+    off, tok, nxt, acc = (np.asarray(aut.edge_offset), np.asarray(aut.edge_token),
+                          np.asarray(aut.edge_next), np.asarray(aut.accepting))
+    for r in range(len(out)):
+        n = int(out["n_tokens"][r])
+        toks = out["tokens"][r][:n].tolist()
+        assert np.all(out["tokens"][r][n:] == -1)
+        assert 1 <= n <= max_tokens and out["logprob"][r] <= 1e-6
+        st, ended = 0, None
+        for i, t in enumerate(toks):
+            assert ended is None, f"row {r}: token after the end"
+            if eos >= 0 and t == eos:
+                assert acc[st], f"row {r}: EOS in a non-accepting state"
+                ended = st
+                continue
+            edges = tok[off[st]:off[st + 1]].tolist()
+            assert t in edges, f"row {r}: token {t} is not an edge of state {st}"
+            st = int(nxt[off[st] + edges.index(t)])
+            if off[st + 1] == off[st]:
+                ended = st
+        if ended is None:
+            assert n == max_tokens, f"row {r}: stopped early in state {st}"
+            ended = st
+        want = ended if acc[ended] else -1
+        assert int(out["value"][r]) == want, f"row {r}: value {out['value'][r]} != {want}"

@@ -9,8 +9,9 @@ import pytest
 import torch
 
 from oracle import KIND_BOOL, KIND_ENUM, KIND_INT, OracleLM
+from oracle.lmop_oracle import KIND_AUTOMATON
 from synth import SHAPES, make_weights, make_workload
-from tests.parity import assert_typed, compare
+from tests.parity import assert_automaton, assert_typed, compare
 
 pytestmark = pytest.mark.gpu
 TINY = SHAPES["tiny"]
@@ -225,6 +226,97 @@ def test_tiny_int_decode(L):
                    cols=list(digits) + [eos])
     _log("int decode, restricted head", st_r)
     assert_typed(out_r, KIND_INT, 10, digits, eos, 4)
+
+
+def test_tiny_options_automaton(tiny, L):
+    """Multi-token options as a token trie: every row's output is one whole
+    option, parity with the oracle (teacher-forced where a sub-margin step
+    diverged), the restricted head, and any batching giving the same bits."""
+    w, orc, ctx = tiny
+    wl = make_workload("options_tiny")
+    aut = wl.automaton
+    pre = ctx.set_prefix(wl.prefix)
+    kw = dict(eos=wl.eos, max_tokens=wl.max_tokens, prefix=pre)
+    _log("options: eval")
+    out, dbg = ctx.eval_rows(wl.tokens, wl.offsets, L.LMOP_AUTOMATON, aut, debug_logits=True,
+                             **kw)
+    assert_automaton(out, aut, wl.eos, wl.max_tokens)
+    final = {f: o for o, f in enumerate(_final_states(wl.options, aut))}
+    for r in range(wl.n_rows):
+        o = final[int(out["value"][r])]
+        assert out["tokens"][r][:out["n_tokens"][r]].tolist() == wl.options[o].tolist()
+    ref = orc.eval_workload(wl, keep_logits=True)
+    forced = orc.eval_rows(wl.prefix, [wl.suffix(r) for r in range(wl.n_rows)], KIND_AUTOMATON,
+                           aut, max_tokens=wl.max_tokens, keep_logits=True,
+                           forced=[out["tokens"][r][: out["n_tokens"][r]]
+                                   for r in range(wl.n_rows)])
+    st = compare(ref, out, dbg, "options", orc_forced=forced)
+    _log("options", st)
+    assert len(set(out["value"].tolist())) >= 3
+    # the restricted head computes only the trie's tokens
+    out_r, dbg_r = ctx.eval_rows(wl.tokens, wl.offsets, L.LMOP_AUTOMATON, aut, debug_logits=True,
+                                 head_restricted=True, **kw)
+    cols = sorted(set(np.asarray(aut.edge_token).tolist()))
+    forced_r = orc.eval_rows(wl.prefix, [wl.suffix(r) for r in range(wl.n_rows)], KIND_AUTOMATON,
+                             aut, max_tokens=wl.max_tokens, keep_logits=True,
+                             forced=[out_r["tokens"][r][: out_r["n_tokens"][r]]
+                                     for r in range(wl.n_rows)])
+    _log("options, restricted head",
+         compare(ref, out_r, dbg_r, "options restricted", orc_forced=forced_r, cols=cols))
+    assert_automaton(out_r, aut, wl.eos, wl.max_tokens)
+    # batching does not change a bit
+    for mbt in (40, 97):
+        o2, d2 = ctx.eval_rows(wl.tokens, wl.offsets, L.LMOP_AUTOMATON, aut, debug_logits=True,
+                               max_batch_tokens=mbt, **kw)
+        assert o2.tobytes() == out.tobytes() and np.array_equal(d2, dbg, equal_nan=True), mbt
+    ctx.release_prefix(pre)
+
+
+def _final_states(options, aut):
+    off, tok, nxt = (np.asarray(aut.edge_offset), np.asarray(aut.edge_token),
+                     np.asarray(aut.edge_next))
+    out = []
+    for o in options:
+        st = 0
+        for t in o.tolist():
+            edges = tok[off[st]:off[st + 1]].tolist()
+            st = int(nxt[off[st] + edges.index(t)])
+        out.append(st)
+    return out
+
+
+def test_tiny_automaton_equals_enum_and_int(tiny, L):
+    """ENUM and INT written as token automata give the same bits as the
+    built-in kinds (value aside: the automaton reports the final state)."""
+    from synth import Automaton
+    w, orc, ctx = tiny
+    wl = make_workload("filter_tiny")
+    pre = ctx.set_prefix(wl.prefix)
+    V = TINY.vocab
+    rng = np.random.default_rng(31)
+    opts = rng.choice(V, 5, replace=False).astype(np.int32)
+    star = Automaton(6, np.array([0, 5, 5, 5, 5, 5, 5], np.int32), opts,
+                     np.arange(1, 6, dtype=np.int32), np.array([0, 1, 1, 1, 1, 1], np.uint8))
+    e, de = ctx.eval_rows(wl.tokens, wl.offsets, KIND_ENUM, opts, prefix=pre, debug_logits=True)
+    a, da = ctx.eval_rows(wl.tokens, wl.offsets, L.LMOP_AUTOMATON, star, max_tokens=2,
+                          prefix=pre, debug_logits=True)
+    for k in ("logprob", "logprob_full", "n_tokens", "tokens"):
+        assert np.array_equal(a[k], e[k]), k
+    assert np.array_equal(a["value"], e["value"] + 1)
+    assert np.array_equal(da[:, :1], de)
+    digits = rng.choice(V, 10, replace=False).astype(np.int32)
+    eos = int(next(t for t in range(V) if t not in digits))
+    ints = Automaton(5, np.array([0, 10, 20, 30, 40, 40], np.int32), np.tile(digits, 4),
+                     np.repeat(np.arange(1, 5, dtype=np.int32), 10),
+                     np.array([0, 1, 1, 1, 1], np.uint8))
+    i, di = ctx.eval_rows(wl.tokens, wl.offsets, KIND_INT, digits, eos=eos, max_tokens=4,
+                          prefix=pre, debug_logits=True)
+    a, da = ctx.eval_rows(wl.tokens, wl.offsets, L.LMOP_AUTOMATON, ints, eos=eos, max_tokens=4,
+                          prefix=pre, debug_logits=True)
+    for k in ("logprob", "logprob_full", "n_tokens", "tokens"):
+        assert np.array_equal(a[k], i[k]), k
+    assert np.array_equal(da, di, equal_nan=True)
+    ctx.release_prefix(pre)
 
 
 def test_tiny_restricted_head(tiny, L):

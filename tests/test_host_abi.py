@@ -203,9 +203,49 @@ def test_dedup_rejects_bad_csr():
     assert nu == 0 and len(rep) == 0
 
 
+def test_automaton_validation(tiny_w):
+    from synth import Automaton
+    ctx = _host_ctx()
+    ctx.load_weights(tiny_w)
+    V = TINY.vocab
+
+    def aut(off, tok, nxt, acc):
+        return Automaton(len(acc), np.array(off, np.int32), np.array(tok, np.int32),
+                         np.array(nxt, np.int32), np.array(acc, np.uint8))
+
+    good = aut([0, 2, 3, 3], [5, 6, 7], [1, 2, 2], [0, 1, 1])
+    run = lambda a, eos=-1, mt=3: ctx.eval_rows([1, 2], [0, 2], L.LMOP_AUTOMATON, a, eos=eos,
+                                                max_tokens=mt)
+    # valid: stops at UNSUPPORTED (host-only ctx) after validation
+    _expect(L.LMOP_ERR_UNSUPPORTED, run, good)
+    _expect(L.LMOP_ERR_UNSUPPORTED, run, good, eos=9)
+    bad = [
+        (aut([0, 2, 3, 3], [5, 6, 7], [1, 2, 2], [0, 1, 1]), dict(mt=0)),
+        (aut([0, 2, 3, 3], [5, 6, 7], [1, 2, 2], [0, 1, 1]), dict(mt=9)),
+        (aut([1, 2, 3, 3], [5, 6, 7], [1, 2, 2], [0, 1, 1]), {}),      # offset[0] != 0
+        (aut([0, 3, 2, 3], [5, 6, 7], [1, 2, 2], [0, 1, 1]), {}),      # decreasing
+        (aut([0, 2, 3, 3], [5, V, 7], [1, 2, 2], [0, 1, 1]), {}),      # token outside V
+        (aut([0, 2, 3, 3], [5, 5, 7], [1, 2, 2], [0, 1, 1]), {}),      # repeated in a state
+        (aut([0, 2, 3, 3], [5, 6, 7], [1, 3, 2], [0, 1, 1]), {}),      # next out of range
+        (aut([0, 2, 3, 3], [5, 6, 7], [1, 2, 2], [0, 1, 0]), {}),      # dead non-accepting
+        (aut([0, 0, 1, 1], [7], [2], [1, 1, 1]), {}),                  # start without edges
+        (aut([0, 2, 3, 3], [5, 6, 7], [1, 2, 2], [0, 1, 1]), dict(eos=6)),   # EOS is an edge
+        (aut([0, 2, 3, 3], [5, 6, 7], [1, 2, 2], [0, 1, 1]), dict(eos=V)),
+    ]
+    for a, kw in bad:
+        _expect(L.LMOP_ERR_INVALID_ARG, run, a, **kw)
+    # more than 4096 distinct tokens
+    n = 4097
+    big = aut([0, n] + [n] * n, list(range(n)), list(range(1, n + 1)), [0] + [1] * n)
+    _expect(L.LMOP_ERR_INVALID_ARG, run, big)
+
+
 def test_binding_constants_match_header():
     """The flag values the binding passes are the header's."""
     hdr = open(os.path.join(ROOT, "include", "lmop.h")).read()
     defs = dict(re.findall(r"#define\s+(LMOP_\w+)\s+(\d+)u", hdr))
     assert defs == {"LMOP_NO_DEDUP": "1", "LMOP_HEAD_RESTRICTED": "2"}
     assert L.LMOP_NO_DEDUP == 1 and L.LMOP_HEAD_RESTRICTED == 2
+    kinds = dict(re.findall(r"(LMOP_(?:BOOL|ENUM|INT|AUTOMATON))\s*=\s*(\d+)", hdr))
+    assert kinds == {"LMOP_BOOL": "0", "LMOP_ENUM": "1", "LMOP_INT": "2", "LMOP_AUTOMATON": "3"}
+    assert (L.LMOP_BOOL, L.LMOP_ENUM, L.LMOP_INT, L.LMOP_AUTOMATON) == (0, 1, 2, 3)
