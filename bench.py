@@ -331,7 +331,7 @@ def main():
     log(f"[bench] load {t_load:.2f} s, prefix {t_prefix * 1e3:.1f} ms")
 
     def step():
-        out, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, eos=wl.eos,
+        out, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.type_spec, eos=wl.eos,
                                max_tokens=wl.max_tokens, prefix=None if row_prefix else root,
                                row_prefix=row_prefix, max_batch_tokens=args.batch_tokens,
                                head_restricted=args.head_restricted)

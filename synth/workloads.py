@@ -253,6 +253,12 @@ class Workload:
     def n_rows(self) -> int:
         return len(self.offsets) - 1
 
+    @property
+    def type_spec(self):
+        """What the output type is given by: the automaton for
+        KIND_AUTOMATON, otherwise the allowed token list."""
+        return self.automaton if self.kind == KIND_AUTOMATON else self.allowed
+
     def suffix(self, r: int) -> np.ndarray:
         return self.tokens[self.offsets[r]:self.offsets[r + 1]]
 

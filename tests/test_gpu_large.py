@@ -15,7 +15,7 @@ import torch
 
 from oracle import OracleLM
 from synth import SHAPES, make_weights, make_workload
-from tests.parity import assert_typed, compare
+from tests.parity import assert_automaton, assert_typed, compare
 
 pytestmark = pytest.mark.gpu
 
@@ -122,6 +122,31 @@ def test_filter_8b_restricted_head(m8b):
     ref = orc.eval_workload(sub, keep_logits=True)
     st = compare(ref, out, dbg, "filter_8b restricted", cols=wl.allowed)
     _log("filter_8b restricted", st)
+    ctx.release_prefix(pre)
+
+
+def test_options_8b_sampled_rows(m8b, L):
+    """24 multi-token options (a token trie, up to 3 tokens) over the whole
+    8B-shape table, then sampled rows against the oracle."""
+    w, ctx, orc = m8b
+    wl = make_workload("options_8b")
+    pre = ctx.set_prefix(wl.prefix)
+    kw = dict(eos=wl.eos, max_tokens=wl.max_tokens, prefix=pre)
+    _log(f"options_8b: full table ({wl.n_rows} rows)")
+    full, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.automaton, **kw)
+    assert_automaton(full, wl.automaton, wl.eos, wl.max_tokens)
+    sample = _sample(wl, 5, 7)
+    sub = wl.subset(sample)
+    out, dbg = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.automaton, debug_logits=True,
+                             **kw)
+    _same_rows(full, out, sample, "options_8b")
+    _log(f"options_8b: oracle on {len(sample)} rows")
+    ref = orc.eval_workload(sub, keep_logits=True)
+    forced = orc.eval_workload(sub, keep_logits=True,
+                               forced=[out["tokens"][r][: out["n_tokens"][r]]
+                                       for r in range(len(sample))])
+    st = compare(ref, out, dbg, "options_8b", orc_forced=forced)
+    _log("options_8b", st)
     ctx.release_prefix(pre)
 
 
