@@ -267,6 +267,9 @@ def main():
     ap.add_argument("--workload", default="filter_8b")
     ap.add_argument("--rows", type=int, default=None, help="truncate the table")
     ap.add_argument("--batch-tokens", type=int, default=0)
+    ap.add_argument("--limit", type=int, default=0,
+                    help="LIMIT k early exit: stop once k rows have value --limit-value")
+    ap.add_argument("--limit-value", type=int, default=1)
     ap.add_argument("--head-restricted", action="store_true",
                     help="compute only the allowed tokens' logits (logprob_full is NaN)")
     ap.add_argument("--cpu-rows", type=int, default=4)
@@ -334,7 +337,8 @@ def main():
         out, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.type_spec, eos=wl.eos,
                                max_tokens=wl.max_tokens, prefix=None if row_prefix else root,
                                row_prefix=row_prefix, max_batch_tokens=args.batch_tokens,
-                               head_restricted=args.head_restricted)
+                               head_restricted=args.head_restricted, limit=args.limit,
+                               limit_value=args.limit_value)
         return out
 
     for i in range(args.warmup):
@@ -354,6 +358,11 @@ def main():
     ms_step = elapsed * 1e3 / args.steps
     rows = wl.n_rows
     n_tok = wl.n_suffix_tokens
+    if args.limit:
+        # a LIMIT query: the rows it evaluated (the rest were skipped)
+        rows = int(np.sum(out["n_tokens"] > 0))
+        n_tok = int(sum(wl.offsets[r + 1] - wl.offsets[r] for r in range(wl.n_rows)
+                        if out["n_tokens"][r] > 0))
     value = rows / (ms_step * 1e-3)
     rep, n_unique = L.lmop_dedup_rows(wl.tokens, wl.offsets,
                                       None if wl.row_child is None else wl.row_child)
@@ -368,6 +377,8 @@ def main():
                    "suffix_tokens": n_tok, "suffix_tokens_per_s": n_tok / (ms_step * 1e-3),
                    "batch_tokens": args.batch_tokens or 16384, "parallelism": "single GPU",
                    "head": "restricted" if args.head_restricted else "full vocabulary"},
+        **({"limit": {"k": args.limit, "value": args.limit_value, "rows_in_table": wl.n_rows,
+                      "rows_evaluated": rows, "ms_per_query": ms_step}} if args.limit else {}),
         "roofline": gemm_roofline(stats),
         "head_roofline": head_roofline(stats),
         "pass_rooflines": pass_rooflines(stats),

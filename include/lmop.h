@@ -197,9 +197,20 @@ typedef struct {
   int32_t max_batch_tokens; /* suffix tokens per device batch; 0 = library default (16384),
                                larger values are capped at 2^21                           */
   float* debug_logits;      /* NULL or host fp32 [n_rows][max_steps][vocab]: the logits of
-                               each step (max_steps = max_tokens for INT, else 1); steps a
-                               row did not take are NaN                                   */
+                               each step (max_steps = max_tokens for INT and AUTOMATON,
+                               else 1); steps a row did not take are NaN                  */
+  int32_t limit;            /* early exit for LIMIT queries (Sec. 2.4): 0 = evaluate every
+                               row; k > 0 = rows are evaluated in table order and the call
+                               stops once k rows have value == limit_value (see below)    */
+  int64_t limit_value;      /* the value a row must have to count toward `limit`          */
 } lmop_eval_opts;
+
+/* With limit = k > 0 every row up to and including the k-th row (in table
+ * order) whose value is limit_value is evaluated, as without a limit, bit
+ * for bit; rows after it may be skipped.  A skipped row gets value -1,
+ * n_tokens 0, NaN log-probabilities, tokens -1 (and NaN debug logits).  If
+ * fewer than k rows qualify, every row is evaluated.  Rows are then batched
+ * in table order, not grouped by prefix. */
 
 /* Evaluates the LM function on every row: row r's sequence is
  * prefix(r) ++ tokens[offsets[r] .. offsets[r+1]), where prefix(r) =

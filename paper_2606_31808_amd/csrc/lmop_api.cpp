@@ -1307,6 +1307,9 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
     return fail(ctx, LMOP_ERR_INVALID_ARG, "unknown flags 0x%x", (unsigned)flags);
   if (opts && opts->max_batch_tokens < 0)
     return fail(ctx, LMOP_ERR_INVALID_ARG, "max_batch_tokens < 0");
+  const int limit = opts ? opts->limit : 0;
+  const int64_t limit_value = opts ? opts->limit_value : 0;
+  if (limit < 0) return fail(ctx, LMOP_ERR_INVALID_ARG, "limit < 0");
   if (ctx->host_only)
     return fail(ctx, LMOP_ERR_UNSUPPORTED, "host-only ctx: arguments are valid, no device to run");
 
@@ -1331,11 +1334,13 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
   uniq.reserve(n_unique);
   for (int r = 0; r < n_rows; ++r)
     if (rep[r] == r) uniq.push_back(r);
-  // group rows of one prefix together (attention reads that prefix's KV)
-  std::stable_sort(uniq.begin(), uniq.end(), [&](int a, int b) {
-    const int64_t ia = pf[a] ? pf[a]->id : 0, ib = pf[b] ? pf[b]->id : 0;
-    return ia < ib;
-  });
+  // group rows of one prefix together (attention reads that prefix's KV);
+  // with a limit the rows stay in table order
+  if (limit == 0)
+    std::stable_sort(uniq.begin(), uniq.end(), [&](int a, int b) {
+      const int64_t ia = pf[a] ? pf[a]->id : 0, ib = pf[b] ? pf[b]->id : 0;
+      return ia < ib;
+    });
 
   // allowed-token map: sel[token] = position in the allowed list (INT: EOS
   // last).  An automaton's list is every edge token in order of first
@@ -1670,6 +1675,17 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
   // further steps) is enqueued before this one is collected, so the GPU does
   // not wait while the host packs and reads back.  A logit dump reuses one
   // device buffer, so then each batch is collected before the next starts.
+  // Early exit (limit > 0): once a batch (or a decode group) is final, every
+  // table row before the first row not yet evaluated has its value; count
+  // the qualifying ones in table order and stop at `limit`.
+  std::vector<char> done(n_rows, 0);  // per representative row: evaluated
+  int scan = 0, n_hits = 0;
+  auto reached_limit = [&](size_t u_next) {
+    const int upto = u_next < uniq.size() ? uniq[u_next] : n_rows;
+    for (; scan < upto; ++scan)
+      if (res[rep[scan]].value == limit_value) ++n_hits;
+    return n_hits >= limit;
+  };
   InFlight fl[2];
   int next_b = 0;
   for (int bi = 0; bi < n_batches; ++bi) {
@@ -1678,10 +1694,22 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
     if (!dbg && next_b == bi + 1 && bi + 1 < n_batches && (dec == 0 || !last_of_group))
       LMOP_TRY(enqueue(next_b++, fl[(bi + 1) & 1]));
     LMOP_TRY(collect(fl[bi & 1]));
+    for (size_t u = batches[bi].first; u < batches[bi].second; ++u) done[uniq[u]] = 1;
     if (dec > 0 && last_of_group) LMOP_TRY(decode(group_of[bi]));
+    if (limit > 0 && (dec == 0 || last_of_group) && reached_limit(batches[bi].second)) break;
   }
   LMOP_TRY(sync(ctx));
+  lmop_result skipped;
+  skipped.value = -1;
+  skipped.logprob = skipped.logprob_full = NAN;
+  skipped.n_tokens = 0;
+  for (int q = 0; q < 8; ++q) skipped.tokens[q] = -1;
   for (int r = 0; r < n_rows; ++r) {
+    if (!done[rep[r]]) {
+      out[r] = skipped;
+      if (dbg) std::fill(dbg + (size_t)r * steps * V, dbg + (size_t)(r + 1) * steps * V, NAN);
+      continue;
+    }
     out[r] = res[rep[r]];
     if (dbg && rep[r] != r)
       std::memcpy(dbg + (size_t)r * steps * V, dbg + (size_t)rep[r] * steps * V,

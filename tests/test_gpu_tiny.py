@@ -319,6 +319,60 @@ def test_tiny_automaton_equals_enum_and_int(tiny, L):
     ctx.release_prefix(pre)
 
 
+def _check_limit(full, out, k, v, label):
+    """Rows up to the k-th with value v equal the full evaluation bit for bit;
+    later rows are either evaluated (and equal) or marked skipped."""
+    hits = np.nonzero(full["value"] == v)[0]
+    last = int(hits[k - 1]) if len(hits) >= k else len(full) - 1
+    assert out[: last + 1].tobytes() == full[: last + 1].tobytes(), label
+    for r in range(last + 1, len(full)):
+        if out["n_tokens"][r] == 0:
+            assert out["value"][r] == -1 and np.isnan(out["logprob"][r]), label
+            assert np.all(out["tokens"][r] == -1), label
+        else:
+            assert out[r].tobytes() == full[r].tobytes(), label
+    return int(np.sum(out["n_tokens"] > 0))
+
+
+def test_tiny_limit_early_exit(tiny, L):
+    """LIMIT k: evaluation stops once k rows (in table order) have the wanted
+    value; every row up to the k-th such row is exactly as without a limit."""
+    w, orc, ctx = tiny
+    wl = make_workload("filter_tiny")
+    pre = ctx.set_prefix(wl.prefix)
+    # duplicates (dedup) and small batches, so the stop comes early
+    idx = np.array(list(range(64)) + [3, 3, 10, 5, 63, 0])
+    sub = wl.subset(idx)
+    full, _ = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, prefix=pre,
+                            max_batch_tokens=64)
+    v = int(np.bincount(full["value"]).argmax())
+    for k in (1, 4, 9):
+        out, _ = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, prefix=pre,
+                               max_batch_tokens=64, limit=k, limit_value=v)
+        n_eval = _check_limit(full, out, k, v, f"limit {k}")
+        _log(f"limit {k}: {n_eval} of {len(idx)} rows evaluated")
+        assert n_eval < len(idx)
+    # more than the table holds: every row is evaluated
+    out, _ = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, prefix=pre,
+                           max_batch_tokens=64, limit=len(idx) + 1, limit_value=v)
+    assert out.tobytes() == full.tobytes()
+    # with the logit dump, skipped rows' logits are NaN
+    out, dbg = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, prefix=pre,
+                             max_batch_tokens=64, limit=2, limit_value=v, debug_logits=True)
+    skipped = out["n_tokens"] == 0
+    assert skipped.any() and np.all(np.isnan(dbg[skipped]))
+    # integer outputs: the stop waits for each decode group's last step
+    digits = np.random.default_rng(3).choice(TINY.vocab, 10, replace=False).astype(np.int32)
+    eos = int(next(t for t in range(TINY.vocab) if t not in digits))
+    fi, _ = ctx.eval_rows(sub.tokens, sub.offsets, KIND_INT, digits, eos=eos, max_tokens=3,
+                          prefix=pre, max_batch_tokens=64)
+    vi = int(np.bincount(fi["value"]).argmax())
+    oi, _ = ctx.eval_rows(sub.tokens, sub.offsets, KIND_INT, digits, eos=eos, max_tokens=3,
+                          prefix=pre, max_batch_tokens=64, limit=2, limit_value=vi)
+    _check_limit(fi, oi, 2, vi, "int limit")
+    ctx.release_prefix(pre)
+
+
 def test_tiny_restricted_head(tiny, L):
     """Restricted head: only the allowed tokens' logits are computed; typed
     outputs and allowed-set log-probabilities match the oracle and the full

@@ -203,6 +203,14 @@ def test_dedup_rejects_bad_csr():
     assert nu == 0 and len(rep) == 0
 
 
+def test_limit_validation(tiny_w):
+    ctx = _host_ctx()
+    ctx.load_weights(tiny_w)
+    ok = dict(kind=L.LMOP_BOOL, allowed=[3, 4])
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [1, 2, 3], [0, 2, 3], limit=-1, **ok)
+    _expect(L.LMOP_ERR_UNSUPPORTED, ctx.eval_rows, [1, 2, 3], [0, 2, 3], limit=1, **ok)
+
+
 def test_automaton_validation(tiny_w):
     from synth import Automaton
     ctx = _host_ctx()
