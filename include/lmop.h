@@ -203,14 +203,19 @@ typedef struct {
                                row; k > 0 = rows are evaluated in table order and the call
                                stops once k rows have value == limit_value (see below)    */
   int64_t limit_value;      /* the value a row must have to count toward `limit`          */
+  const uint8_t* row_mask;  /* NULL or host [n_rows]: cascade filtering (Sec. 2.4) - only
+                               rows with row_mask[r] != 0 are evaluated (e.g. the rows an
+                               earlier predicate kept); the others are skipped           */
 } lmop_eval_opts;
 
 /* With limit = k > 0 every row up to and including the k-th row (in table
  * order) whose value is limit_value is evaluated, as without a limit, bit
- * for bit; rows after it may be skipped.  A skipped row gets value -1,
- * n_tokens 0, NaN log-probabilities, tokens -1 (and NaN debug logits).  If
- * fewer than k rows qualify, every row is evaluated.  Rows are then batched
- * in table order, not grouped by prefix. */
+ * for bit; rows after it may be skipped.  If fewer than k rows qualify,
+ * every row is evaluated.  Rows are then batched in table order, not
+ * grouped by prefix.  A skipped row (by the limit or the row mask) gets
+ * value -1, n_tokens 0, NaN log-probabilities, tokens -1 (and NaN debug
+ * logits).  An evaluated row's result does not depend on which other rows
+ * are evaluated. */
 
 /* Evaluates the LM function on every row: row r's sequence is
  * prefix(r) ++ tokens[offsets[r] .. offsets[r+1]), where prefix(r) =

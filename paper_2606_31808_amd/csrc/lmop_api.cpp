@@ -10,6 +10,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdint>
 #include <cstring>
 #include <map>
 #include <memory>
@@ -1319,7 +1320,10 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
   float* dbg = opts ? opts->debug_logits : nullptr;
   const int V = cf.vocab;
 
-  // early deduplication: one evaluation per distinct (prefix, suffix)
+  // early deduplication: one evaluation per distinct (prefix, suffix); a
+  // row the mask leaves out gets a key of its own, so it represents no
+  // other row, and is not evaluated
+  const uint8_t* row_mask = opts ? opts->row_mask : nullptr;
   std::vector<int32_t> rep(n_rows);
   int32_t n_unique = 0;
   if (flags & LMOP_NO_DEDUP) {
@@ -1327,13 +1331,14 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
     n_unique = n_rows;
   } else {
     std::vector<int64_t> keys(n_rows);
-    for (int r = 0; r < n_rows; ++r) keys[r] = pf[r] ? pf[r]->id : 0;
+    for (int r = 0; r < n_rows; ++r)
+      keys[r] = row_mask && !row_mask[r] ? INT64_MIN + r : (pf[r] ? pf[r]->id : 0);
     dedup(tokens, offsets, n_rows, keys.data(), rep.data(), &n_unique);
   }
   std::vector<int32_t> uniq;
   uniq.reserve(n_unique);
   for (int r = 0; r < n_rows; ++r)
-    if (rep[r] == r) uniq.push_back(r);
+    if (rep[r] == r && (!row_mask || row_mask[r])) uniq.push_back(r);
   // group rows of one prefix together (attention reads that prefix's KV);
   // with a limit the rows stay in table order
   if (limit == 0)
@@ -1683,7 +1688,7 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
   auto reached_limit = [&](size_t u_next) {
     const int upto = u_next < uniq.size() ? uniq[u_next] : n_rows;
     for (; scan < upto; ++scan)
-      if (res[rep[scan]].value == limit_value) ++n_hits;
+      if (done[rep[scan]] && res[rep[scan]].value == limit_value) ++n_hits;
     return n_hits >= limit;
   };
   InFlight fl[2];

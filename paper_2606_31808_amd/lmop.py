@@ -74,7 +74,7 @@ class lmop_result(C.Structure):
 class lmop_eval_opts(C.Structure):
     _fields_ = [("flags", C.c_uint32), ("max_batch_tokens", C.c_int32),
                 ("debug_logits", C.POINTER(C.c_float)), ("limit", C.c_int32),
-                ("limit_value", C.c_int64)]
+                ("limit_value", C.c_int64), ("row_mask", C.POINTER(C.c_uint8))]
 
 
 class lmop_kernel_stat(C.Structure):
@@ -228,7 +228,7 @@ def lmop_prefix_length(prefix) -> int:
 def lmop_eval_rows(ctx, tokens, offsets, kind: int, allowed: Sequence[int], eos: int = -1,
                    max_tokens: int = 1, prefix=None, row_prefix=None, flags: int = 0,
                    max_batch_tokens: int = 0, debug_logits: bool = False, vocab: int = 0,
-                   limit: int = 0, limit_value: int = 1):
+                   limit: int = 0, limit_value: int = 1, row_mask=None):
     """Returns a structured numpy array of lmop_result (value, logprob, logprob_full,
     n_tokens, tokens) and, with debug_logits, fp32 logits [n_rows][steps][vocab].
     For LMOP_AUTOMATON, `allowed` is an object with n_states, edge_offset,
@@ -251,7 +251,13 @@ def lmop_eval_rows(ctx, tokens, offsets, kind: int, allowed: Sequence[int], eos:
     out = np.zeros(max(n, 0), dtype=RESULT_DTYPE)
     steps = max_tokens if kind in (LMOP_INT, LMOP_AUTOMATON) else 1
     dbg = None
-    opts = lmop_eval_opts(flags, max_batch_tokens, None, int(limit), int(limit_value))
+    opts = lmop_eval_opts(flags, max_batch_tokens, None, int(limit), int(limit_value), None)
+    if row_mask is not None:
+        mk = np.ascontiguousarray(np.asarray(row_mask, dtype=bool).astype(np.uint8))
+        if len(mk) != n:
+            raise ValueError("row_mask needs one entry per row")
+        keep.append(mk)
+        opts.row_mask = _ptr(mk, C.c_uint8)
     if debug_logits:
         if vocab <= 0:
             raise ValueError("debug_logits needs vocab")
@@ -341,11 +347,11 @@ class Context:
 
     def eval_rows(self, tokens, offsets, kind, allowed, eos=-1, max_tokens=1, prefix=None,
                   row_prefix=None, no_dedup=False, max_batch_tokens=0, debug_logits=False,
-                  head_restricted=False, limit=0, limit_value=1):
+                  head_restricted=False, limit=0, limit_value=1, row_mask=None):
         flags = (LMOP_NO_DEDUP if no_dedup else 0) | (LMOP_HEAD_RESTRICTED if head_restricted else 0)
         return lmop_eval_rows(self.ctx, tokens, offsets, kind, allowed, eos, max_tokens, prefix,
                               row_prefix, flags, max_batch_tokens, debug_logits, self.vocab,
-                              limit, limit_value)
+                              limit, limit_value, row_mask)
 
     def set_profiling(self, on: bool):
         lmop_set_profiling(self.ctx, on)

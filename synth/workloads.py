@@ -309,6 +309,8 @@ def make_workload(name: str, seed: int = 7, n_rows: Optional[int] = None) -> Wor
                   all 40,000 pairs left-major; bool; one child prefix per left value
     options_tiny  as filter_tiny, output one of 24 options of 1..3 tokens (a token trie)
     options_8b    as filter_8b, output one of 24 options of 1..3 tokens (a token trie)
+    qa_tiny       LLMQA: tiny decoder, 2 prompts of 96 + 1,500 tokens, one of 24 options
+    qa_8b         LLMQA: 8B shape, one prompt of 256 + 8,192 tokens, one of 24 options
     `n_rows` truncates the table to its first rows (same draws otherwise).
     """
     cfg = WORKLOADS[name]
@@ -353,6 +355,8 @@ def make_workload(name: str, seed: int = 7, n_rows: Optional[int] = None) -> Wor
         n = cfg["rows"]
         if cfg["len"][0] == "uniform":
             lens = rng.integers(cfg["len"][1], cfg["len"][2] + 1, size=n)
+        elif cfg["len"][0] == "fixed":
+            lens = np.full(n, cfg["len"][1], dtype=np.int64)
         else:
             lens = _lognormal_lengths(rng, n, cfg["len"][1], cfg["len"][2], cfg["len"][3])
         parts = [rng.integers(0, V, size=int(s)).astype(np.int32) for s in lens]
@@ -382,4 +386,9 @@ WORKLOADS = {
                          kind=KIND_AUTOMATON, n_allowed=24, max_tokens=3),
     "options_8b": dict(id=7, shape="8b", rows=10000, prefix=512, len=("lognormal", 60, 8, 512),
                        kind=KIND_AUTOMATON, n_allowed=24, max_tokens=3),
+    # LLMQA (Sec. 2.3.1): one long prompt holding a whole subset of the data
+    "qa_tiny": dict(id=8, shape="tiny", rows=2, prefix=96, len=("fixed", 1500),
+                    kind=KIND_AUTOMATON, n_allowed=24, max_tokens=3),
+    "qa_8b": dict(id=9, shape="8b", rows=1, prefix=256, len=("fixed", 8192),
+                  kind=KIND_AUTOMATON, n_allowed=24, max_tokens=3),
 }

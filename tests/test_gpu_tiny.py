@@ -373,6 +373,64 @@ def test_tiny_limit_early_exit(tiny, L):
     ctx.release_prefix(pre)
 
 
+def test_tiny_llmqa_long_prompt(tiny, L):
+    """LLMQA (one prompt holding a whole data subset): two 1,596-token
+    prompts, each one row, against the oracle; one row per batch (a budget
+    below the row's length) gives the same bits."""
+    w, orc, ctx = tiny
+    wl = make_workload("qa_tiny")
+    pre = ctx.set_prefix(wl.prefix)
+    kw = dict(eos=wl.eos, max_tokens=wl.max_tokens, prefix=pre, debug_logits=True)
+    _log("llmqa: eval")
+    out, dbg = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.automaton, **kw)
+    assert_automaton(out, wl.automaton, wl.eos, wl.max_tokens)
+    ref = orc.eval_workload(wl, keep_logits=True)
+    forced = orc.eval_workload(wl, keep_logits=True,
+                               forced=[out["tokens"][r][: out["n_tokens"][r]]
+                                       for r in range(wl.n_rows)])
+    _log("llmqa", compare(ref, out, dbg, "llmqa", orc_forced=forced))
+    o1, d1 = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.automaton, max_batch_tokens=700,
+                           **kw)
+    assert o1.tobytes() == out.tobytes() and np.array_equal(d1, dbg, equal_nan=True)
+    ctx.release_prefix(pre)
+
+
+def test_tiny_cascade_row_mask(tiny, L):
+    """Cascade filtering: a second predicate evaluated only on the rows the
+    first one kept equals that predicate on those rows alone, bit for bit;
+    the other rows are skipped (also with duplicates and a LIMIT)."""
+    w, orc, ctx = tiny
+    wl = make_workload("filter_tiny")
+    pre = ctx.set_prefix(wl.prefix)
+    idx = np.array(list(range(64)) + [3, 3, 10, 5, 63, 0])
+    sub = wl.subset(idx)
+    first, _ = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, prefix=pre)
+    keep = first["value"] == 1
+    assert 0 < keep.sum() < len(idx)
+    opts2 = np.random.default_rng(41).choice(TINY.vocab, 6, replace=False).astype(np.int32)
+    second, d2 = ctx.eval_rows(sub.tokens, sub.offsets, KIND_ENUM, opts2, prefix=pre,
+                               row_mask=keep, debug_logits=True)
+    alone = sub.subset(np.nonzero(keep)[0])
+    ref, dref = ctx.eval_rows(alone.tokens, alone.offsets, KIND_ENUM, opts2, prefix=pre,
+                              debug_logits=True)
+    assert second[keep].tobytes() == ref.tobytes()
+    assert np.array_equal(d2[keep], dref)
+    sk = second[~keep]
+    assert np.all(sk["value"] == -1) and np.all(sk["n_tokens"] == 0)
+    assert np.all(np.isnan(sk["logprob"])) and np.all(np.isnan(d2[~keep]))
+    # with a limit: the mask's rows in table order, stopping at the k-th hit
+    v = int(np.bincount(ref["value"]).argmax())
+    lim, _ = ctx.eval_rows(sub.tokens, sub.offsets, KIND_ENUM, opts2, prefix=pre, row_mask=keep,
+                           limit=2, limit_value=v, max_batch_tokens=64)
+    kept = np.nonzero(keep)[0]
+    hits = kept[second["value"][kept] == v]
+    stop = int(hits[1]) if len(hits) >= 2 else len(idx) - 1
+    head = [r for r in kept if r <= stop]
+    assert lim[head].tobytes() == second[head].tobytes()
+    assert np.all(lim["n_tokens"][~keep] == 0)
+    ctx.release_prefix(pre)
+
+
 def test_tiny_restricted_head(tiny, L):
     """Restricted head: only the allowed tokens' logits are computed; typed
     outputs and allowed-set log-probabilities match the oracle and the full
