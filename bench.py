@@ -270,6 +270,10 @@ def main():
     ap.add_argument("--limit", type=int, default=0,
                     help="LIMIT k early exit: stop once k rows have value --limit-value")
     ap.add_argument("--limit-value", type=int, default=1)
+    ap.add_argument("--cascade", action="store_true",
+                    help="cascade filtering: a bool predicate first, the workload on its survivors")
+    ap.add_argument("--cascade-model", default="",
+                    help="model shape of the cascade's first predicate (default: the workload's)")
     ap.add_argument("--head-restricted", action="store_true",
                     help="compute only the allowed tokens' logits (logprob_full is NaN)")
     ap.add_argument("--cpu-rows", type=int, default=4)
@@ -311,6 +315,8 @@ def main():
     from synth import make_weights, make_workload
 
     wl = make_workload(args.workload, n_rows=args.rows)
+    # the first predicate of a cascade: a yes/no choice between two seeded tokens
+    wl.cascade_allowed = np.random.default_rng(99).choice(wl.shape.vocab, 2, replace=False)
     shape = wl.shape
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev).cuda_stream
@@ -319,7 +325,12 @@ def main():
     w = make_weights(shape, seed=1234, device=dev)
     torch.cuda.synchronize()
     log(f"[bench] weights {time.perf_counter() - t0:.1f} s; loading into the library")
-    ctx = L.Context(shape, device=0, stream=stream)
+    # room for the longest sequence (LLMQA prompts run past the default 4,096)
+    longest = len(wl.prefix) + int(np.diff(wl.offsets).max()) + wl.max_tokens
+    if wl.children is not None:
+        longest += max(len(c) for c in wl.children)
+    max_seq = 0 if longest <= 4096 else -(-longest // 1024) * 1024
+    ctx = L.Context(shape, device=0, stream=stream, max_seq=max_seq)
     t0 = time.perf_counter()
     ctx.load_weights(w)
     t_load = time.perf_counter() - t0
@@ -333,12 +344,40 @@ def main():
     t_prefix = time.perf_counter() - t0
     log(f"[bench] load {t_load:.2f} s, prefix {t_prefix * 1e3:.1f} ms")
 
+    cascade = {}
+    first_ctx, first_root = ctx, root
+    if args.cascade and args.cascade_model:
+        # the first predicate on a smaller model of the same vocabulary
+        from synth import SHAPES
+        s1 = SHAPES[args.cascade_model]
+        w1 = make_weights(s1, seed=4321, device=dev)
+        first_ctx = L.Context(s1, device=0, stream=stream, max_seq=max_seq)
+        first_ctx.load_weights(w1)
+        del w1
+        torch.cuda.empty_cache()
+        first_root = first_ctx.set_prefix(wl.prefix)
+        if row_prefix:
+            raise SystemExit("--cascade-model supports tables without child prefixes")
+
     def step():
+        mask = None
+        if args.cascade:
+            # cascade filtering: a yes/no predicate on every row first, then
+            # the workload's own predicate on the rows it kept
+            t0 = time.perf_counter()
+            first, _ = first_ctx.eval_rows(wl.tokens, wl.offsets, 0, wl.cascade_allowed,
+                                           prefix=None if row_prefix else first_root,
+                                           row_prefix=row_prefix,
+                                           max_batch_tokens=args.batch_tokens)
+            mask = first["value"] == 1
+            cascade.update(first_ms=(time.perf_counter() - t0) * 1e3, kept=int(mask.sum()))
+        t0 = time.perf_counter()
         out, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.type_spec, eos=wl.eos,
                                max_tokens=wl.max_tokens, prefix=None if row_prefix else root,
                                row_prefix=row_prefix, max_batch_tokens=args.batch_tokens,
                                head_restricted=args.head_restricted, limit=args.limit,
-                               limit_value=args.limit_value)
+                               limit_value=args.limit_value, row_mask=mask)
+        cascade.update(second_ms=(time.perf_counter() - t0) * 1e3)
         return out
 
     for i in range(args.warmup):
@@ -379,6 +418,10 @@ def main():
                    "head": "restricted" if args.head_restricted else "full vocabulary"},
         **({"limit": {"k": args.limit, "value": args.limit_value, "rows_in_table": wl.n_rows,
                       "rows_evaluated": rows, "ms_per_query": ms_step}} if args.limit else {}),
+        **({"cascade": {"first_model": args.cascade_model or shape.name,
+                        "rows": wl.n_rows, "kept_by_first": cascade.get("kept"),
+                        "first_ms": cascade.get("first_ms"),
+                        "second_ms": cascade.get("second_ms")}} if args.cascade else {}),
         "roofline": gemm_roofline(stats),
         "head_roofline": head_roofline(stats),
         "pass_rooflines": pass_rooflines(stats),
