@@ -95,6 +95,32 @@ def dequant(qweight: np.ndarray, scales: np.ndarray, k: int, dtype=np.float64) -
     return out[:, :k] if k != kp else out
 
 
+def decode_e4m3(codes: np.ndarray) -> np.ndarray:
+    """Value of each FP8 code in the OCP 8-bit floating-point format E4M3
+    (the "fn" variant: no infinities, S.1111.111 is NaN, largest finite
+    448): sign bit, 4 exponent bits with bias 7, 3 mantissa bits; exponent
+    field 0 holds the subnormals m/8 * 2^-6."""
+    c = np.arange(256)
+    sign = np.where(c & 0x80, -1.0, 1.0)
+    e = (c >> 3) & 0xF
+    m = c & 7
+    mag = np.where(e == 0, (m / 8.0) * 2.0 ** -6, (1.0 + m / 8.0) * np.exp2(e - 7.0))
+    table = sign * mag
+    table[(c & 0x7F) == 0x7F] = np.nan
+    return table[np.asarray(codes, dtype=np.int64)]
+
+
+def dequant_fp8(codes: np.ndarray, scales: np.ndarray, dtype=np.float64) -> np.ndarray:
+    """W'[n, j] = e4m3(q[n, j]) * s[n] (FP8 weights with one scale per output
+    channel, the layout of FP8 checkpoints).  An E4M3 value has 4 significant
+    bits, so with an fp32 scale the product is exact in fp64."""
+    codes = np.asarray(codes)
+    scales = np.asarray(scales, dtype=np.float64)
+    assert codes.ndim == 2 and scales.shape == (codes.shape[0],)
+    out = decode_e4m3(codes) * scales[:, None]
+    return out.astype(dtype)
+
+
 def rms_norm(x: np.ndarray, gamma: np.ndarray, eps: float) -> np.ndarray:
     """x / sqrt(mean(x^2) + eps) * gamma over the last axis."""
     ms = np.mean(x * x, axis=-1, keepdims=True)
@@ -261,7 +287,8 @@ class OracleLM:
             mats = {}
             for name in ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down"):
                 m = getattr(l, name)
-                mats[name] = (_np(m.qweight), _np(m.scales), int(m.n), int(m.k))
+                mats[name] = (_np(m.qweight), _np(m.scales), int(m.n), int(m.k),
+                              getattr(m, "fmt", "int4_g32"))
             self.layers.append((_np(l.attn_norm), _np(l.mlp_norm), mats))
         n_params = sum(m[2] * m[3] for _, _, mats in self.layers for m in mats.values())
         if cache_dequant is None:
@@ -274,7 +301,9 @@ class OracleLM:
         if self._cache is not None and l in self._cache:
             return self._cache[l]
         g1, g2, mats = self.layers[l]
-        w = {name: dequant(q, s, k, self.dtype) for name, (q, s, n, k) in mats.items()}
+        w = {name: (dequant_fp8(q, s, self.dtype) if fmt == "fp8_e4m3"
+                    else dequant(q, s, k, self.dtype))
+             for name, (q, s, n, k, fmt) in mats.items()}
         out = (g1, g2, w)
         if self._cache is not None:
             self._cache[l] = out

@@ -15,6 +15,7 @@ from .workloads import (  # noqa: F401
     make_weights,
     make_workload,
     quantize_int4_g32,
+    quantize_fp8_e4m3,
     WORKLOADS,
     Automaton,
     option_trie,

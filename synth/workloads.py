@@ -59,10 +59,11 @@ SHAPES = {
 
 @dataclasses.dataclass
 class QMat:
-    qweight: torch.Tensor  # uint8 [N][Kp/2]
-    scales: torch.Tensor   # float16 [N][Kp/32]
+    qweight: torch.Tensor  # int4_g32: uint8 [N][Kp/2]; fp8_e4m3: uint8 codes [N][K]
+    scales: torch.Tensor   # int4_g32: float16 [N][Kp/32]; fp8_e4m3: float32 [N]
     n: int
     k: int
+    fmt: str = "int4_g32"
 
 
 @dataclasses.dataclass
@@ -88,7 +89,7 @@ class Weights:
 
     def to(self, device) -> "Weights":
         def qm(m: QMat) -> QMat:
-            return QMat(m.qweight.to(device), m.scales.to(device), m.n, m.k)
+            return QMat(m.qweight.to(device), m.scales.to(device), m.n, m.k, m.fmt)
         layers = [Layer(l.attn_norm.to(device), l.mlp_norm.to(device), qm(l.wq), qm(l.wk),
                         qm(l.wv), qm(l.wo), qm(l.w_gate), qm(l.w_up), qm(l.w_down))
                   for l in self.layers]
@@ -128,9 +129,23 @@ def quantize_int4_g32(w: torch.Tensor):
     return packed.contiguous(), s.contiguous()
 
 
+def quantize_fp8_e4m3(w: torch.Tensor):
+    """FP8 (OCP e4m3, "fn" variant: max 448, no infinities) with one fp32
+    scale per output channel, the layout of FP8 checkpoints.
+
+    Input generation, not part of the operator: s = max|w| / 448 per row (1
+    if that is 0), q = e4m3(round to nearest even of w / s, clamped to
+    +-448).  Returns (codes uint8 [N][K], scales float32 [N])."""
+    s = w.abs().amax(-1) / 448.0
+    s = torch.where(s == 0, torch.ones_like(s), s)
+    q = (w / s.unsqueeze(-1)).clamp_(-448.0, 448.0).to(torch.float8_e4m3fn)
+    return q.view(torch.uint8).contiguous(), s.float().contiguous()
+
+
 def make_weights(shape: ModelShape, seed: int = 1234, device="cpu", std: float = 0.02,
-                 n_layers: Optional[int] = None) -> Weights:
-    """Random-init weights of `shape`, linear layers quantised to int4 g32.
+                 n_layers: Optional[int] = None, fmt: str = "int4_g32") -> Weights:
+    """Random-init weights of `shape`, linear layers quantised to int4 g32
+    (fmt "int4_g32") or to FP8 e4m3 with per-channel scales ("fp8_e4m3").
 
     Each tensor has its own stream keyed by (seed, shape, layer, tensor), so a
     model with fewer layers is a prefix of the full one.
@@ -143,9 +158,12 @@ def make_weights(shape: ModelShape, seed: int = 1234, device="cpu", std: float =
 
     def qmat(layer: int, tid: int, n: int, k: int) -> QMat:
         w = _normal((n, k), std, _seed(seed, sid, layer, tid), dev)
-        qw, sc = quantize_int4_g32(w)
+        if fmt == "fp8_e4m3":
+            qw, sc = quantize_fp8_e4m3(w)
+        else:
+            qw, sc = quantize_int4_g32(w)
         del w
-        return QMat(qw, sc, n, k)
+        return QMat(qw, sc, n, k, fmt)
 
     emb = _normal((shape.vocab, d), std, _seed(seed, sid, 10_000, 0), dev).to(torch.float16)
     head = _normal((shape.vocab, d), std, _seed(seed, sid, 10_000, 1), dev).to(torch.float16)

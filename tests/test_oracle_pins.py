@@ -12,9 +12,9 @@ import torch
 
 from oracle import (KIND_BOOL, KIND_ENUM, KIND_INT, OracleLM, attention, constrained_pick,
                     decode_nibbles, dequant, rms_norm, rope, silu)
-from oracle.lmop_oracle import KIND_AUTOMATON, automaton_steps
+from oracle.lmop_oracle import KIND_AUTOMATON, automaton_steps, decode_e4m3, dequant_fp8
 from synth import (SHAPES, Automaton, ModelShape, make_weights, make_workload, option_trie,
-                   quantize_int4_g32)
+                   quantize_fp8_e4m3, quantize_int4_g32)
 
 GOLD = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -69,6 +69,59 @@ def test_quant_roundtrip_error_bound_and_requant_identity():
 
 
 # ---------------------------------------------------------------- rmsnorm / silu
+def test_e4m3_hand_values():
+    # sign | exponent (bias 7) | mantissa, OCP E4M3 "fn"
+    hand = {0x38: 1.0, 0x3C: 1.5, 0x40: 2.0, 0x7E: 448.0, 0x08: 2.0 ** -6, 0x01: 2.0 ** -9,
+            0x07: 7 * 2.0 ** -9, 0x00: 0.0, 0xB8: -1.0, 0xFE: -448.0, 0x30: 0.5, 0x77: 240.0}
+    got = decode_e4m3(np.array(list(hand)))
+    assert got.tolist() == list(hand.values())
+    assert np.isnan(decode_e4m3(np.array([0x7F, 0xFF]))).all()
+    assert math.copysign(1.0, float(decode_e4m3(np.array([0x80]))[0])) == -1.0
+
+
+def test_e4m3_decode_matches_torch_for_every_code():
+    codes = torch.arange(256, dtype=torch.int32).to(torch.uint8)
+    ref = codes.view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    ours = decode_e4m3(np.arange(256))
+    assert np.array_equal(np.isnan(ours), np.isnan(ref))
+    ok = ~np.isnan(ref)
+    assert np.array_equal(ours[ok], ref[ok])
+
+
+def test_fp8_quantiser_error_bound_and_requant_identity():
+    g = torch.Generator().manual_seed(5)
+    w = torch.randn(64, 200, generator=g) * 0.02
+    w[3, 7] = 0.0
+    w[5] = 0.0  # an all-zero row takes scale 1
+    q, sc = quantize_fp8_e4m3(w)
+    assert q.dtype == torch.uint8 and sc.shape == (64,) and sc[5] == 1.0
+    deq = dequant_fp8(q.numpy(), sc.numpy())
+    x = w.double().numpy() / sc.double().numpy()[:, None]
+    err = np.abs(deq / sc.double().numpy()[:, None] - x)
+    normal = np.abs(x) >= 2.0 ** -6
+    # round to nearest: half a unit in the last place (3 mantissa bits)
+    assert np.all(err[normal] <= np.abs(x[normal]) * 2.0 ** -4 + 1e-12)
+    assert np.all(err[~normal] <= 2.0 ** -10 + 1e-12)
+    # the largest magnitude of every nonzero row is exactly 448
+    assert np.allclose(np.abs(deq / sc.double().numpy()[:, None]).max(axis=1)[np.arange(64) != 5],
+                       448.0)
+    q2, _ = quantize_fp8_e4m3(torch.from_numpy(deq).float())
+    assert torch.equal(q2, q)
+
+
+def test_fp8_model_prefix_cached_equals_full_forward():
+    w = make_weights(MICRO, seed=13, fmt="fp8_e4m3")
+    assert w.layers[0].wq.fmt == "fp8_e4m3" and w.layers[0].wq.scales.dtype == torch.float32
+    orc = OracleLM(w, MICRO)
+    rng = np.random.default_rng(17)
+    prefix = rng.integers(0, MICRO.vocab, size=9)
+    rows = _rand_rows(rng, 5, 1, 7, MICRO.vocab)
+    res = orc.eval_rows(prefix, rows, KIND_ENUM, np.array([3, 50, 7]), keep_logits=True)
+    for r in range(5):
+        z = orc.logits(orc.forward_sequence(np.concatenate([prefix, rows[r]]))[-1])[0]
+        assert np.allclose(res["logits"][r][0], z, atol=1e-11)
+
+
 def test_rmsnorm_hand_value_and_unit_rms():
     y = rms_norm(np.array([3.0, 4.0]), np.ones(2), 0.0)
     assert np.allclose(y, [3 / math.sqrt(12.5), 4 / math.sqrt(12.5)], rtol=0, atol=1e-15)
