@@ -71,14 +71,24 @@ void lmop_destroy(lmop_ctx* ctx); /* frees everything, including live prefixes; 
 const char* lmop_last_error(const lmop_ctx* ctx);
 const char* lmop_status_string(lmop_status s);
 
-/* One W4A16 linear map y = x W^T with W [n][k]:
+/* Formats of the linear maps' weights (lmop_weights.format). */
+#define LMOP_W_INT4_G32 0u /* W4A16: int4 codes, one fp16 scale per 32 input features (Sec. 3.2) */
+#define LMOP_W_FP8_E4M3 1u /* FP8 checkpoints: OCP E4M3 codes, one fp32 scale per output row   */
+
+/* One linear map y = x W^T with W [n][k].
+ * LMOP_W_INT4_G32:
  *   qweight uint8 [n][kp/2], kp = k rounded up to 32: feature j is the low
  *     nibble of byte j/2 when j is even, the high nibble when j is odd; each
  *     nibble is a two's-complement int4 in [-8, 7]; pad features hold 0.
- *   scales  fp16 bit patterns [n][kp/32]: W[r][j] = q[r][j] * scales[r][j/32]. */
+ *   scales  fp16 bit patterns [n][kp/32]: W[r][j] = q[r][j] * scales[r][j/32].
+ * LMOP_W_FP8_E4M3:
+ *   qweight uint8 [n][k]: OCP FP8 E4M3 codes (the "fn" variant: largest 448,
+ *     no infinities; NaN codes are not allowed);
+ *   scales  fp32 [n]: W[r][j] = e4m3(q[r][j]) * scales[r].
+ * Activations stay fp16 in both (weight-only quantisation). */
 typedef struct {
   const uint8_t* qweight;
-  const uint16_t* scales;
+  const void* scales;
   int32_t n, k;
 } lmop_qmat;
 
@@ -99,6 +109,7 @@ typedef struct {
   const lmop_layer* layers;      /* host array [n_layers] (always host memory) */
   int32_t n_layers;
   int32_t on_device; /* 0: the tensor pointers are host memory; 1: device memory on the ctx's device */
+  int32_t format;    /* LMOP_W_INT4_G32 or LMOP_W_FP8_E4M3, for all seven maps of every layer */
 } lmop_weights;
 
 /* Copies the weights to the device and repacks them into the kernels'

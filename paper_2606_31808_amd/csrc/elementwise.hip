@@ -153,6 +153,43 @@ __global__ void repack_kernel(RepackSrc src, const int32_t* __restrict__ colsrc,
   if (g == 0) spack[blk * 64 + c * 4 + f] = scale;
 }
 
+// One item per (64-column block, 32-feature group, half, lane): 16 bytes,
+// the 8 codes of two columns.
+__global__ void repack_fp8_kernel(RepackSrc src, const int32_t* __restrict__ colsrc, int np,
+                                  int kg_n, uint8_t* __restrict__ qpack,
+                                  float* __restrict__ sscale) {
+  const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t total = (size_t)(np / 64) * kg_n * 128;
+  if (item >= total) return;
+  const int lane = item & 63;
+  const int h = (item >> 6) & 1;
+  const size_t blk = item >> 7;  // nb * kg_n + kg
+  const int kg = (int)(blk % kg_n);
+  const int nb = (int)(blk / kg_n);
+  const int g = lane >> 4, c = lane & 15;
+  uint32_t w[4] = {0u, 0u, 0u, 0u};  // code 0 = +0.0
+#pragma unroll
+  for (int ff = 0; ff < 2; ++ff) {
+    const int col = nb * 64 + 16 * (2 * h + ff) + c;
+    const int cs = colsrc[col];
+    float scale = 0.f;
+    if (cs >= 0) {
+      const int si = cs >> 24, r = cs & 0xFFFFFF;
+      const int K = src.kp_src[si];
+      const uint8_t* qr = src.q[si] + (size_t)r * K;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int k = kg * 32 + 8 * g + j;
+        const uint32_t code = k < K ? qr[k] : 0u;
+        w[2 * ff + (j >> 2)] |= code << (8 * (j & 3));
+      }
+      scale = src.sf[si][r];
+    }
+    if (kg == 0 && g == 0) sscale[col] = scale;
+  }
+  *(uint4*)(qpack + item * 16) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
 // --------------------------------------------------------------- restricted head
 // Logits of the allowed tokens only: one workgroup per row, one wave per
 // allowed token at a time; each lane sums 8-feature runs with a stride of
@@ -307,12 +344,22 @@ hipError_t launch_rmsnorm(hipStream_t s, const float* x, int ldx, const float* c
 }
 
 hipError_t launch_repack_w4(hipStream_t s, const RepackSrc& src, const int32_t* colsrc,
-                            PackedW4& dst) {
+                            PackedW& dst) {
   const int kg_n = dst.kp / 32;
   const size_t total = (size_t)(dst.np / 64) * kg_n * 256;
   const int blocks = (int)((total + 255) / 256);
   hipLaunchKernelGGL(repack_kernel, dim3(blocks), dim3(256), 0, s, src, colsrc, dst.np, kg_n,
                      dst.qpack, (f16*)dst.spack);
+  return hipGetLastError();
+}
+
+hipError_t launch_repack_w8(hipStream_t s, const RepackSrc& src, const int32_t* colsrc,
+                            PackedW& dst) {
+  const int kg_n = dst.kp / 32;
+  const size_t total = (size_t)(dst.np / 64) * kg_n * 128;
+  const int blocks = (int)((total + 255) / 256);
+  hipLaunchKernelGGL(repack_fp8_kernel, dim3(blocks), dim3(256), 0, s, src, colsrc, dst.np, kg_n,
+                     (uint8_t*)dst.qpack, dst.sscale);
   return hipGetLastError();
 }
 

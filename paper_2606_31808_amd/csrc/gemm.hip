@@ -1,7 +1,8 @@
 // W4A16 GEMM for gfx950: C = A . deq(W)^T with A fp16 [M][K] (tokens x
 // features), W int4 [N][K] with one fp16 scale per 32 input features, fp32
-// accumulation on MFMA 16x16x32 f16.  The same body with an fp16 weight is
-// the LM head.
+// accumulation on MFMA 16x16x32 f16.  The same body serves FP8 weights (OCP
+// E4M3 codes, one fp32 scale per output column: the FP8 checkpoint layout)
+// and, with an fp16 weight, the LM head.
 //
 // Tiling.  4 waves side by side along N; a wave owns all (16*MI) tokens of
 // the tile and 64 output columns, the workgroup (16*MI) x 256.  K advances
@@ -25,6 +26,12 @@
 // as its B operand, so the accumulator holds C^T: every lane owns 4
 // consecutive output columns of one token, which makes the epilogue's
 // stores 8-byte (fp16) or 16-byte (fp32) vectors.
+//
+// FP8 weights: the tile is 1 KB per 64 columns x 16 features, so a K step
+// holds twice the int4 bytes and the ring has two stages (64 KB, two
+// workgroups per CU).  A lane's 8 codes convert to fp16 exactly with four
+// v_cvt_scalef32_pk_f16_fp8 (every E4M3 value is an fp16 value); the
+// per-column scale multiplies the fp32 accumulator before the epilogue.
 //
 // The LM head (fp16 weight, M = vocabulary, N = tokens) has 4 or 8 waves (8:
 // one LDS tile of the head weight serves up to 512 token rows); its token
@@ -67,6 +74,16 @@ LMOP_DEVICE f16x8 dequant8(uint32_t w, f16 s, uint32_t mask, uint32_t magic) {
   return f16x8{h0.x, h0.y, h1.x, h1.y, h2.x, h2.y, h3.x, h3.y};
 }
 
+// The 8 E4M3 codes of two words (feature order, byte 0 first) as fp16,
+// exactly: every E4M3 value is an fp16 value, so a unit scale changes nothing.
+LMOP_DEVICE f16x8 fp8x8(uint32_t d0, uint32_t d1) {
+  const f16x2 a = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d0, 1.0f, false);
+  const f16x2 b = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d0, 1.0f, true);
+  const f16x2 c = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d1, 1.0f, false);
+  const f16x2 d = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d1, 1.0f, true);
+  return f16x8{a.x, a.y, b.x, b.y, c.x, c.y, d.x, d.y};
+}
+
 LMOP_DEVICE float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
 
 // 16-byte chunk swizzle of a 128-byte LDS row; with it a fragment load (16
@@ -79,7 +96,12 @@ constexpr int BN4 = 256;   // int4 GEMMs: 4 waves x 64 columns
 constexpr int GM = 8;      // token tiles per L2 group
 constexpr int NSTAGE = 3;  // LDS ring depth
 
-template <int MI, bool INT4, int NW_ = 4>
+// weight formats of the kernel's A operand
+constexpr int WF_F16 = 0;   // fp16 (the LM head; its token rows bypass LDS)
+constexpr int WF_INT4 = 1;  // int4, one fp16 scale per 32 features
+constexpr int WF_FP8 = 2;   // OCP E4M3, one fp32 scale per output column
+
+template <int MI, int WF, int NW_ = 4>
 struct Cfg {
   // waves per workgroup, side by side along N (64 columns each): 4 for the
   // int4 GEMMs; 4 or 8 for the LM head (8: up to 512 token rows share each
@@ -90,14 +112,15 @@ struct Cfg {
   static constexpr int A_BYTES = BM * 128;
   // the fp16 operand of the LM head is private to each wave and goes from
   // global memory straight to registers, so it takes no LDS
-  static constexpr int B_BYTES = INT4 ? BN * 32 : 0;
-  static constexpr int S_BYTES = INT4 ? 1024 : 0;
+  static constexpr int B_BYTES = WF == WF_INT4 ? BN * 32 : WF == WF_FP8 ? BN * 64 : 0;
+  static constexpr int S_BYTES = WF == WF_INT4 ? 1024 : 0;
   static constexpr int STAGE = A_BYTES + B_BYTES + S_BYTES;
-  static constexpr int LDS = NSTAGE * STAGE;
+  static constexpr int NS = WF == WF_FP8 ? 2 : NSTAGE;  // ring stages
+  static constexpr int LDS = NS * STAGE;
   // global->LDS instructions one wave issues per K step (A rows, weight tile, scales)
   static constexpr int A_LOADS = (BM / 8 + NW - 1) / NW;
-  static constexpr int B_LOADS = INT4 ? BN / 32 / NW : 0;
-  static constexpr int LOADS = A_LOADS + B_LOADS + (INT4 ? 1 : 0);
+  static constexpr int B_LOADS = B_BYTES / 1024 / NW;
+  static constexpr int LOADS = A_LOADS + B_LOADS + (WF == WF_INT4 ? 1 : 0);
 };
 
 // Workgroup: 4 waves side by side along N; wave w owns all BM tokens of the
@@ -109,10 +132,11 @@ struct Occ {
   static constexpr int value = MI >= 16 ? 1 : 2;
 };
 
-template <int MI, bool INT4, int EPI, int NW_ = 4>
+template <int MI, int WF, int EPI, int NW_ = 4>
 __global__ __launch_bounds__((64 * NW_), (NW_ == 4 ? Occ<MI>::value : 1)) void gemm_kernel(
     const GemmArgs p) {
-  using C = Cfg<MI, INT4, NW_>;
+  constexpr bool INT4 = WF == WF_INT4;
+  using C = Cfg<MI, WF, NW_>;
   constexpr int BM = C::BM, BN = C::BN, NW = C::NW;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
 
@@ -167,6 +191,16 @@ __global__ __launch_bounds__((64 * NW_), (NW_ == 4 ? Occ<MI>::value : 1)) void g
         const int pi = lane >> 3;
         const size_t blk = (nb0 + (pi >> 1)) * KG + kt * 2 + (pi & 1);
         if ((lane >> 4) == wave) g2l16((const char*)p.bs + blk * 128 + (lane & 7) * 16, sS);
+      }
+    } else if constexpr (WF == WF_FP8) {
+      // 1 KB chunks: (64-column block, group) pair q >> 1, half q & 1
+      const size_t nb0 = (size_t)(n0 >> 6);
+#pragma unroll
+      for (int i = 0; i < C::B_LOADS; ++i) {
+        const int q = wave + NW * i;
+        const int pr = q >> 1;
+        const size_t blk = (nb0 + (pr >> 1)) * KG + kt * 2 + (pr & 1);
+        g2l16((const char*)p.bq + (blk * 2 + (q & 1)) * 1024 + lane * 16, sB + q * 1024);
       }
     }
   };
@@ -234,6 +268,47 @@ __global__ __launch_bounds__((64 * NW_), (NW_ == 4 ? Occ<MI>::value : 1)) void g
           __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // VALU
         }
     }
+  } else if constexpr (WF == WF_FP8) {
+    // two stages: the next step's tiles load while this step's MFMAs run
+    issue(0, 0);
+    for (int kt = 0; kt < KT; ++kt) {
+      // this step's loads are the only ones in flight
+      wait_vmcnt<0>();
+      barrier();
+      if (kt + 1 < KT) issue((kt + 1) & 1, kt + 1);
+      const char* sA = smem + (kt & 1) * C::STAGE;
+      const char* sB = sA + C::A_BYTES;
+      f16x8 a[2][MI];
+      uint4 cw[2][2];  // [group][half]: half h holds columns 16*(2h + f') + c
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+          const int r = 16 * i + c;
+          a[kk][i] = *(const f16x8*)(sA + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
+        }
+        const int q = wave * 2 + kk;
+        cw[kk][0] = *(const uint4*)(sB + q * 2048 + lane * 16);
+        cw[kk][1] = *(const uint4*)(sB + q * 2048 + 1024 + lane * 16);
+      }
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+        for (int f = 0; f < 4; ++f) {
+          const uint4 h = cw[kk][f >> 1];
+          const f16x8 w = (f & 1) ? fp8x8(h.z, h.w) : fp8x8(h.x, h.y);
+#pragma unroll
+          for (int i = 0; i < MI; ++i) acc[f][i] = mfma16x16x32(w, a[kk][i], acc[f][i]);
+        }
+      }
+      __builtin_amdgcn_sched_group_barrier(0x100, 2 * MI + 4, 0);  // DS reads
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);           // VALU
+#pragma unroll
+      for (int j = 0; j < 8 * MI; ++j) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);  // VALU
+      }
+    }
   } else {
     // LM head: the vocabulary tile (A) streams through the LDS ring; each
     // wave's 64 token rows (B) are loaded from global memory into registers
@@ -299,6 +374,15 @@ __global__ __launch_bounds__((64 * NW_), (NW_ == 4 ? Occ<MI>::value : 1)) void g
   // acc[f][i][r] = C[m][n], m = m0 + 16i + c, n = n0 + 64*wave + 16f + 4g + r
   const int mrow = m0 + c;
   const int ncol = n0 + wave * 64 + 4 * g;
+  if constexpr (WF == WF_FP8) {
+    // the FP8 weight's per-column scale
+#pragma unroll
+    for (int f = 0; f < 4; ++f) {
+      const float4 sc = *(const float4*)(p.bsc + ncol + 16 * f);
+#pragma unroll
+      for (int i = 0; i < MI; ++i) acc[f][i] = acc[f][i] * f32x4{sc.x, sc.y, sc.z, sc.w};
+    }
+  }
   if constexpr (EPI == EPI_STORE_F16) {
     f16* Cp = (f16*)p.C;
 #pragma unroll
@@ -436,27 +520,27 @@ __global__ __launch_bounds__((64 * NW_), (NW_ == 4 ? Occ<MI>::value : 1)) void g
   }
 }
 
-template <int MI, bool INT4, int EPI, int NW = 4>
+template <int MI, int WF, int EPI, int NW = 4>
 hipError_t launch_cfg(hipStream_t s, const GemmArgs& a) {
-  using C = Cfg<MI, INT4, NW>;
+  using C = Cfg<MI, WF, NW>;
   const int tiles = ((a.M + C::BM - 1) / C::BM) * ((a.N + C::BN - 1) / C::BN);
   if (tiles == 0) return hipSuccess;
   // set once per instantiation (a function-local static is initialised once,
   // also when several threads launch)
   static const hipError_t attr = hipFuncSetAttribute(
-      (const void*)gemm_kernel<MI, INT4, EPI, NW>, hipFuncAttributeMaxDynamicSharedMemorySize,
+      (const void*)gemm_kernel<MI, WF, EPI, NW>, hipFuncAttributeMaxDynamicSharedMemorySize,
       C::LDS);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((gemm_kernel<MI, INT4, EPI, NW>), dim3(tiles), dim3(64 * NW), C::LDS, s, a);
+  hipLaunchKernelGGL((gemm_kernel<MI, WF, EPI, NW>), dim3(tiles), dim3(64 * NW), C::LDS, s, a);
   return hipGetLastError();
 }
 
-template <bool INT4, int EPI>
+template <int WF, int EPI>
 hipError_t launch_epi(hipStream_t s, const GemmArgs& a) {
   // the head's epilogue does not fit the register file next to a 256-token tile
-  if (a.M > 256) return launch_cfg<8, INT4, EPI>(s, a);
-  if (a.M > 64) return launch_cfg<4, INT4, EPI>(s, a);
-  return launch_cfg<2, INT4, EPI>(s, a);
+  if (a.M > 256) return launch_cfg<8, WF, EPI>(s, a);
+  if (a.M > 64) return launch_cfg<4, WF, EPI>(s, a);
+  return launch_cfg<2, WF, EPI>(s, a);
 }
 
 }  // namespace
@@ -465,10 +549,22 @@ hipError_t launch_gemm_w4(hipStream_t s, const GemmArgs& a, int epi) {
   // the packed weight is padded to 256 columns so every tile shape divides it
   if (a.K % BK != 0 || a.N % 256 != 0) return hipErrorInvalidValue;
   switch (epi) {
-    case EPI_STORE_F16: return launch_epi<true, EPI_STORE_F16>(s, a);
-    case EPI_ADD_F32: return launch_epi<true, EPI_ADD_F32>(s, a);
-    case EPI_SWIGLU: return launch_epi<true, EPI_SWIGLU>(s, a);
-    case EPI_QKV: return launch_epi<true, EPI_QKV>(s, a);
+    case EPI_STORE_F16: return launch_epi<WF_INT4, EPI_STORE_F16>(s, a);
+    case EPI_ADD_F32: return launch_epi<WF_INT4, EPI_ADD_F32>(s, a);
+    case EPI_SWIGLU: return launch_epi<WF_INT4, EPI_SWIGLU>(s, a);
+    case EPI_QKV: return launch_epi<WF_INT4, EPI_QKV>(s, a);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_gemm_w8(hipStream_t s, const GemmArgs& a, int epi) {
+  // the packed weight is padded to 256 columns (and its scales with it)
+  if (a.K % BK != 0 || a.N % 256 != 0 || !a.bsc) return hipErrorInvalidValue;
+  switch (epi) {
+    case EPI_STORE_F16: return launch_epi<WF_FP8, EPI_STORE_F16>(s, a);
+    case EPI_ADD_F32: return launch_epi<WF_FP8, EPI_ADD_F32>(s, a);
+    case EPI_SWIGLU: return launch_epi<WF_FP8, EPI_SWIGLU>(s, a);
+    case EPI_QKV: return launch_epi<WF_FP8, EPI_QKV>(s, a);
     default: return hipErrorInvalidValue;
   }
 }
@@ -480,8 +576,8 @@ hipError_t launch_gemm_f16(hipStream_t s, const GemmArgs& a, int epi) {
   // XCD, so the LM head weight streams from HBM about once
   // up to 256 token rows: 4 waves (two workgroups per CU stream the weight);
   // more: 8 waves, so up to 512 rows share each weight tile
-  if (a.N <= 256) return launch_cfg<8, false, EPI_HEAD, 4>(s, a);
-  return launch_cfg<8, false, EPI_HEAD, 8>(s, a);
+  if (a.N <= 256) return launch_cfg<8, WF_F16, EPI_HEAD, 4>(s, a);
+  return launch_cfg<8, WF_F16, EPI_HEAD, 8>(s, a);
 }
 
 }  // namespace lmop

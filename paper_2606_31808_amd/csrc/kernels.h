@@ -14,9 +14,12 @@ typedef uint16_t half_bits;  // fp16 storage as seen from host code
 //          nibble p = feature 2p (p < 4) / 2(p-4)+1 (p >= 4)
 //   spack: fp16 [Np/64][KG][16 c][4 f]
 // Np is a multiple of 256, Kp (= 32*KG) a multiple of 64.
-struct PackedW4 {
+// A linear map packed for the GEMM: int4 codes and fp16 group scales
+// (spack), or FP8 codes and fp32 per-column scales (sscale).
+struct PackedW {
   uint32_t* qpack = nullptr;
   half_bits* spack = nullptr;
+  float* sscale = nullptr;
   int n = 0;   // logical output columns (fused)
   int np = 0;  // padded columns
   int kp = 0;  // padded input features (multiple of 64)
@@ -36,9 +39,11 @@ struct GemmArgs {
   const void* A;  // fp16 [M][lda]; columns >= K are never read
   int lda;
   int M, N, K;    // N: columns of the (padded) weight walked by the grid; K multiple of 64
-  // int4 weight
+  // int4 weight (bq codes, bs fp16 group scales) or FP8 weight (bq E4M3
+  // codes, bsc fp32 per-column scales)
   const uint32_t* bq;
   const half_bits* bs;
+  const float* bsc;
   // fp16 weight (LM head): [N][ldb]
   const half_bits* bh;
   int ldb;
@@ -71,17 +76,24 @@ struct GemmArgs {
 
 // Picks the tile shape for M and launches.  Returns hipSuccess or the launch error.
 hipError_t launch_gemm_w4(hipStream_t s, const GemmArgs& a, int epi);
+hipError_t launch_gemm_w8(hipStream_t s, const GemmArgs& a, int epi);  // FP8 weights
 hipError_t launch_gemm_f16(hipStream_t s, const GemmArgs& a, int epi);  // head only
 
 // Repacks one source matrix's rows into columns of a packed weight.
 // colsrc[j] (device, [np]): (source index << 24) | source row, or -1 (zero column).
 struct RepackSrc {
   const uint8_t* q[3];
-  const half_bits* s[3];
-  int kp_src[3];  // padded K of each source (multiple of 32)
+  const half_bits* s[3];   // int4: fp16 group scales
+  const float* sf[3];      // FP8: fp32 per-row scales
+  int kp_src[3];  // int4: padded K of each source (multiple of 32); FP8: K
 };
 hipError_t launch_repack_w4(hipStream_t s, const RepackSrc& src, const int32_t* colsrc,
-                            PackedW4& dst);
+                            PackedW& dst);
+// FP8 rows [n][K] of E4M3 codes -> tiles of 2 KB per 64 columns x 32
+// features (two 1 KB halves; lane 16g+c of half h holds the 8 codes of
+// features 8g.. of columns 16(2h)+c and 16(2h+1)+c), scales in column order
+hipError_t launch_repack_w8(hipStream_t s, const RepackSrc& src, const int32_t* colsrc,
+                            PackedW& dst);
 
 // ---------------------------------------------------------------- elementwise
 hipError_t launch_embed(hipStream_t s, const int32_t* tok, int T, const half_bits* emb, int d,

@@ -41,7 +41,7 @@ int64_t round_up64(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 struct LayerW {
   float* attn_norm = nullptr;
   float* mlp_norm = nullptr;
-  PackedW4 qkv, o, gu, down;
+  PackedW qkv, o, gu, down;
 };
 
 struct Stat {
@@ -97,6 +97,7 @@ struct lmop_ctx {
 
   // dims
   int nq_dim = 0, nkv_dim = 0, qkv_n = 0, f64 = 0;
+  uint32_t wfmt = LMOP_W_INT4_G32;  // format of the loaded linear maps
 
   // weights (device)
   uint16_t* emb = nullptr;
@@ -479,9 +480,15 @@ void free_weights(lmop_ctx* c) {
 
 // Packs up to three source matrices (rows = output columns) into one tiled
 // int4 weight.  colmap[j] = (source << 24) | row, or -1 for a zero column.
+lmop_status pack_fp8(lmop_ctx* c, const lmop_qmat* const* srcs, int n_src,
+                     const std::vector<int32_t>& colmap, int n_logical, int k, bool on_device,
+                     PackedW* out);
+
 lmop_status pack(lmop_ctx* c, const lmop_qmat* const* srcs, int n_src, const std::vector<int32_t>& colmap,
-                 int n_logical, int k, bool on_device, PackedW4* out) {
-  PackedW4 w;
+                 int n_logical, int k, bool on_device, PackedW* out) {
+  if (c->wfmt == LMOP_W_FP8_E4M3)
+    return pack_fp8(c, srcs, n_src, colmap, n_logical, k, on_device, out);
+  PackedW w;
   w.n = n_logical;
   w.np = (int)colmap.size();
   w.k = k;
@@ -504,7 +511,7 @@ lmop_status pack(lmop_ctx* c, const lmop_qmat* const* srcs, int n_src, const std
     rs.kp_src[i] = kps;
     if (on_device) {
       rs.q[i] = m.qweight;
-      rs.s[i] = m.scales;
+      rs.s[i] = (const half_bits*)m.scales;
     } else {
       void* dq = nullptr;
       void* ds = nullptr;
@@ -530,6 +537,82 @@ lmop_status pack(lmop_ctx* c, const lmop_qmat* const* srcs, int n_src, const std
   for (void* p : staging) HIP_OK(c, hipFree(p));
   *out = w;
   return LMOP_OK;
+}
+
+// The same for FP8 weights: E4M3 codes [n][k] and fp32 row scales [n] of up
+// to three sources -> 2 KB tiles per 64 columns x 32 features, fp32 scales in
+// packed column order.
+lmop_status pack_fp8(lmop_ctx* c, const lmop_qmat* const* srcs, int n_src,
+                     const std::vector<int32_t>& colmap, int n_logical, int k, bool on_device,
+                     PackedW* out) {
+  PackedW w;
+  w.n = n_logical;
+  w.np = (int)colmap.size();
+  w.k = k;
+  w.kp = round_up(k, 64);
+  const int kg = w.kp / 32;
+  void* qp = nullptr;
+  void* sp = nullptr;
+  LMOP_TRY(dev_alloc(c, &qp, (size_t)(w.np / 64) * kg * 2048));
+  c->weight_allocs.push_back(qp);
+  LMOP_TRY(dev_alloc(c, &sp, (size_t)w.np * 4));
+  c->weight_allocs.push_back(sp);
+  w.qpack = (uint32_t*)qp;
+  w.sscale = (float*)sp;
+  RepackSrc rs{};
+  std::vector<void*> staging;
+  for (int i = 0; i < n_src; ++i) {
+    const lmop_qmat& m = *srcs[i];
+    rs.kp_src[i] = m.k;
+    if (on_device) {
+      rs.q[i] = m.qweight;
+      rs.sf[i] = (const float*)m.scales;
+    } else {
+      void* dq = nullptr;
+      void* ds = nullptr;
+      LMOP_TRY(dev_alloc(c, &dq, (size_t)m.n * m.k));
+      staging.push_back(dq);
+      LMOP_TRY(dev_alloc(c, &ds, (size_t)m.n * 4));
+      staging.push_back(ds);
+      HIP_OK(c, hipMemcpyAsync(dq, m.qweight, (size_t)m.n * m.k, hipMemcpyHostToDevice,
+                               c->stream));
+      HIP_OK(c, hipMemcpyAsync(ds, m.scales, (size_t)m.n * 4, hipMemcpyHostToDevice, c->stream));
+      rs.q[i] = (const uint8_t*)dq;
+      rs.sf[i] = (const float*)ds;
+    }
+  }
+  void* dmap = nullptr;
+  LMOP_TRY(dev_alloc(c, &dmap, colmap.size() * 4));
+  staging.push_back(dmap);
+  HIP_OK(c, hipMemcpyAsync(dmap, colmap.data(), colmap.size() * 4, hipMemcpyHostToDevice,
+                           c->stream));
+  LMOP_TRY(timed(c, "repack_w8", 0, 0,
+                 [&] { return launch_repack_w8(c->stream, rs, (const int32_t*)dmap, w); }));
+  HIP_OK(c, hipStreamSynchronize(c->stream));
+  for (void* p : staging) HIP_OK(c, hipFree(p));
+  *out = w;
+  return LMOP_OK;
+}
+
+// The GEMM of a packed linear map in the loaded weight format.
+hipError_t launch_gemm_packed(const lmop_ctx* c, GemmArgs& ga, const PackedW& W, int epi) {
+  ga.bq = W.qpack;
+  if (c->wfmt == LMOP_W_FP8_E4M3) {
+    ga.bsc = W.sscale;
+    return launch_gemm_w8(c->stream, ga, epi);
+  }
+  ga.bs = W.spack;
+  return launch_gemm_w4(c->stream, ga, epi);
+}
+
+// timing names and weight bytes per parameter of the loaded format
+const char* gemm_name(const lmop_ctx* c, const char* proj) {
+  static thread_local std::string n;
+  n = std::string(c->wfmt == LMOP_W_FP8_E4M3 ? "gemm_w8a16_" : "gemm_w4a16_") + proj;
+  return n.c_str();
+}
+double weight_bytes(const lmop_ctx* c, double n, double k) {
+  return c->wfmt == LMOP_W_FP8_E4M3 ? n * k + n * 4 : n * k * 0.5625;
 }
 
 std::vector<int32_t> concat_map(const int* rows, int n_parts, int np) {
@@ -596,8 +679,6 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
       ga.M = T;
       ga.N = L.qkv.np;
       ga.K = L.qkv.kp;
-      ga.bq = L.qkv.qpack;
-      ga.bs = L.qkv.spack;
       ga.pos = pos;
       ga.slot = slot;
       ga.rope = c->rope_tab;
@@ -609,10 +690,10 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
       ga.nkv = cf.n_kv_heads;
       ga.hd = hd;
       const double flops = 2.0 * T * L.qkv.n * L.qkv.k;
-      const double bytes = (double)T * L.qkv.k * 2 + (double)L.qkv.n * L.qkv.k * 0.5625 +
+      const double bytes = (double)T * L.qkv.k * 2 + weight_bytes(c, L.qkv.n, L.qkv.k) +
                            (double)T * L.qkv.n * 2;
-      LMOP_TRY(timed(c, "gemm_w4a16_qkv", flops, bytes,
-                     [&] { return launch_gemm_w4(c->stream, ga, EPI_QKV); }));
+      LMOP_TRY(timed(c, gemm_name(c, "qkv"), flops, bytes,
+                     [&] { return launch_gemm_packed(c, ga, L.qkv, EPI_QKV); }));
     }
     AttnArgs aa{};
     aa.q = q;
@@ -645,7 +726,7 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
       }));
       M = b.n_last;
     }
-    auto gemm2 = [&](const char* name, const void* A, int lda, const PackedW4& W, int epi,
+    auto gemm2 = [&](const char* name, const void* A, int lda, const PackedW& W, int epi,
                      void* C, int ldc, int n_out) {
       GemmArgs ga{};
       ga.A = A;
@@ -653,24 +734,23 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
       ga.M = M;
       ga.N = W.np;
       ga.K = W.kp;
-      ga.bq = W.qpack;
-      ga.bs = W.spack;
       ga.C = C;
       ga.ldc = ldc;
       ga.n_out = n_out;
       ga.X = xr;
       ga.ldx = d;
       const double flops = 2.0 * M * W.n * W.k;
-      const double bytes = (double)M * W.k * 2 + (double)W.n * W.k * 0.5625 +
+      const double bytes = (double)M * W.k * 2 + weight_bytes(c, W.n, W.k) +
                            (double)M * W.n * (epi == EPI_ADD_F32 ? 8 : 2);
-      return timed(c, name, flops, bytes, [&] { return launch_gemm_w4(c->stream, ga, epi); });
+      return timed(c, gemm_name(c, name), flops, bytes,
+                   [&] { return launch_gemm_packed(c, ga, W, epi); });
     };
-    LMOP_TRY(gemm2("gemm_w4a16_o", ar, c->nq_dim, L.o, EPI_ADD_F32, nullptr, 0, d));
+    LMOP_TRY(gemm2("o", ar, c->nq_dim, L.o, EPI_ADD_F32, nullptr, 0, d));
     LMOP_TRY(timed(c, "rmsnorm", 0, (double)M * d * 6, [&] {
       return launch_rmsnorm(c->stream, xr, d, nullptr, M, L.mlp_norm, d, cf.rms_eps, h, d);
     }));
-    LMOP_TRY(gemm2("gemm_w4a16_gateup", h, d, L.gu, EPI_SWIGLU, act, c->f64, c->f64));
-    LMOP_TRY(gemm2("gemm_w4a16_down", act, c->f64, L.down, EPI_ADD_F32, nullptr, 0, d));
+    LMOP_TRY(gemm2("gateup", h, d, L.gu, EPI_SWIGLU, act, c->f64, c->f64));
+    LMOP_TRY(gemm2("down", act, c->f64, L.down, EPI_ADD_F32, nullptr, 0, d));
   }
   return LMOP_OK;
 }
@@ -958,6 +1038,8 @@ lmop_status lmop_load_weights(lmop_ctx* ctx, const lmop_weights* w) {
                 cf.n_layers);
   if (!w->tok_embedding || !w->lm_head || !w->final_norm || (cf.n_layers > 0 && !w->layers))
     return fail(ctx, LMOP_ERR_INVALID_ARG, "NULL embedding, head, final norm or layer array");
+  if (w->format != (int32_t)LMOP_W_INT4_G32 && w->format != (int32_t)LMOP_W_FP8_E4M3)
+    return fail(ctx, LMOP_ERR_INVALID_ARG, "unknown weight format %d", w->format);
   const int d = cf.d_model, nq = ctx->nq_dim, nkv = ctx->nkv_dim, F = cf.d_ff;
   for (int l = 0; l < cf.n_layers; ++l) {
     const lmop_layer& L = w->layers[l];
@@ -983,6 +1065,7 @@ lmop_status lmop_load_weights(lmop_ctx* ctx, const lmop_weights* w) {
   ctx->loaded = false;
   ctx->generation++;
   const bool od = w->on_device != 0;
+  ctx->wfmt = (uint32_t)w->format;
   const size_t V = cf.vocab;
   void* p = nullptr;
   LMOP_TRY(upload(ctx, w->tok_embedding, V * d * 2, od, &p));

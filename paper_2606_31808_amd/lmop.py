@@ -20,6 +20,8 @@ LIB_PATH = os.path.join(_HERE, "_lib", "liblmop.so")
 LMOP_OK, LMOP_ERR_INVALID_ARG, LMOP_ERR_STATE, LMOP_ERR_OOM, LMOP_ERR_DEVICE, \
     LMOP_ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 LMOP_BOOL, LMOP_ENUM, LMOP_INT, LMOP_AUTOMATON = 0, 1, 2, 3
+LMOP_W_INT4_G32, LMOP_W_FP8_E4M3 = 0, 1
+_WEIGHT_FORMATS = {"int4_g32": LMOP_W_INT4_G32, "fp8_e4m3": LMOP_W_FP8_E4M3}
 LMOP_NO_DEDUP = 1
 LMOP_HEAD_RESTRICTED = 2
 
@@ -51,7 +53,7 @@ class lmop_layer(C.Structure):
 class lmop_weights(C.Structure):
     _fields_ = [("tok_embedding", C.c_void_p), ("lm_head", C.c_void_p),
                 ("final_norm", C.c_void_p), ("layers", C.POINTER(lmop_layer)),
-                ("n_layers", C.c_int32), ("on_device", C.c_int32)]
+                ("n_layers", C.c_int32), ("on_device", C.c_int32), ("format", C.c_int32)]
 
 
 class lmop_automaton(C.Structure):
@@ -172,7 +174,8 @@ def _tensor_ptr(t, keep):
 
 def lmop_load_weights(ctx, weights) -> None:
     """weights: object with tok_embedding, lm_head (fp16 [V][d]), final_norm, layers[...]
-    (attn_norm, mlp_norm, wq .. w_down each with qweight/scales/n/k), all on one device."""
+    (attn_norm, mlp_norm, wq .. w_down each with qweight/scales/n/k and a format name
+    `fmt`, "int4_g32" (default) or "fp8_e4m3"), all on one device."""
     keep = []
     where = set()
 
@@ -189,8 +192,13 @@ def lmop_load_weights(ctx, weights) -> None:
     for i, l in enumerate(weights.layers):
         arr[i] = lmop_layer(p(l.attn_norm), p(l.mlp_norm), qm(l.wq), qm(l.wk), qm(l.wv), qm(l.wo),
                             qm(l.w_gate), qm(l.w_up), qm(l.w_down))
+    fmts = {getattr(getattr(l, nm), "fmt", "int4_g32") for l in weights.layers
+            for nm in ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")}
+    if len(fmts) > 1:
+        raise ValueError("all linear maps must have one weight format")
+    fmt = _WEIGHT_FORMATS[fmts.pop() if fmts else "int4_g32"]
     w = lmop_weights(p(weights.tok_embedding), p(weights.lm_head), p(weights.final_norm),
-                     C.cast(arr, C.POINTER(lmop_layer)), L, 0)
+                     C.cast(arr, C.POINTER(lmop_layer)), L, 0, fmt)
     if len(where) != 1:
         raise ValueError("weights must all be on the host or all on the device")
     w.on_device = 1 if where.pop() else 0

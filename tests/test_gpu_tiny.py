@@ -431,6 +431,62 @@ def test_tiny_cascade_row_mask(tiny, L):
     ctx.release_prefix(pre)
 
 
+@pytest.fixture(scope="module")
+def tiny_fp8(L):
+    w = make_weights(TINY, seed=1234, fmt="fp8_e4m3")
+    orc = OracleLM(w, TINY)
+    ctx = L.Context(TINY, device=0)
+    ctx.load_weights(w)
+    return w, orc, ctx
+
+
+def test_tiny_fp8_weights(tiny_fp8, L):
+    """FP8 (E4M3, per-channel scale) weights: the filter, an integer decode
+    and a two-level join against the oracle of the same FP8 weights; batching
+    does not change a bit; device-resident weights load the same."""
+    w, orc, ctx = tiny_fp8
+    wl = make_workload("filter_tiny")
+    pre = ctx.set_prefix(wl.prefix)
+    _log("fp8: filter")
+    out, dbg = _run(ctx, wl, pre)
+    ref = orc.eval_workload(wl, keep_logits=True)
+    _log("fp8 filter", compare(ref, out, dbg, "fp8 filter"))
+    assert_typed(out, wl.kind, len(wl.allowed), wl.allowed)
+    o2, d2 = _run(ctx, wl, pre, max_batch_tokens=50)
+    assert o2.tobytes() == out.tobytes() and np.array_equal(d2, dbg)
+    rng = np.random.default_rng(8)
+    digits = rng.choice(TINY.vocab, 10, replace=False).astype(np.int32)
+    eos = int(next(t for t in range(TINY.vocab) if t not in digits))
+    rows = [wl.suffix(r) for r in range(24)]
+    offs = np.concatenate([[0], np.cumsum([len(r) for r in rows])])
+    oi, di = ctx.eval_rows(np.concatenate(rows), offs, KIND_INT, digits, eos=eos, max_tokens=3,
+                           prefix=pre, debug_logits=True)
+    ri = orc.eval_rows(wl.prefix, rows, KIND_INT, digits, eos=eos, max_tokens=3, keep_logits=True)
+    fi = orc.eval_rows(wl.prefix, rows, KIND_INT, digits, eos=eos, max_tokens=3, keep_logits=True,
+                       forced=[oi["tokens"][r][: oi["n_tokens"][r]] for r in range(24)])
+    _log("fp8 int", compare(ri, oi, di, "fp8 int", orc_forced=fi))
+    kids = ctx.set_prefixes([wl.suffix(40)[:9], wl.suffix(41)[:20]], parent=pre)
+    jrows = [wl.suffix(r) for r in range(6)]
+    rc = [0, 1, 0, 1, 1, 0]
+    jo, jd = ctx.eval_rows(np.concatenate(jrows), np.concatenate([[0], np.cumsum([len(r) for r in jrows])]),
+                           KIND_BOOL, wl.allowed, row_prefix=[kids[i] for i in rc],
+                           debug_logits=True)
+    jr = orc.eval_rows(wl.prefix, jrows, KIND_BOOL, wl.allowed,
+                       children=[wl.suffix(40)[:9], wl.suffix(41)[:20]], row_child=rc,
+                       keep_logits=True)
+    _log("fp8 join", compare(jr, jo, jd, "fp8 join"))
+    for k in kids:
+        ctx.release_prefix(k)
+    ctx.release_prefix(pre)
+    # the same weights from device memory
+    ctx2 = L.Context(TINY, device=0)
+    ctx2.load_weights(w.to("cuda:0"))
+    p2 = ctx2.set_prefix(wl.prefix)
+    o3, d3 = _run(ctx2, wl, p2)
+    assert o3.tobytes() == out.tobytes() and np.array_equal(d3, dbg)
+    ctx2.close()
+
+
 def test_tiny_restricted_head(tiny, L):
     """Restricted head: only the allowed tokens' logits are computed; typed
     outputs and allowed-set log-probabilities match the oracle and the full

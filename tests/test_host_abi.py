@@ -203,6 +203,15 @@ def test_dedup_rejects_bad_csr():
     assert nu == 0 and len(rep) == 0
 
 
+def test_fp8_weights_load_on_host_ctx():
+    w8 = make_weights(TINY, seed=5, fmt="fp8_e4m3")
+    ctx = _host_ctx()
+    ctx.load_weights(w8)  # validation passes; a host-only ctx keeps nothing
+    w8.layers[0].wq.fmt = "int4_g32"
+    with pytest.raises(ValueError):
+        ctx.load_weights(w8)
+
+
 def test_limit_validation(tiny_w):
     ctx = _host_ctx()
     ctx.load_weights(tiny_w)
@@ -252,7 +261,9 @@ def test_binding_constants_match_header():
     """The flag values the binding passes are the header's."""
     hdr = open(os.path.join(ROOT, "include", "lmop.h")).read()
     defs = dict(re.findall(r"#define\s+(LMOP_\w+)\s+(\d+)u", hdr))
-    assert defs == {"LMOP_NO_DEDUP": "1", "LMOP_HEAD_RESTRICTED": "2"}
+    assert defs == {"LMOP_NO_DEDUP": "1", "LMOP_HEAD_RESTRICTED": "2", "LMOP_W_INT4_G32": "0",
+                    "LMOP_W_FP8_E4M3": "1"}
+    assert (L.LMOP_W_INT4_G32, L.LMOP_W_FP8_E4M3) == (0, 1)
     assert L.LMOP_NO_DEDUP == 1 and L.LMOP_HEAD_RESTRICTED == 2
     kinds = dict(re.findall(r"(LMOP_(?:BOOL|ENUM|INT|AUTOMATON))\s*=\s*(\d+)", hdr))
     assert kinds == {"LMOP_BOOL": "0", "LMOP_ENUM": "1", "LMOP_INT": "2", "LMOP_AUTOMATON": "3"}
