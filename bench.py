@@ -35,8 +35,11 @@ def log(*a):
 
 
 def gemm_roofline(stats):
-    """Dominant kernel family: the W4A16 GEMMs (all four projections)."""
-    names = [n for n in stats if n.startswith("gemm_w4a16")]
+    """Dominant kernel family: the weight GEMMs (all four projections), W4A16
+    or, with FP8 weights, W8A16."""
+    fp8 = any(n.startswith("gemm_w8a16") for n in stats)
+    fam = "gemm_w8a16" if fp8 else "gemm_w4a16"
+    names = [n for n in stats if n.startswith(fam)]
     ms = sum(stats[n]["ms"] for n in names)
     fl = sum(stats[n]["flops"] for n in names)
     launches = sum(stats[n]["launches"] for n in names)
@@ -44,9 +47,10 @@ def gemm_roofline(stats):
         return None
     ach = fl / (ms * 1e-3) / 1e12
     algo_bytes = sum(stats[n]["bytes"] for n in names) / launches
-    return {"bound": "mfma", "kernel": "gemm_w4a16 (qkv, o, gate/up, down)", "achieved": ach,
+    return {"bound": "mfma", "kernel": f"{fam} (qkv, o, gate/up, down)", "achieved": ach,
             "peak": PEAK_F16_TFLOPS, "unit": "TFLOP/s", "frac": ach / PEAK_F16_TFLOPS,
-            "traffic": measured_traffic(), "algorithmic_bytes_per_launch": algo_bytes,
+            "traffic": None if fp8 else measured_traffic(),
+            "algorithmic_bytes_per_launch": algo_bytes,
             "launches": launches, "avg_launch_ms": ms / launches, "flops_per_launch": fl / launches}
 
 
@@ -75,7 +79,11 @@ def _bench_line(log_path):
 
 
 def _is_w4_gemm(name):
-    return "gemm_kernel<" in name and ", true," in name
+    # gemm_kernel<MI, weight format, epilogue, waves>; format 1 = int4
+    if "gemm_kernel<" not in name:
+        return False
+    args = name.split("gemm_kernel<")[1].split(">")[0].split(",")
+    return len(args) >= 2 and args[1].strip() in ("1", "true")
 
 
 def _timed_gemm_rows(rows, n_timed):
@@ -153,7 +161,8 @@ def mfma_summary(root):
             return {"1": "W4A16 GEMM, residual add (o, down)", "2": "W4A16 GEMM, SwiGLU (gate/up)",
                     "4": "W4A16 GEMM, QKV + RoPE (qkv)", "0": "W4A16 GEMM, fp16 store"}.get(epi, epi)
         if "gemm_kernel<" in name:
-            return "LM head GEMM"
+            fmt = name.split("gemm_kernel<")[1].split(",")[1].strip()
+            return "W8A16 GEMM (FP8 weights)" if fmt == "2" else "LM head GEMM"
         if "attn_kernel" in name:
             return "attention"
         return None
@@ -270,6 +279,8 @@ def main():
     ap.add_argument("--limit", type=int, default=0,
                     help="LIMIT k early exit: stop once k rows have value --limit-value")
     ap.add_argument("--limit-value", type=int, default=1)
+    ap.add_argument("--weights", default="int4_g32", choices=["int4_g32", "fp8_e4m3"],
+                    help="weight format of the linear maps")
     ap.add_argument("--cascade", action="store_true",
                     help="cascade filtering: a bool predicate first, the workload on its survivors")
     ap.add_argument("--cascade-model", default="",
@@ -322,7 +333,7 @@ def main():
     stream = torch.cuda.current_stream(dev).cuda_stream
     log(f"[bench] generating {shape.name} weights on the GPU")
     t0 = time.perf_counter()
-    w = make_weights(shape, seed=1234, device=dev)
+    w = make_weights(shape, seed=1234, device=dev, fmt=args.weights)
     torch.cuda.synchronize()
     log(f"[bench] weights {time.perf_counter() - t0:.1f} s; loading into the library")
     # room for the longest sequence (LLMQA prompts run past the default 4,096)
@@ -415,7 +426,8 @@ def main():
                    "unique_rows": n_unique, "prefix_tokens": len(wl.prefix),
                    "suffix_tokens": n_tok, "suffix_tokens_per_s": n_tok / (ms_step * 1e-3),
                    "batch_tokens": args.batch_tokens or 16384, "parallelism": "single GPU",
-                   "head": "restricted" if args.head_restricted else "full vocabulary"},
+                   "head": "restricted" if args.head_restricted else "full vocabulary",
+                   "weights": args.weights},
         **({"limit": {"k": args.limit, "value": args.limit_value, "rows_in_table": wl.n_rows,
                       "rows_evaluated": rows, "ms_per_query": ms_step}} if args.limit else {}),
         **({"cascade": {"first_model": args.cascade_model or shape.name,

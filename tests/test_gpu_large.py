@@ -218,3 +218,21 @@ def test_join_8b_sampled_pairs(m8b):
     for k in kids:
         ctx.release_prefix(k)
     ctx.release_prefix(root)
+
+
+def test_filter_8b_fp8_sampled_rows(L):
+    """FP8 (E4M3, per-channel scales) weights at the 8B shape: the whole
+    filter table, then sampled rows against the oracle of the same weights."""
+    shape = SHAPES["8b"]
+    _log("8B fp8: weights on the GPU, library load")
+    w = make_weights(shape, seed=1234, device="cuda", fmt="fp8_e4m3")
+    torch.cuda.synchronize()
+    ctx = L.Context(shape, device=0, stream=torch.cuda.current_stream().cuda_stream)
+    ctx.load_weights(w)
+    orc = OracleLM(w, shape, dtype=np.float32, cache_dequant=False)
+    wl = make_workload("filter_8b")
+    pre = ctx.set_prefix(wl.prefix)
+    _check_filter(ctx, orc, wl, pre, _sample(wl, 4, 3), "filter_8b fp8")
+    ctx.close()
+    del w, orc
+    torch.cuda.empty_cache()
