@@ -487,6 +487,72 @@ def test_tiny_fp8_weights(tiny_fp8, L):
     ctx2.close()
 
 
+@pytest.mark.parametrize("seed", [101, 202, 303])
+def test_tiny_mixed_features_random(tiny, L, seed):
+    """Seeded mixes of the features in one call: rows under a root prefix, a
+    child prefix or none, empty suffixes, duplicates, one of the four output
+    types, the full or restricted head and a random batch budget, against the
+    oracle (typed outputs exact where the margin allows)."""
+    from synth import automaton_of_options
+    w, orc, ctx = tiny
+    V = TINY.vocab
+    rng = np.random.default_rng(seed)
+    root_t = rng.integers(0, V, size=int(rng.integers(1, 150))).astype(np.int32)
+    kid_t = rng.integers(0, V, size=int(rng.integers(1, 70))).astype(np.int32)
+    root = ctx.set_prefix(root_t)
+    kid = ctx.set_prefixes([kid_t], parent=root)[0]
+    n = int(rng.integers(8, 40))
+    where = rng.integers(0, 3, size=n)  # 0: none, 1: root, 2: child
+    rows = []
+    for r in range(n):
+        lo = 1 if where[r] == 0 else 0
+        rows.append(rng.integers(0, V, size=int(rng.integers(lo, 90))).astype(np.int32))
+    for r in rng.choice(n, size=min(4, n - 1), replace=False):  # duplicates
+        rows[r], where[r] = rows[0].copy(), where[0]
+    offs = np.concatenate([[0], np.cumsum([len(x) for x in rows])])
+    toks = np.concatenate(rows) if offs[-1] else np.zeros(0, np.int32)
+    rp = [None if where[r] == 0 else (root if where[r] == 1 else kid) for r in range(n)]
+    kind = int(rng.integers(0, 4))
+    eos, max_tokens, spec = -1, 1, None
+    if kind == KIND_BOOL:
+        spec = rng.choice(V, 2, replace=False).astype(np.int32)
+    elif kind == KIND_ENUM:
+        spec = rng.choice(V, int(rng.integers(1, 30)), replace=False).astype(np.int32)
+    elif kind == KIND_INT:
+        spec = rng.choice(V, 10, replace=False).astype(np.int32)
+        eos = int(next(t for t in range(V) if t not in spec))
+        max_tokens = int(rng.integers(1, 5))
+    else:
+        _, spec, _ = automaton_of_options(int(rng.integers(2, 20)), V, rng, max_len=3)
+        max_tokens = 3
+    restricted = bool(rng.integers(0, 2))
+    mbt = int(rng.choice([0, 40, 120]))
+    _log(f"seed {seed}: {n} rows, kind {kind}, restricted {restricted}, budget {mbt}")
+    out, dbg = ctx.eval_rows(toks, offs, kind, spec, eos=eos, max_tokens=max_tokens,
+                             row_prefix=rp, debug_logits=True, head_restricted=restricted,
+                             max_batch_tokens=mbt)
+    # the oracle, per prefix level
+    for lvl in range(3):
+        idx = [r for r in range(n) if where[r] == lvl]
+        if not idx:
+            continue
+        kw = dict(eos=eos, max_tokens=max_tokens, keep_logits=True)
+        pre = None if lvl == 0 else root_t
+        ch = dict(children=[kid_t], row_child=[0] * len(idx)) if lvl == 2 else {}
+        sub = [rows[r] for r in idx]
+        ref = orc.eval_rows(pre, sub, kind, spec, **kw, **ch)
+        forced = orc.eval_rows(pre, sub, kind, spec, **kw, **ch,
+                               forced=[out["tokens"][r][: out["n_tokens"][r]] for r in idx])
+        cols = None
+        if restricted:
+            cols = (sorted(set(np.asarray(spec.edge_token).tolist())) if kind == 3
+                    else list(spec) + ([eos] if kind == KIND_INT else []))
+        _log(f"  level {lvl}", compare(ref, out[idx], dbg[idx], f"seed {seed} level {lvl}",
+                                       orc_forced=forced, cols=cols))
+    ctx.release_prefix(kid)
+    ctx.release_prefix(root)
+
+
 def test_tiny_restricted_head(tiny, L):
     """Restricted head: only the allowed tokens' logits are computed; typed
     outputs and allowed-set log-probabilities match the oracle and the full
