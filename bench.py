@@ -416,12 +416,13 @@ def main():
     value = rows / (ms_step * 1e-3)
     rep, n_unique = L.lmop_dedup_rows(wl.tokens, wl.offsets,
                                       None if wl.row_child is None else wl.row_child)
+    wdesc = "int4-g32" if args.weights == "int4_g32" else "fp8-e4m3 per-channel"
     res = {
         "metric": "rows/sec, 8B-shape W4 LM filter (10k rows); MFMA util %, HBM GB/s",
         "value": value, "unit": "rows/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f16 (int4 weights, fp32 accum)",
-        "data": "synthetic (seeded uniform token ids, random-init N(0,0.02) int4-g32 weights)",
+        "scaling": "weak", "vs_baseline": None, "dtype": f"f16 ({wdesc} weights, fp32 accum)",
+        "data": f"synthetic (seeded uniform token ids, random-init N(0,0.02) {wdesc} weights)",
         "config": {"workload": wl.name, "model_shape": shape.name, "rows": rows,
                    "unique_rows": n_unique, "prefix_tokens": len(wl.prefix),
                    "suffix_tokens": n_tok, "suffix_tokens_per_s": n_tok / (ms_step * 1e-3),
