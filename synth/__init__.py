@@ -20,5 +20,7 @@ from .workloads import (  # noqa: F401
     Automaton,
     option_trie,
     automaton_of_options,
+    automaton_of_list,
+    automaton_of_record,
     KIND_AUTOMATON,
 )

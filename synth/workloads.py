@@ -246,6 +246,98 @@ def automaton_of_options(n_options: int, V: int, rng, max_len: int = 3, n_heads:
     return opts, aut, final
 
 
+def _automaton_of_dicts(edges, accepting) -> Automaton:
+    """Packs per-state {token: next state} dicts (edge order = insertion
+    order) and accepting flags into the CSR automaton."""
+    off, tok, nxt = [0], [], []
+    for e in edges:
+        for t, c in e.items():
+            tok.append(int(t))
+            nxt.append(int(c))
+        off.append(len(tok))
+    return Automaton(len(edges), np.array(off, dtype=np.int32), np.array(tok, dtype=np.int32),
+                     np.array(nxt, dtype=np.int32), np.array(accepting, dtype=np.uint8))
+
+
+def automaton_of_list(items, sep: int, lo: int, hi: int) -> Automaton:
+    """A collection output (Sec. 2.3: a list return type with a regex-style
+    quantifier {lo,hi}): lo..hi items, each one of the token strings
+    `items`, with the token `sep` between two items.  The automaton is hi
+    copies of the items' trie; copy c holds item c + 1.  Where an item ends
+    in copy c, `sep` leads to copy c + 1 (if c + 1 < hi) and the output may
+    end (if c + 1 >= lo).  {3} is lo = hi = 3."""
+    if not 1 <= lo <= hi:
+        raise ValueError(f"quantifier {{{lo},{hi}}}: need 1 <= lo <= hi")
+    if any(int(sep) in {int(t) for t in it} for it in items):
+        raise ValueError("the separator is a token of an item")
+    trie, final = option_trie(items)
+    n = trie.n_states
+    ends = set(int(f) for f in final)
+    edges, acc = [], []
+    for c in range(hi):
+        for st in range(n):
+            e = {int(trie.edge_token[i]): c * n + int(trie.edge_next[i])
+                 for i in range(trie.edge_offset[st], trie.edge_offset[st + 1])}
+            if st in ends and c + 1 < hi:
+                e[int(sep)] = (c + 1) * n
+            edges.append(e)
+            acc.append(1 if st in ends and c + 1 >= lo else 0)
+    return _automaton_of_dicts(edges, acc)
+
+
+def automaton_of_record(open_tok: int, close_tok: int, sep: int, fields) -> Automaton:
+    """A JSON-shaped record over token ids (Sec. 5: a JSON object with a given
+    schema): open_tok, the fields in order separated by sep, close_tok.  A
+    field is ("enum", key, values): its key token (standing for the
+    `"name":` text) and one of the single-token values; or ("int", key,
+    digits, max_digits): its key token and 1..max_digits of the 10 digit
+    tokens.  The state after close_tok is the only accepting state and has
+    no edges, so a complete record ends the output."""
+    edges, acc = [], []
+
+    def new():
+        edges.append({})
+        acc.append(0)
+        return len(edges) - 1
+
+    def add(st, t, nx):
+        if int(t) in edges[st]:
+            raise ValueError(f"token {t} has two meanings in one state")
+        edges[st][int(t)] = nx
+
+    exits = [new()]
+    for i, f in enumerate(fields):
+        lit = open_tok if i == 0 else sep
+        st = new()
+        for e in exits:
+            add(e, lit, st)
+        key = new()
+        add(st, f[1], key)
+        if f[0] == "enum":
+            after = new()
+            for v in f[2]:
+                add(key, v, after)
+            exits = [after]
+        elif f[0] == "int":
+            digits, max_digits = f[2], int(f[3])
+            if len(digits) != 10 or max_digits < 1:
+                raise ValueError("an int field needs 10 digit tokens and max_digits >= 1")
+            exits, prev = [], key
+            for _ in range(max_digits):
+                d = new()
+                for t in digits:
+                    add(prev, t, d)
+                exits.append(d)
+                prev = d
+        else:
+            raise ValueError(f"unknown field kind {f[0]!r}")
+    end = new()
+    for e in exits:
+        add(e, close_tok, end)
+    acc[end] = 1
+    return _automaton_of_dicts(edges, acc)
+
+
 @dataclasses.dataclass
 class Workload:
     """A table of rows for one LM-operator call.

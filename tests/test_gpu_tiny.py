@@ -272,6 +272,50 @@ def test_tiny_options_automaton(tiny, L):
     ctx.release_prefix(pre)
 
 
+@pytest.mark.parametrize("grammar", ["list", "record"])
+def test_tiny_list_and_record_grammars(tiny, L, grammar):
+    """Collection and JSON-shaped outputs as token automata: a list of 1..3
+    items with a separator (quantifier {1,3}) and a two-field record; every
+    output is a string of the grammar, parity with the oracle (teacher-forced
+    where a sub-margin step diverged), and batching gives the same bits."""
+    from synth import automaton_of_list, automaton_of_record
+    w, orc, ctx = tiny
+    V = TINY.vocab
+    rng = np.random.default_rng(57)
+    ids = rng.choice(V, size=40, replace=False).astype(np.int32)
+    eos = int(ids[0])
+    if grammar == "list":
+        heads = ids[1:4]
+        items = [np.array([heads[0]]), np.array([heads[0], ids[4]]), np.array([heads[1], ids[5]]),
+                 np.array([heads[2]]), np.array([ids[6], ids[7]])]
+        aut = automaton_of_list(items, sep=int(ids[8]), lo=1, hi=3)
+    else:
+        aut = automaton_of_record(int(ids[9]), int(ids[10]), int(ids[11]),
+                                  [("enum", int(ids[12]), ids[13:18].tolist()),
+                                   ("int", int(ids[18]), ids[19:29].tolist(), 2)])
+    max_tokens = 8
+    wl = make_workload("filter_tiny", n_rows=48)
+    pre = ctx.set_prefix(wl.prefix)
+    kw = dict(eos=eos, max_tokens=max_tokens, prefix=pre)
+    _log(f"{grammar} grammar: eval")
+    out, dbg = ctx.eval_rows(wl.tokens, wl.offsets, L.LMOP_AUTOMATON, aut, debug_logits=True, **kw)
+    assert_automaton(out, aut, eos, max_tokens)
+    ref = orc.eval_rows(wl.prefix, [wl.suffix(r) for r in range(wl.n_rows)], KIND_AUTOMATON, aut,
+                        eos=eos, max_tokens=max_tokens, keep_logits=True)
+    forced = orc.eval_rows(wl.prefix, [wl.suffix(r) for r in range(wl.n_rows)], KIND_AUTOMATON,
+                           aut, eos=eos, max_tokens=max_tokens, keep_logits=True,
+                           forced=[out["tokens"][r][: out["n_tokens"][r]]
+                                   for r in range(wl.n_rows)])
+    st = compare(ref, out, dbg, grammar, orc_forced=forced)
+    _log(grammar, st)
+    assert len(set(map(tuple, out["tokens"].tolist()))) >= 2
+    for mbt in (40, 97):
+        o2, d2 = ctx.eval_rows(wl.tokens, wl.offsets, L.LMOP_AUTOMATON, aut, debug_logits=True,
+                               max_batch_tokens=mbt, **kw)
+        assert o2.tobytes() == out.tobytes() and np.array_equal(d2, dbg, equal_nan=True), mbt
+    ctx.release_prefix(pre)
+
+
 def _final_states(options, aut):
     off, tok, nxt = (np.asarray(aut.edge_offset), np.asarray(aut.edge_token),
                      np.asarray(aut.edge_next))

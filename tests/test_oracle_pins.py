@@ -2,6 +2,7 @@
 invariants, special cases that reduce to a few matrix products, and brute
 force on tiny inputs.  CPU only."""
 import dataclasses
+import itertools
 import json
 import math
 import os
@@ -13,8 +14,8 @@ import torch
 from oracle import (KIND_BOOL, KIND_ENUM, KIND_INT, OracleLM, attention, constrained_pick,
                     decode_nibbles, dequant, rms_norm, rope, silu)
 from oracle.lmop_oracle import KIND_AUTOMATON, automaton_steps, decode_e4m3, dequant_fp8
-from synth import (SHAPES, Automaton, ModelShape, make_weights, make_workload, option_trie,
-                   quantize_fp8_e4m3, quantize_int4_g32)
+from synth import (SHAPES, Automaton, ModelShape, automaton_of_list, automaton_of_record,
+                   make_weights, make_workload, option_trie, quantize_fp8_e4m3, quantize_int4_g32)
 
 GOLD = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -520,6 +521,115 @@ def test_automaton_endings(micro):
         assert res["value"][r] == (1 if toks == [5, 9] else 2)
     lp = res["logprob"]
     assert np.all(lp <= 0.0)
+
+
+def _language(aut, max_len):
+    """Every token string an output can be: the paths from state 0 that stop
+    in an accepting state (found by brute-force search)."""
+    out = set()
+
+    def walk(st, path):
+        if aut.accepting[st]:
+            out.add(tuple(path))
+        if len(path) < max_len:
+            for e in range(aut.edge_offset[st], aut.edge_offset[st + 1]):
+                walk(int(aut.edge_next[e]), path + [int(aut.edge_token[e])])
+
+    walk(0, [])
+    return out
+
+
+def _assert_deterministic(aut):
+    for st in range(aut.n_states):
+        t = aut.edge_token[aut.edge_offset[st]:aut.edge_offset[st + 1]].tolist()
+        assert len(set(t)) == len(t), st
+
+
+def test_list_automaton_language():
+    # items with a shared first token, one a prefix of another
+    items = [np.array(x) for x in ([4], [4, 9], [6], [7, 7])]
+    sep = 2
+    for lo, hi in ((1, 1), (1, 3), (2, 3), (3, 3)):
+        aut = automaton_of_list(items, sep=sep, lo=lo, hi=hi)
+        _assert_deterministic(aut)
+        want = set()
+        for n in range(lo, hi + 1):
+            for combo in itertools.product(items, repeat=n):
+                want.add(tuple(sum(([sep] * (j > 0) + it.tolist()
+                                    for j, it in enumerate(combo)), [])))
+        assert _language(aut, 3 * hi) == want, (lo, hi)
+    with pytest.raises(ValueError):
+        automaton_of_list(items, sep=9, lo=1, hi=2)   # the separator is an item token
+    with pytest.raises(ValueError):
+        automaton_of_list(items, sep=sep, lo=0, hi=2)
+    with pytest.raises(ValueError):
+        automaton_of_list(items, sep=sep, lo=3, hi=2)
+
+
+def test_record_automaton_language():
+    digits = list(range(10, 20))
+    fields = [("enum", 50, [60, 61, 62]), ("int", 51, digits, 2)]
+    aut = automaton_of_record(1, 3, 2, fields)
+    _assert_deterministic(aut)
+    want = {tuple([1, 50, v, 2, 51] + list(d) + [3])
+            for v in (60, 61, 62) for n in (1, 2) for d in itertools.product(digits, repeat=n)}
+    assert _language(aut, 12) == want
+    # one accepting state, without edges: a complete record ends the output
+    (end,) = np.flatnonzero(aut.accepting)
+    assert aut.edge_offset[end] == aut.edge_offset[end + 1]
+    with pytest.raises(ValueError):
+        automaton_of_record(1, 12, 2, fields)         # the closing token is a digit
+    with pytest.raises(ValueError):
+        automaton_of_record(1, 3, 2, [("int", 51, digits[:9], 2)])
+
+
+@pytest.mark.parametrize("grammar", ["list", "record"])
+def test_grammar_decode_matches_full_recompute(micro, grammar):
+    """Greedy constrained decoding over a list or record grammar: every output
+    is a string of the grammar, and each step's logits, pick and
+    log-probabilities equal a full recompute of the sequence so far."""
+    _, orc = micro
+    rng = np.random.default_rng(31)
+    eos = 91  # with these rows, some lists end early on EOS
+    if grammar == "list":
+        items = [np.array(x) for x in ([40, 2], [40, 7], [66], [21, 5])]
+        aut, max_tokens = automaton_of_list(items, sep=9, lo=1, hi=3), 8
+    else:
+        aut = automaton_of_record(30, 31, 32, [("enum", 33, [60, 61, 62]),
+                                               ("int", 34, list(range(70, 80)), 2)])
+        max_tokens = 8
+    lang = _language(aut, max_tokens)
+    g = automaton_steps(aut, eos=eos)
+    prefix = rng.integers(0, MICRO.vocab, size=5)
+    rows = _rand_rows(rng, 12, 1, 6, MICRO.vocab)
+    res = orc.eval_rows(prefix, rows, KIND_AUTOMATON, aut, eos=eos, max_tokens=max_tokens,
+                        keep_logits=True)
+    ends, eos_ends = 0, 0
+    for r in range(12):
+        n = res["n_tokens"][r]
+        toks = res["tokens"][r][:n].tolist()
+        body = toks[:-1] if toks[-1] == eos else toks
+        if res["value"][r] >= 0:
+            assert tuple(body) in lang
+            ends += 1
+            eos_ends += toks[-1] == eos
+        st, lp, lpf = 0, 0.0, 0.0
+        for s in range(n):
+            seq = np.concatenate([prefix, rows[r], toks[:s]])
+            z = orc.logits(orc.forward_sequence(seq)[-1])[0]
+            assert np.allclose(res["logits"][r][s], z, atol=1e-11)
+            allowed, to = g[st]
+            ci, a, b, _ = constrained_pick(z, allowed)
+            assert allowed[ci] == toks[s]
+            lp, lpf = lp + a, lpf + b
+            st = to[ci] if to[ci] is not None else st
+        assert math.isclose(res["logprob"][r], lp, abs_tol=1e-12)
+        assert math.isclose(res["logprob_full"][r], lpf, abs_tol=1e-12)
+    assert ends == 12
+    if grammar == "list":
+        assert 0 < eos_ends < 12  # both endings: EOS after fewer items, and {3} reached
+    else:
+        assert eos_ends == 0      # a complete record ends by itself
 
 
 def test_batch_and_order_invariance(micro):
