@@ -247,17 +247,26 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
 lmop_status lmop_dedup_rows(const int32_t* tokens, const int64_t* offsets, int32_t n_rows,
                             const int64_t* keys, int32_t* rep, int32_t* n_unique);
 
-/* Per-kernel timing of the ctx's launches, measured with HIP events on the
- * ctx stream while profiling is on (off by default). */
+/* Per-kernel timing of the ctx's launches while profiling is on (off by
+ * default).  Every launch is counted; a systematic sample is timed with HIP
+ * events on the ctx stream (the first, (N+1)-th, (2N+1)-th ... launch of
+ * each kernel for period N).  total_ms, flops and bytes cover the timed
+ * launches: their mean duration is total_ms / timed_launches. */
 typedef struct {
   char name[48];
-  int64_t launches;
-  double total_ms;
-  double flops; /* algorithmic FLOPs of those launches */
-  double bytes; /* algorithmic HBM bytes of those launches */
+  int64_t launches;       /* all launches while profiling was on */
+  int64_t timed_launches; /* the sampled ones */
+  double total_ms;        /* summed over the timed launches */
+  double flops;           /* algorithmic FLOPs of the timed launches */
+  double bytes;           /* algorithmic HBM bytes of the timed launches */
 } lmop_kernel_stat;
 
-lmop_status lmop_set_profiling(lmop_ctx* ctx, int32_t enable); /* also clears the counters */
+/* period 0 turns profiling off; period N >= 1 times every N-th launch of
+ * each kernel (1: all).  Each timed launch adds two events to the stream, so
+ * a period above 1 keeps the timing from slowing what it measures; a period
+ * with no common factor with the layer count samples every layer.  Clears
+ * the counters; INVALID_ARG for a negative period. */
+lmop_status lmop_set_profiling(lmop_ctx* ctx, int32_t period);
 lmop_status lmop_get_kernel_stats(lmop_ctx* ctx, lmop_kernel_stat* out, int32_t max_entries,
                                   int32_t* n_entries);
 

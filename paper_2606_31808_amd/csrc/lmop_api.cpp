@@ -45,8 +45,9 @@ struct LayerW {
 };
 
 struct Stat {
-  int64_t launches = 0;
-  double ms = 0, flops = 0, bytes = 0;
+  int64_t launches = 0;                 // all launches while profiling is on
+  int64_t timed = 0;                    // the sampled ones, timed with events
+  double ms = 0, flops = 0, bytes = 0;  // of the timed launches
 };
 
 struct Span {
@@ -124,7 +125,7 @@ struct lmop_ctx {
   Staging stage[2];
 
   // profiling
-  bool prof = false;
+  int32_t prof = 0;  // 0: off; N: every N-th launch of each kernel is timed
   std::vector<hipEvent_t> ev_free;
   std::vector<Span> spans;
   std::map<std::string, Stat> stats;
@@ -247,6 +248,10 @@ size_t stage_need(int T, int R, size_t n_work) {
 }
 
 // ---------------------------------------------------------------- profiling
+// Timing events are only read for elapsed times, so they are recorded
+// without the system-scope fence (a cache writeback and invalidate at every
+// record, which with two events per kernel both slowed the step and
+// perturbed the timed kernels).
 hipEvent_t take_event(lmop_ctx* c) {
   if (!c->ev_free.empty()) {
     hipEvent_t e = c->ev_free.back();
@@ -254,22 +259,28 @@ hipEvent_t take_event(lmop_ctx* c) {
     return e;
   }
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
   return e;
 }
 
 template <typename F>
 lmop_status timed(lmop_ctx* c, const char* name, double flops, double bytes, F&& launch) {
   hipEvent_t a = nullptr, b = nullptr;
-  if (c->prof) {
+  if (c->prof > 0 && c->stats[name].launches++ % c->prof == 0) {
     a = take_event(c);
     b = take_event(c);
-    if (a && b) HIP_OK(c, hipEventRecord(a, c->stream));
+    if (a && b) {
+      HIP_OK(c, hipEventRecord(a, c->stream));
+    } else {
+      if (a) c->ev_free.push_back(a);
+      if (b) c->ev_free.push_back(b);
+      a = b = nullptr;
+    }
   }
   hipError_t e = launch();
   if (e != hipSuccess) return fail(c, LMOP_ERR_DEVICE, "launch of %s failed: %s", name,
                                    hipGetErrorString(e));
-  if (c->prof && a && b) {
+  if (a && b) {
     HIP_OK(c, hipEventRecord(b, c->stream));
     c->spans.push_back(Span{name, a, b, flops, bytes});
   }
@@ -282,7 +293,7 @@ lmop_status resolve_spans(lmop_ctx* c) {
     float ms = 0.f;
     HIP_OK(c, hipEventElapsedTime(&ms, s.a, s.b));
     Stat& st = c->stats[s.name];
-    st.launches += 1;
+    st.timed += 1;
     st.ms += ms;
     st.flops += s.flops;
     st.bytes += s.bytes;
@@ -1806,10 +1817,11 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
   return LMOP_OK;
 }
 
-lmop_status lmop_set_profiling(lmop_ctx* ctx, int32_t enable) {
+lmop_status lmop_set_profiling(lmop_ctx* ctx, int32_t period) {
   if (!ctx) return LMOP_ERR_INVALID_ARG;
+  if (period < 0) return fail(ctx, LMOP_ERR_INVALID_ARG, "profiling period %d < 0", period);
   if (!ctx->host_only) LMOP_TRY(sync(ctx));
-  ctx->prof = enable != 0;
+  ctx->prof = period;
   ctx->stats.clear();
   return LMOP_OK;
 }
@@ -1826,6 +1838,7 @@ lmop_status lmop_get_kernel_stats(lmop_ctx* ctx, lmop_kernel_stat* out, int32_t 
       std::memset(&s, 0, sizeof s);
       std::snprintf(s.name, sizeof s.name, "%s", kv.first.c_str());
       s.launches = kv.second.launches;
+      s.timed_launches = kv.second.timed;
       s.total_ms = kv.second.ms;
       s.flops = kv.second.flops;
       s.bytes = kv.second.bytes;

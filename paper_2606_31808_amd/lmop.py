@@ -80,8 +80,8 @@ class lmop_eval_opts(C.Structure):
 
 
 class lmop_kernel_stat(C.Structure):
-    _fields_ = [("name", C.c_char * 48), ("launches", C.c_int64), ("total_ms", C.c_double),
-                ("flops", C.c_double), ("bytes", C.c_double)]
+    _fields_ = [("name", C.c_char * 48), ("launches", C.c_int64), ("timed_launches", C.c_int64),
+                ("total_ms", C.c_double), ("flops", C.c_double), ("bytes", C.c_double)]
 
 
 RESULT_DTYPE = np.dtype([("value", "<i8"), ("logprob", "<f4"), ("logprob_full", "<f4"),
@@ -298,8 +298,10 @@ def lmop_dedup_rows(tokens, offsets, keys=None):
     return rep, int(nu.value)
 
 
-def lmop_set_profiling(ctx, enable: bool) -> None:
-    _check(_lib.lmop_set_profiling(ctx, 1 if enable else 0), ctx)
+def lmop_set_profiling(ctx, period) -> None:
+    """period: False/0 off, True/1 time every launch, N time every N-th launch
+    of each kernel."""
+    _check(_lib.lmop_set_profiling(ctx, int(period)), ctx)
 
 
 def lmop_get_kernel_stats(ctx):
@@ -307,8 +309,8 @@ def lmop_get_kernel_stats(ctx):
     _check(_lib.lmop_get_kernel_stats(ctx, None, 0, C.byref(n)), ctx)
     arr = (lmop_kernel_stat * max(n.value, 1))()
     _check(_lib.lmop_get_kernel_stats(ctx, arr, n.value, C.byref(n)), ctx)
-    return {arr[i].name.decode(): dict(launches=arr[i].launches, ms=arr[i].total_ms,
-                                       flops=arr[i].flops, bytes=arr[i].bytes)
+    return {arr[i].name.decode(): dict(launches=arr[i].launches, timed=arr[i].timed_launches,
+                                       ms=arr[i].total_ms, flops=arr[i].flops, bytes=arr[i].bytes)
             for i in range(n.value)}
 
 
@@ -361,8 +363,8 @@ class Context:
                               row_prefix, flags, max_batch_tokens, debug_logits, self.vocab,
                               limit, limit_value, row_mask)
 
-    def set_profiling(self, on: bool):
-        lmop_set_profiling(self.ctx, on)
+    def set_profiling(self, period):
+        lmop_set_profiling(self.ctx, period)
 
     def kernel_stats(self):
         return lmop_get_kernel_stats(self.ctx)

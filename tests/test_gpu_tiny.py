@@ -597,6 +597,31 @@ def test_tiny_mixed_features_random(tiny, L, seed):
     ctx.release_prefix(root)
 
 
+def test_tiny_sampled_profiling(tiny, L):
+    """Kernel timing on a sample: every launch is counted, the first and then
+    every period-th launch of each kernel is timed; the results do not
+    change."""
+    w, orc, ctx = tiny
+    wl = make_workload("filter_tiny", n_rows=40)
+    pre = ctx.set_prefix(wl.prefix)
+    ref, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, prefix=pre,
+                           max_batch_tokens=97)
+    counts = {}
+    for period in (1, 3):
+        ctx.set_profiling(period)
+        out, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, prefix=pre,
+                               max_batch_tokens=97)
+        st = ctx.kernel_stats()
+        ctx.set_profiling(0)
+        assert out.tobytes() == ref.tobytes()
+        for name, s in st.items():
+            assert s["timed"] == (s["launches"] + period - 1) // period, (name, s)
+            assert s["ms"] > 0 and s["flops"] >= 0
+        counts[period] = {k: v["launches"] for k, v in st.items()}
+    assert counts[1] == counts[3] and counts[1]["gemm_w4a16_qkv"] >= 2 * TINY.n_layers
+    ctx.release_prefix(pre)
+
+
 def test_tiny_restricted_head(tiny, L):
     """Restricted head: only the allowed tokens' logits are computed; typed
     outputs and allowed-set log-probabilities match the oracle and the full

@@ -257,6 +257,15 @@ def test_automaton_validation(tiny_w):
     _expect(L.LMOP_ERR_INVALID_ARG, run, big)
 
 
+def test_profiling_period_validation():
+    ctx = _host_ctx()
+    _expect(-1, ctx.set_profiling, -1)
+    for period in (0, 1, 5, True, False):
+        ctx.set_profiling(period)
+    assert ctx.kernel_stats() == {}
+    ctx.close()
+
+
 def test_binding_constants_match_header():
     """The flag values the binding passes are the header's."""
     hdr = open(os.path.join(ROOT, "include", "lmop.h")).read()
