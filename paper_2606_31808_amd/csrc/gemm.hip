@@ -93,7 +93,7 @@ LMOP_DEVICE int swz(int row) { return row & 7; }
 
 constexpr int BK = 64;
 constexpr int BN4 = 256;   // int4 GEMMs: 4 waves x 64 columns
-constexpr int GM = 8;      // token tiles per L2 group
+constexpr int GM = 4;      // token tiles per L2 group
 constexpr int NSTAGE = 3;  // LDS ring depth
 
 // weight formats of the kernel's A operand
