@@ -167,8 +167,9 @@ def mfma_summary(root):
             return {"1": "W4A16 GEMM, residual add (o, down)", "2": "W4A16 GEMM, SwiGLU (gate/up)",
                     "4": "W4A16 GEMM, QKV + RoPE (qkv)", "0": "W4A16 GEMM, fp16 store"}.get(epi, epi)
         if "gemm_kernel<" in name:
-            fmt = name.split("gemm_kernel<")[1].split(",")[1].strip()
-            return "W8A16 GEMM (FP8 weights)" if fmt == "2" else "LM head GEMM"
+            return "W8A16 GEMM (FP8 weights)"
+        if "head_kernel" in name:
+            return "LM head GEMM"
         if "attn_kernel" in name:
             return "attention"
         return None

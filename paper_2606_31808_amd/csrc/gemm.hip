@@ -33,9 +33,8 @@
 // v_cvt_scalef32_pk_f16_fp8 (every E4M3 value is an fp16 value); the
 // per-column scale multiplies the fp32 accumulator before the epilogue.
 //
-// The LM head (fp16 weight, M = vocabulary, N = tokens) has 4 or 8 waves (8:
-// one LDS tile of the head weight serves up to 512 token rows); its token
-// rows are private to a wave and go from global memory straight to registers.
+// The LM head (fp16 weight, M = vocabulary, N = token rows) has a kernel of
+// its own at the end of this file.
 //
 // Workgroups are mapped to tiles XCD-aware: the hardware deals workgroups to
 // the 8 XCDs round-robin, so each XCD is given one contiguous range of
@@ -96,23 +95,18 @@ constexpr int BN4 = 256;   // int4 GEMMs: 4 waves x 64 columns
 constexpr int GM = 4;      // token tiles per L2 group
 constexpr int NSTAGE = 3;  // LDS ring depth
 
-// weight formats of the kernel's A operand
-constexpr int WF_F16 = 0;   // fp16 (the LM head; its token rows bypass LDS)
+// weight formats of the kernel's weight operand
 constexpr int WF_INT4 = 1;  // int4, one fp16 scale per 32 features
 constexpr int WF_FP8 = 2;   // OCP E4M3, one fp32 scale per output column
 
 template <int MI, int WF, int NW_ = 4>
 struct Cfg {
-  // waves per workgroup, side by side along N (64 columns each): 4 for the
-  // int4 GEMMs; 4 or 8 for the LM head (8: up to 512 token rows share each
-  // LDS tile of the head weight)
+  // waves per workgroup, side by side along N (64 columns each)
   static constexpr int NW = NW_;
   static constexpr int BN = 64 * NW;
   static constexpr int BM = 16 * MI;
   static constexpr int A_BYTES = BM * 128;
-  // the fp16 operand of the LM head is private to each wave and goes from
-  // global memory straight to registers, so it takes no LDS
-  static constexpr int B_BYTES = WF == WF_INT4 ? BN * 32 : WF == WF_FP8 ? BN * 64 : 0;
+  static constexpr int B_BYTES = WF == WF_INT4 ? BN * 32 : BN * 64;
   static constexpr int S_BYTES = WF == WF_INT4 ? 1024 : 0;
   static constexpr int STAGE = A_BYTES + B_BYTES + S_BYTES;
   static constexpr int NS = WF == WF_FP8 ? 2 : NSTAGE;  // ring stages
@@ -133,8 +127,7 @@ struct Occ {
 };
 
 template <int MI, int WF, int EPI, int NW_ = 4>
-__global__ __launch_bounds__((64 * NW_), (NW_ == 4 ? Occ<MI>::value : 1)) void gemm_kernel(
-    const GemmArgs p) {
+__global__ __launch_bounds__((64 * NW_), Occ<MI>::value) void gemm_kernel(const GemmArgs p) {
   constexpr bool INT4 = WF == WF_INT4;
   using C = Cfg<MI, WF, NW_>;
   constexpr int BM = C::BM, BN = C::BN, NW = C::NW;
@@ -309,65 +302,6 @@ __global__ __launch_bounds__((64 * NW_), (NW_ == 4 ? Occ<MI>::value : 1)) void g
         __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);  // VALU
       }
     }
-  } else {
-    // LM head: the vocabulary tile (A) streams through the LDS ring; each
-    // wave's 64 token rows (B) are loaded from global memory into registers
-    // one K step ahead.  Within a step the token loads are issued before the
-    // next stage's LDS loads, so the same vmcnt wait covers both.  Rows past
-    // the last token load the last token (their results are never stored).
-    const f16* brow[4];
-#pragma unroll
-    for (int f = 0; f < 4; ++f) {
-      int r = n0 + wave * 64 + 16 * f + c;
-      r = r < p.N ? r : p.N - 1;
-      brow[f] = (const f16*)p.bh + (size_t)r * p.ldb + 8 * g;
-    }
-    // a wave whose 64 token rows all lie past the last token only helps load
-    // the shared vocabulary tile (the vmcnt waits count that tile's loads
-    // only, so skipping the token loads keeps them valid)
-    const bool wave_active = n0 + wave * 64 < p.N;
-    auto load_b = [&](f16x8(&bb)[2][4], int kt) {
-      if (!wave_active) return;
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int f = 0; f < 4; ++f) bb[kk][f] = *(const f16x8*)(brow[f] + kt * BK + kk * 32);
-    };
-    auto step = [&](int kt, const f16x8(&bc)[2][4], f16x8(&bn)[2][4]) {
-      if (kt + 1 < KT)
-        wait_vmcnt<C::LOADS>();
-      else
-        wait_vmcnt<0>();
-      barrier();
-      if (kt + 1 < KT) load_b(bn, kt + 1);
-      if (kt + 2 < KT) issue((kt + 2) % NSTAGE, kt + 2);
-      if (!wave_active) return;
-      const char* sA = smem + (kt % NSTAGE) * C::STAGE;
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        f16x8 a[MI];
-#pragma unroll
-        for (int i = 0; i < MI; ++i) {
-          const int r = 16 * i + c;
-          a[i] = *(const f16x8*)(sA + r * 128 + (((kk * 4 + g) ^ swz(r)) * 16));
-        }
-#pragma unroll
-        for (int f = 0; f < 4; ++f) {
-          // ragged token tiles: skip sub-tiles with no valid token
-          if (n0 + wave * 64 + 16 * f >= p.N) continue;
-#pragma unroll
-          for (int i = 0; i < MI; ++i) acc[f][i] = mfma16x16x32(bc[kk][f], a[i], acc[f][i]);
-        }
-      }
-    };
-    f16x8 b0[2][4], b1[2][4];
-    issue(0, 0);
-    load_b(b0, 0);
-    if (KT > 1) issue(1, 1);
-    for (int kt = 0; kt < KT; kt += 2) {
-      step(kt, b0, b1);
-      if (kt + 1 < KT) step(kt + 1, b1, b0);
-    }
   }
 
   // ------------------------------------------------------------ epilogue
@@ -484,39 +418,6 @@ __global__ __launch_bounds__((64 * NW_), (NW_ == 4 ? Occ<MI>::value : 1)) void g
         }
       }
     }
-  } else {  // EPI_HEAD: rows of A are vocabulary entries, rows of B are tokens
-    // per token n and this workgroup's 16*MI-entry vocabulary slice (chunk mt):
-    // (max, sum exp(z - max)), plus the logits of the allowed tokens
-    const int n_chunks = (p.M + BM - 1) / BM;
-#pragma unroll
-    for (int f = 0; f < 4; ++f)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int n = ncol + 16 * f + r;  // token
-        float mx = -INFINITY;
-#pragma unroll
-        for (int i = 0; i < MI; ++i)
-          if (mrow + 16 * i < p.M) mx = fmaxf(mx, acc[f][i][r]);
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, shfl_xor(mx, o));
-        float sm = 0.f;
-#pragma unroll
-        for (int i = 0; i < MI; ++i) {
-          const int v = mrow + 16 * i;  // vocabulary entry
-          if (v < p.M) {
-            const float z = acc[f][i][r];
-            sm += __expf(z - mx);
-            if (n < p.N) {
-              const int si = p.sel[v];
-              if (si >= 0) p.zsel[(size_t)n * p.n_sel + si] = z;
-              if (p.dump) p.dump[(size_t)n * p.ld_dump + v] = z;
-            }
-          }
-        }
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) sm += shfl_xor(sm, o);
-        if (c == 0 && n < p.N) p.part[(size_t)n * n_chunks + mt] = make_float2(mx, sm);
-      }
   }
 }
 
@@ -543,7 +444,200 @@ hipError_t launch_epi(hipStream_t s, const GemmArgs& a) {
   return launch_cfg<2, WF, EPI>(s, a);
 }
 
+// ---------------------------------------------------------------- LM head
+// z = W_lm . h for R token rows: the head weight W_lm fp16 [V][K] is the
+// vocabulary operand (M), the final-normalised rows h fp16 [R][K] the token
+// operand (N); both stream through a three-stage LDS ring by direct
+// global->LDS loads, 32 features per step in 64-byte LDS rows.  A workgroup
+// holds 16*MI = 128 vocabulary entries and 64*F = 256 token rows: four waves
+// side by side along the tokens (64 rows each) share the vocabulary tile;
+// 72 KB of LDS, two workgroups per CU.  The log-sum-exp partials are per
+// 128-entry vocabulary chunk whatever the number of rows, so a row's
+// log-probabilities do not depend on how rows are batched.  (Loading each
+// wave's token rows straight into registers instead was measured ~35%
+// slower: those loads, not LDS, bounded the head.  A 96 x 320 tile for
+// 257..320 rows was 7% faster there but changes the chunking.)
+template <int MI_, int F_>
+struct HeadCfg {
+  static constexpr int MI = MI_, F = F_;
+  static constexpr int BK = 32, NW = 4, NS = 3;
+  static constexpr int BM = 16 * MI, BN = NW * 16 * F;
+  static constexpr int A_BYTES = BM * 64, T_BYTES = BN * 64;
+  static constexpr int STAGE = A_BYTES + T_BYTES;
+  static constexpr int LDS = NS * STAGE;
+  static_assert(LDS <= 80 * 1024, "two workgroups per CU");
+  // 16 rows per instruction; surplus waves repeat the last vocabulary block
+  static constexpr int A_LOADS = (MI + NW - 1) / NW;
+  static constexpr int T_LOADS = F;  // a wave's own token blocks
+};
+
+// 16-byte chunk swizzle of a 64-byte LDS row: the 8 lanes a ds_read_b128
+// serves together (rows c .. c+7 of a fragment, one chunk) fall on 8
+// distinct 16-byte bank groups of a 128-byte window
+LMOP_DEVICE int swz64(int row) { return (row >> 1) & 3; }
+
+template <int MI, int F>
+__global__ __launch_bounds__(256, 2) void head_kernel(const GemmArgs p) {
+  using C = HeadCfg<MI, F>;
+  constexpr int BK = C::BK, BM = C::BM, BN = C::BN, NW = C::NW, NS = C::NS;
+  constexpr int A_BYTES = C::A_BYTES, STAGE = C::STAGE;
+  constexpr int A_LOADS = C::A_LOADS, T_LOADS = C::T_LOADS;
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 4, c = lane & 15;
+
+  // XCD-aware tile order as in gemm_kernel: the token tiles of one
+  // vocabulary tile run side by side on one XCD, so the head weight streams
+  // from HBM about once
+  const int ntm = (p.M + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
+  const int total = ntm * ntn;
+  const int b = blockIdx.x;
+  const int xcd = b & 7, j = b >> 3;
+  const int per = total >> 3, rem = total & 7;
+  const int logical = xcd * per + (xcd < rem ? xcd : rem) + j;
+  const int grp = logical / (GM * ntn);
+  const int within = logical - grp * GM * ntn;
+  const int gsz = (ntm - grp * GM) < GM ? (ntm - grp * GM) : GM;
+  const int mt = grp * GM + within % gsz;
+  const int nt = within / gsz;
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int w0 = n0 + wave * 16 * F;  // this wave's first token row
+  const int KT = p.K / BK;
+  const f16* W = (const f16*)p.A;
+  const f16* H = (const f16*)p.bh;
+
+  // one instruction fills 16 rows x 64 bytes: lane L writes row L/4, chunk
+  // L%4, and reads the swizzled source chunk for it.  A wave loads only its
+  // 16-row blocks that hold a token row (the rest of its LDS rows are stale
+  // and feed only results that are never stored), so the number of loads it
+  // has in flight per K step is its own constant.
+  const int rr = lane >> 2, pc = lane & 3;
+  int tb = (p.N - w0 + 15) / 16;
+  tb = tb < 0 ? 0 : (tb > T_LOADS ? T_LOADS : tb);
+  // wave-uniform, so a skipped load is a scalar branch, never an issued
+  // instruction with no active lane
+  const int t_blocks = __builtin_amdgcn_readfirstlane(tb);
+  const int my_loads = A_LOADS + t_blocks;
+  auto issue = [&](int st, int kt) {
+    char* sA = smem + st * STAGE;
+    char* sT = sA + A_BYTES;
+#pragma unroll
+    for (int i = 0; i < A_LOADS; ++i) {
+      int q = wave + NW * i;
+      if (q >= MI) q = MI - 1;
+      const int r = q * 16 + rr;
+      int gm = m0 + r;
+      gm = gm < p.M ? gm : p.M - 1;
+      g2l16(W + (size_t)gm * p.lda + kt * BK + (pc ^ swz64(r)) * 8, sA + q * 1024);
+    }
+#pragma unroll
+    for (int i = 0; i < T_LOADS; ++i) {
+      if (i >= t_blocks) break;
+      const int q = wave * T_LOADS + i;  // the wave's own rows
+      const int r = q * 16 + rr;
+      int gn = n0 + r;
+      gn = gn < p.N ? gn : p.N - 1;
+      g2l16(H + (size_t)gn * p.ldb + kt * BK + (pc ^ swz64(r)) * 8, sT + q * 1024);
+    }
+  };
+
+  f32x4 acc[F][MI];
+#pragma unroll
+  for (int f = 0; f < F; ++f)
+#pragma unroll
+    for (int i = 0; i < MI; ++i) acc[f][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const bool wave_active = w0 < p.N;
+  issue(0, 0);
+  if (KT > 1) issue(1, 1);
+  for (int kt = 0; kt < KT; ++kt) {
+    // this step's stage is complete once at most the next step's loads are in flight
+    if (kt + 1 < KT)
+      wait_vmcnt_upto8(my_loads);
+    else
+      wait_vmcnt<0>();
+    barrier();
+    if (kt + 2 < KT) issue((kt + 2) % NS, kt + 2);
+    if (wave_active) {
+      const char* sA = smem + (kt % NS) * STAGE;
+      const char* sT = sA + A_BYTES;
+      f16x8 a[MI], t[F];
+#pragma unroll
+      for (int i = 0; i < MI; ++i) {
+        const int r = 16 * i + c;
+        a[i] = *(const f16x8*)(sA + r * 64 + ((g ^ swz64(r)) * 16));
+      }
+#pragma unroll
+      for (int f = 0; f < F; ++f) {
+        const int r = wave * 16 * F + 16 * f + c;
+        t[f] = *(const f16x8*)(sT + r * 64 + ((g ^ swz64(r)) * 16));
+      }
+#pragma unroll
+      for (int f = 0; f < F; ++f)
+#pragma unroll
+        for (int i = 0; i < MI; ++i) acc[f][i] = mfma16x16x32(t[f], a[i], acc[f][i]);
+    }
+  }
+
+  // acc[f][i][r] = z[vocabulary m0 + 16i + c][token w0 + 16f + 4g + r].
+  // Per token and this workgroup's vocabulary chunk mt: (max, sum exp(z -
+  // max)), plus the logits of the allowed tokens
+  const int mrow = m0 + c;
+  const int ncol = w0 + 4 * g;
+  const int n_chunks = ntm;
+#pragma unroll
+  for (int f = 0; f < F; ++f)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int n = ncol + 16 * f + r;  // token
+      float mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+        if (mrow + 16 * i < p.M) mx = fmaxf(mx, acc[f][i][r]);
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, shfl_xor(mx, o));
+      float sm = 0.f;
+#pragma unroll
+      for (int i = 0; i < MI; ++i) {
+        const int v = mrow + 16 * i;  // vocabulary entry
+        if (v < p.M) {
+          const float z = acc[f][i][r];
+          sm += __expf(z - mx);
+          if (n < p.N) {
+            const int si = p.sel[v];
+            if (si >= 0) p.zsel[(size_t)n * p.n_sel + si] = z;
+            if (p.dump) p.dump[(size_t)n * p.ld_dump + v] = z;
+          }
+        }
+      }
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) sm += shfl_xor(sm, o);
+      if (c == 0 && n < p.N) p.part[(size_t)n * n_chunks + mt] = make_float2(mx, sm);
+    }
+}
+
+template <int MI, int F>
+hipError_t launch_head(hipStream_t s, const GemmArgs& a) {
+  using C = HeadCfg<MI, F>;
+  const int tiles = ((a.M + C::BM - 1) / C::BM) * ((a.N + C::BN - 1) / C::BN);
+  if (tiles == 0) return hipSuccess;
+  static const hipError_t attr = hipFuncSetAttribute(
+      (const void*)head_kernel<MI, F>, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((head_kernel<MI, F>), dim3(tiles), dim3(256), C::LDS, s, a);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_gemm_f16(hipStream_t s, const GemmArgs& a, int epi) {
+  static_assert(HeadCfg<8, 4>::BM == kHeadVocabChunk, "partials per vocabulary chunk");
+  if (a.K % 32 != 0 || epi != EPI_HEAD || a.ldb % 8 != 0 || a.lda % 8 != 0)
+    return hipErrorInvalidValue;
+  return launch_head<8, 4>(s, a);
+}
 
 hipError_t launch_gemm_w4(hipStream_t s, const GemmArgs& a, int epi) {
   // the packed weight is padded to 256 columns so every tile shape divides it
@@ -567,17 +661,6 @@ hipError_t launch_gemm_w8(hipStream_t s, const GemmArgs& a, int epi) {
     case EPI_QKV: return launch_epi<WF_FP8, EPI_QKV>(s, a);
     default: return hipErrorInvalidValue;
   }
-}
-
-hipError_t launch_gemm_f16(hipStream_t s, const GemmArgs& a, int epi) {
-  if (a.K % BK != 0 || epi != EPI_HEAD || a.ldb % 8 != 0) return hipErrorInvalidValue;
-  // vocabulary along M in 128-entry tiles, tokens in 256- or 512-row column
-  // tiles; the column tiles of one vocabulary tile run side by side on one
-  // XCD, so the LM head weight streams from HBM about once
-  // up to 256 token rows: 4 waves (two workgroups per CU stream the weight);
-  // more: 8 waves, so up to 512 rows share each weight tile
-  if (a.N <= 256) return launch_cfg<8, WF_F16, EPI_HEAD, 4>(s, a);
-  return launch_cfg<8, WF_F16, EPI_HEAD, 8>(s, a);
 }
 
 }  // namespace lmop

@@ -78,6 +78,9 @@ struct GemmArgs {
 hipError_t launch_gemm_w4(hipStream_t s, const GemmArgs& a, int epi);
 hipError_t launch_gemm_w8(hipStream_t s, const GemmArgs& a, int epi);  // FP8 weights
 hipError_t launch_gemm_f16(hipStream_t s, const GemmArgs& a, int epi);  // head only
+// the head writes one (max, sum exp) partial per row and chunk of this many
+// vocabulary entries, for any number of rows
+constexpr int kHeadVocabChunk = 128;
 
 // Repacks one source matrix's rows into columns of a packed weight.
 // colsrc[j] (device, [np]): (source index << 24) | source row, or -1 (zero column).

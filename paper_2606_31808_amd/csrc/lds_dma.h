@@ -43,6 +43,21 @@ LMOP_DEVICE void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// s_waitcnt vmcnt(n) for a wave-uniform n in 0..8 known only at run time
+LMOP_DEVICE void wait_vmcnt_upto8(int n) {
+  switch (n) {
+    case 0: wait_vmcnt<0>(); break;
+    case 1: wait_vmcnt<1>(); break;
+    case 2: wait_vmcnt<2>(); break;
+    case 3: wait_vmcnt<3>(); break;
+    case 4: wait_vmcnt<4>(); break;
+    case 5: wait_vmcnt<5>(); break;
+    case 6: wait_vmcnt<6>(); break;
+    case 7: wait_vmcnt<7>(); break;
+    default: wait_vmcnt<8>(); break;
+  }
+}
+
 // workgroup barrier without the memory fence of __syncthreads (which would
 // wait for every outstanding load, including the prefetches in flight);
 // the empty asm statements keep the compiler from moving memory accesses

@@ -828,8 +828,7 @@ lmop_status run_head(lmop_ctx* c, int k, int R, const std::vector<const float*>&
                      const std::vector<int32_t>* states = nullptr) {
   const lmop_config& cf = c->cfg;
   const int d = cf.d_model, V = cf.vocab;
-  constexpr int kVocabTile = 128;
-  const int n_chunks = (V + kVocabTile - 1) / kVocabTile;
+  const int n_chunks = (V + kHeadVocabChunk - 1) / kHeadVocabChunk;
   const float** drp;
   uint16_t* hn;
   float2* part;
