@@ -1,8 +1,8 @@
 // W4A16 GEMM for gfx950: C = A . deq(W)^T with A fp16 [M][K] (tokens x
 // features), W int4 [N][K] with one fp16 scale per 32 input features, fp32
 // accumulation on MFMA 16x16x32 f16.  The same body serves FP8 weights (OCP
-// E4M3 codes, one fp32 scale per output column: the FP8 checkpoint layout)
-// and, with an fp16 weight, the LM head.
+// E4M3 codes, one fp32 scale per output column: the FP8 checkpoint layout).
+// The LM head (fp16 weight) is a kernel of its own at the end of the file.
 //
 // Tiling.  4 waves side by side along N; a wave owns all (16*MI) tokens of
 // the tile and 64 output columns, the workgroup (16*MI) x 256.  K advances
@@ -32,9 +32,6 @@
 // workgroups per CU).  A lane's 8 codes convert to fp16 exactly with four
 // v_cvt_scalef32_pk_f16_fp8 (every E4M3 value is an fp16 value); the
 // per-column scale multiplies the fp32 accumulator before the epilogue.
-//
-// The LM head (fp16 weight, M = vocabulary, N = token rows) has a kernel of
-// its own at the end of this file.
 //
 // Workgroups are mapped to tiles XCD-aware: the hardware deals workgroups to
 // the 8 XCDs round-robin, so each XCD is given one contiguous range of
