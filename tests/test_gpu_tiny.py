@@ -622,6 +622,40 @@ def test_tiny_sampled_profiling(tiny, L):
     ctx.release_prefix(pre)
 
 
+def test_ragged_vocab_and_wide_batch(L):
+    """A vocabulary that is not a multiple of the head's 128-entry chunk
+    (1,999 = 15 x 128 + 79) and a batch of 300 rows (two 256-row column
+    tiles in the head): logits and typed outputs against the oracle, every
+    row; the same bits when the rows are batched in small pieces."""
+    shape = dataclasses.replace(TINY, name="tiny_v1999", vocab=1999, n_layers=1, shape_id=7)
+    w = make_weights(shape, seed=99)
+    orc = OracleLM(w, shape)
+    ctx = L.Context(shape, device=0)
+    ctx.load_weights(w)
+    rng = np.random.default_rng(12)
+    prefix = rng.integers(0, shape.vocab, size=40).astype(np.int32)
+    rows = [rng.integers(0, shape.vocab, size=int(rng.integers(1, 6))).astype(np.int32)
+            for _ in range(300)]
+    offs = np.concatenate([[0], np.cumsum([len(r) for r in rows])])
+    toks = np.concatenate(rows)
+    # allowed tokens include the last vocabulary entries (the ragged chunk)
+    allowed = np.array([1998, 1990, 1920, 5, 700], dtype=np.int32)
+    pre = ctx.set_prefix(prefix)
+    _log("ragged vocab: eval 300 rows in one batch")
+    out, dbg = ctx.eval_rows(toks, offs, KIND_ENUM, allowed, prefix=pre, debug_logits=True,
+                             no_dedup=True)
+    ref = orc.eval_rows(prefix, rows, KIND_ENUM, allowed, keep_logits=True)
+    st = compare(ref, out, dbg, "ragged vocab")
+    _log("ragged vocab", st)
+    assert st["exact_checked"] >= 200
+    assert_typed(out, KIND_ENUM, len(allowed), allowed)
+    o2, d2 = ctx.eval_rows(toks, offs, KIND_ENUM, allowed, prefix=pre, debug_logits=True,
+                           no_dedup=True, max_batch_tokens=37)
+    assert o2.tobytes() == out.tobytes() and np.array_equal(d2, dbg)
+    ctx.release_prefix(pre)
+    ctx.close()
+
+
 def test_tiny_restricted_head(tiny, L):
     """Restricted head: only the allowed tokens' logits are computed; typed
     outputs and allowed-set log-probabilities match the oracle and the full
