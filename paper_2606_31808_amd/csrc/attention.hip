@@ -16,7 +16,8 @@
 // K/V tile reads.  Keys are walked segment by segment (root prefix, child
 // prefix, own) in blocks of 64 through a two-stage LDS ring (one barrier per
 // block: the next block's loads are issued right after it).  Each wave owns
-// 32 query vectors and keeps an online softmax (fp32 reference maximum and
+// 16 (hd 128) or 32 (hd 64) query vectors and keeps an online softmax (fp32
+// reference maximum and
 // sum, base-2 exponent); the reference maximum moves only when a score
 // exceeds it by a wide margin, so the running output is rarely rescaled.
 // Waves whose query vectors all lie past the row's end only help load.  Scores are computed transposed, S^T = K Q^T, so
@@ -31,8 +32,13 @@ namespace lmop {
 namespace {
 
 constexpr int KB = 64;   // keys per block
-constexpr int QW = 32;   // query vectors per wave
 constexpr int QT = ATTN_QTILE;  // query vectors per workgroup
+// waves per workgroup: with hd = 128, 8 waves of 16 query vectors (4 waves
+// per SIMD hide more of each block's score -> softmax -> P.V chain than 4
+// waves of 32; measured 6% faster); with hd = 64 a wave's block is already
+// short, and 4 waves of 32 are 6% faster
+template <int HD>
+constexpr int attn_waves() { return HD == 128 ? 8 : 4; }
 
 // Key order inside a 32-key chunk: score tile hf (0, 1) row m = 4a + b
 // (a, b in 0..3) holds key 8a + 4hf + b, so that the MFMA result layout puts
@@ -75,12 +81,16 @@ LMOP_DEVICE float sum_x32(float x) {
 }
 
 template <int HD>
-__global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float scale_log2) {
+__global__ __launch_bounds__(64 * attn_waves<HD>(), 2) void attn_kernel(const AttnArgs p,
+                                                                         float scale_log2) {
+  constexpr int NWV = attn_waves<HD>();
+  constexpr int QW = QT / NWV;  // query vectors per wave
+  constexpr int QS = QW / 16;   // 16-vector query sub-tiles per wave
   constexpr int K_BYTES = KB * HD * 2;
   constexpr int V_BYTES = HD * KB * 2;
   constexpr int STAGE = K_BYTES + V_BYTES;
-  constexpr int K_LOADS = K_BYTES / 1024 / 4;  // per wave
-  constexpr int V_LOADS = V_BYTES / 1024 / 4;
+  constexpr int K_LOADS = K_BYTES / 1024 / NWV;  // per wave
+  constexpr int V_LOADS = V_BYTES / 1024 / NWV;
   constexpr int NS = HD / 32;  // k-steps of the score MFMA
   constexpr int NT = HD / 16;  // 16-dim output tiles
   constexpr int KCH = HD / 8;  // 16-byte chunks per K row
@@ -123,14 +133,14 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
   uint32_t koff[K_LOADS], vdim[V_LOADS], vchunk[V_LOADS];
 #pragma unroll
   for (int i = 0; i < K_LOADS; ++i) {
-    const int q = wave + 4 * i;  // 1 KB = 1024 / (2*HD) keys
+    const int q = wave + NWV * i;  // 1 KB = 1024 / (2*HD) keys
     const int key = q * (512 / HD) + lane / KCH;
     const int chunk = (lane % KCH) ^ kswz<HD>(key);
     koff[i] = (uint32_t)(key * kvdim + h * HD + chunk * 8) * 2u;
   }
 #pragma unroll
   for (int i = 0; i < V_LOADS; ++i) {
-    const int q = wave + 4 * i;  // 8 dim rows of 128 bytes
+    const int q = wave + NWV * i;  // 8 dim rows of 128 bytes
     const int dim = q * 8 + (lane >> 3);
     vdim[i] = (uint32_t)dim;
     vchunk[i] = (uint32_t)(((lane & 7) ^ vswz(dim)) * 16);
@@ -164,10 +174,10 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
   auto issue = [&](int st) {
     const uint32_t mk = lds0 + (uint32_t)(st * STAGE);
 #pragma unroll
-    for (int i = 0; i < K_LOADS; ++i) g2l16_m0(la.k, koff[i], mk + 4096u * i);
+    for (int i = 0; i < K_LOADS; ++i) g2l16_m0(la.k, koff[i], mk + 1024u * NWV * i);
 #pragma unroll
     for (int i = 0; i < V_LOADS; ++i)
-      g2l16_m0(la.v, __umul24(vdim[i], la.vrow) + vchunk[i], mk + K_BYTES + 4096u * i);
+      g2l16_m0(la.v, __umul24(vdim[i], la.vrow) + vchunk[i], mk + K_BYTES + 1024u * NWV * i);
     lkb += KB;
     la.k += (size_t)KB * kvdim * 2;
     la.v += KB * 2;
@@ -178,13 +188,13 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
     }
   };
 
-  // this lane's query vectors: v = tile*128 + wave*32 + 16*qs + c
-  f16x8 qf[2][NS];
-  int n_vis[2];  // own keys visible to the query (prefix keys are all visible)
-  bool qvalid[2];
-  int tok[2], hq[2];
+  // this lane's query vectors: v = tile*128 + wave*QW + 16*qs + c
+  f16x8 qf[QS][NS];
+  int n_vis[QS];  // own keys visible to the query (prefix keys are all visible)
+  bool qvalid[QS];
+  int tok[QS], hq[QS];
 #pragma unroll
-  for (int qs = 0; qs < 2; ++qs) {
+  for (int qs = 0; qs < QS; ++qs) {
     const int v = wk.y * QT + wave * QW + 16 * qs + c;
     const int t = v / G;
     qvalid[qs] = t < row.n_q;
@@ -201,12 +211,14 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
     }
   }
 
-  f32x4 o[2][NT];
+  f32x4 o[QS][NT];
 #pragma unroll
-  for (int qs = 0; qs < 2; ++qs)
+  for (int qs = 0; qs < QS; ++qs)
 #pragma unroll
     for (int i = 0; i < NT; ++i) o[qs][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run[2] = {-1e30f, -1e30f}, l_run[2] = {0.f, 0.f};
+  float m_run[QS], l_run[QS];
+#pragma unroll
+  for (int qs = 0; qs < QS; ++qs) m_run[qs] = -1e30f, l_run[qs] = 0.f;
   const float thr = 8.0f / scale_log2;
 
   // a wave whose query vectors all lie past the row's end only helps load
@@ -240,7 +252,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
 
     // S^T tiles kt = 2*kc + hf: register r of lane group g holds key
     // kb + 32*kc + 8g + 4hf + r, query (qs, c)
-    f32x4 st[2][4];
+    f32x4 st[QS][4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
       f16x8 a[NS];
@@ -249,7 +261,7 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
       for (int ks = 0; ks < NS; ++ks)
         a[ks] = *(const f16x8*)(sK + key * (HD * 2) + (((ks * 4 + g) ^ kswz<HD>(key)) * 16));
 #pragma unroll
-      for (int qs = 0; qs < 2; ++qs) {
+      for (int qs = 0; qs < QS; ++qs) {
         st[qs][kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < NS; ++ks) st[qs][kt] = mfma16x16x32(a[ks], qf[qs][ks], st[qs][kt]);
@@ -259,9 +271,9 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
     // Blocks whose every key is visible to every query of the workgroup skip
     // the mask.
     const bool need_mask = kb_cur + KB > seg_n || (own_cur && kb_cur + KB > vis_min);
-    f16x8 pb[2][2];
+    f16x8 pb[QS][2];
 #pragma unroll
-    for (int qs = 0; qs < 2; ++qs) {
+    for (int qs = 0; qs < QS; ++qs) {
       float mb = -INFINITY;
       if (need_mask) {
         // key kb + 8g + j is visible iff j < lim - kb - 8g
@@ -311,13 +323,13 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs p, float sc
         const int dim = 16 * i + c;
         const f16x8 a = *(const f16x8*)(sV + dim * 128 + (((4 * kc + g) ^ vswz(dim)) * 16));
 #pragma unroll
-        for (int qs = 0; qs < 2; ++qs) o[qs][i] = mfma16x16x32(a, pb[qs][kc], o[qs][i]);
+        for (int qs = 0; qs < QS; ++qs) o[qs][i] = mfma16x16x32(a, pb[qs][kc], o[qs][i]);
       }
     }
   }
 
 #pragma unroll
-  for (int qs = 0; qs < 2; ++qs) {
+  for (int qs = 0; qs < QS; ++qs) {
     const float l_tot = sum_x32(sum_x16(l_run[qs]));
     if (qvalid[qs]) {
       const float inv = 1.0f / l_tot;
@@ -340,9 +352,9 @@ hipError_t launch_attention(hipStream_t s, const AttnArgs& a) {
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)a.hd);
   dim3 grid(a.n_work, a.nkv);
   if (a.hd == 128)
-    hipLaunchKernelGGL(attn_kernel<128>, grid, dim3(256), 0, s, a, scale_log2);
+    hipLaunchKernelGGL(attn_kernel<128>, grid, dim3(64 * attn_waves<128>()), 0, s, a, scale_log2);
   else if (a.hd == 64)
-    hipLaunchKernelGGL(attn_kernel<64>, grid, dim3(256), 0, s, a, scale_log2);
+    hipLaunchKernelGGL(attn_kernel<64>, grid, dim3(64 * attn_waves<64>()), 0, s, a, scale_log2);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

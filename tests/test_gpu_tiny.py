@@ -656,6 +656,42 @@ def test_ragged_vocab_and_wide_batch(L):
     ctx.close()
 
 
+def test_head_dim_128_attention(L):
+    """Attention with 128-dimensional heads (the 8B head width) at a small
+    size: grouped queries (G = 2), a root and a child prefix, rows long
+    enough for several 128-vector query tiles, against the oracle; the same
+    bits for any batching."""
+    shape = dataclasses.replace(TINY, name="tiny_hd128", n_heads=2, n_kv_heads=1, head_dim=128,
+                                shape_id=8)
+    w = make_weights(shape, seed=5)
+    orc = OracleLM(w, shape)
+    ctx = L.Context(shape, device=0)
+    ctx.load_weights(w)
+    rng = np.random.default_rng(21)
+    root_t = rng.integers(0, shape.vocab, size=100).astype(np.int32)
+    kid_t = rng.integers(0, shape.vocab, size=37).astype(np.int32)
+    root = ctx.set_prefix(root_t)
+    kid = ctx.set_prefixes([kid_t], parent=root)[0]
+    lens = [1, 2, 63, 64, 65, 130, 7, 90, 150, 33, 0, 5]
+    rows = [rng.integers(0, shape.vocab, size=n).astype(np.int32) for n in lens]
+    offs = np.concatenate([[0], np.cumsum(lens)])
+    toks = np.concatenate(rows)
+    allowed = rng.choice(shape.vocab, 6, replace=False).astype(np.int32)
+    for pre, label, kw in ((root, "root", {}), (kid, "child",
+                                                 dict(children=[kid_t], row_child=[0] * len(rows)))):
+        _log(f"hd 128, {label} prefix: eval")
+        out, dbg = ctx.eval_rows(toks, offs, KIND_ENUM, allowed, prefix=pre, debug_logits=True,
+                                 no_dedup=True)
+        ref = orc.eval_rows(root_t, rows, KIND_ENUM, allowed, keep_logits=True, **kw)
+        _log(f"hd 128 {label}", compare(ref, out, dbg, f"hd 128 {label}"))
+        o2, d2 = ctx.eval_rows(toks, offs, KIND_ENUM, allowed, prefix=pre, debug_logits=True,
+                               no_dedup=True, max_batch_tokens=70)
+        assert o2.tobytes() == out.tobytes() and np.array_equal(d2, dbg)
+    ctx.release_prefix(kid)
+    ctx.release_prefix(root)
+    ctx.close()
+
+
 def test_tiny_restricted_head(tiny, L):
     """Restricted head: only the allowed tokens' logits are computed; typed
     outputs and allowed-set log-probabilities match the oracle and the full
