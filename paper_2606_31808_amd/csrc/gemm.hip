@@ -107,7 +107,10 @@ struct Cfg {
   static constexpr int S_BYTES = WF == WF_INT4 ? 1024 : 0;
   static constexpr int STAGE = A_BYTES + B_BYTES + S_BYTES;
   static constexpr int NS = WF == WF_FP8 ? 2 : NSTAGE;  // ring stages
-  static constexpr int LDS = NS * STAGE;
+  // int4 residual-add tiles prefetch the residual rows into an unread LDS
+  // area (1 KB per wave), only so that they are in the caches by the epilogue
+  static constexpr int PF = WF == WF_INT4 ? 1024 * NW : 0;
+  static constexpr int LDS = NS * STAGE + PF;
   // global->LDS instructions one wave issues per K step (A rows, weight tile, scales)
   static constexpr int A_LOADS = (BM / 8 + NW - 1) / NW;
   static constexpr int B_LOADS = B_BYTES / 1024 / NW;
@@ -152,6 +155,9 @@ __global__ __launch_bounds__((64 * NW_), Occ<MI>::value) void gemm_kernel(const 
   const int KT = p.K / BK;
   const int KG = p.K / 32;
   const f16* A = (const f16*)p.A;
+  // K steps whose stage also prefetches one residual row per wave (the last
+  // PFW steps; 4 waves x 32 steps cover the tile's 128 rows)
+  const int PFW = KT < BM / NW ? KT : BM / NW;
 
   // ---- global -> LDS issue of one K step into stage st; every wave issues
   // exactly C::LOADS instructions, which the vmcnt waits below rely on
@@ -182,6 +188,18 @@ __global__ __launch_bounds__((64 * NW_), Occ<MI>::value) void gemm_kernel(const 
         const size_t blk = (nb0 + (pi >> 1)) * KG + kt * 2 + (pi & 1);
         if ((lane >> 4) == wave) g2l16((const char*)p.bs + blk * 128 + (lane & 7) * 16, sS);
       }
+      if constexpr (EPI == EPI_ADD_F32) {
+        // the residual row r of the tile (1 KB: this wave's 256 columns),
+        // issued after the stage so the waits below can count it
+        if (kt >= KT - PFW) {
+          const int r = (kt - (KT - PFW)) * NW + wave;
+          int gm = m0 + (r < BM ? r : BM - 1);
+          gm = gm < p.M ? gm : p.M - 1;
+          int col = n0 + lane * 4;
+          col = col + 4 <= p.n_out ? col : p.n_out - 4;
+          g2l16(p.X + (size_t)gm * p.ldx + col, smem + C::NS * C::STAGE + wave * 1024);
+        }
+      }
     } else if constexpr (WF == WF_FP8) {
       // 1 KB chunks: (64-column block, group) pair q >> 1, half q & 1
       const size_t nb0 = (size_t)(n0 >> 6);
@@ -210,11 +228,16 @@ __global__ __launch_bounds__((64 * NW_), Occ<MI>::value) void gemm_kernel(const 
     issue(0, 0);
     if (KT > 1) issue(1, 1);
     for (int kt = 0; kt < KT; ++kt) {
-      // this step's stage is complete once at most the next step's loads are in flight
-      if (kt + 1 < KT)
-        wait_vmcnt<C::LOADS>();
-      else
+      // this step's stage is complete once at most the next step's loads
+      // (and the residual prefetch issued after them) are in flight
+      if (kt + 1 < KT) {
+        if (EPI == EPI_ADD_F32 && kt + 1 >= KT - PFW)
+          wait_vmcnt<C::LOADS + 1>();
+        else
+          wait_vmcnt<C::LOADS>();
+      } else {
         wait_vmcnt<0>();
+      }
       barrier();
       if (kt + 2 < KT) issue((kt + 2) % NSTAGE, kt + 2);
       const char* sA = smem + (kt % NSTAGE) * C::STAGE;
