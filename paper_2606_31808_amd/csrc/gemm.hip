@@ -489,6 +489,7 @@ struct HeadCfg {
   // 16 rows per instruction; surplus waves repeat the last vocabulary block
   static constexpr int A_LOADS = (MI + NW - 1) / NW;
   static constexpr int T_LOADS = F;  // a wave's own token blocks
+  static_assert(A_LOADS + T_LOADS <= 8, "the per-wave wait covers at most 8 loads in flight");
 };
 
 // 16-byte chunk swizzle of a 64-byte LDS row: the 8 lanes a ds_read_b128
