@@ -692,6 +692,43 @@ def test_head_dim_128_attention(L):
     ctx.close()
 
 
+def test_tiny_max_sizes(tiny, L):
+    """Maximum sizes: an integer type with max_tokens = 8 (numbers of up to 8
+    digits fill the result's token array), and 2,100 one-to-three-token rows
+    (more than one batch's 2,048-row cap; the LM head runs eight 256-row
+    column tiles); against the oracle."""
+    w, orc, ctx = tiny
+    rng = np.random.default_rng(77)
+    prefix = rng.integers(0, TINY.vocab, size=20).astype(np.int32)
+    pre = ctx.set_prefix(prefix)
+    digits = rng.choice(TINY.vocab, 10, replace=False).astype(np.int32)
+    eos = int(next(t for t in range(TINY.vocab) if t not in digits))
+    rows = [rng.integers(0, TINY.vocab, size=int(rng.integers(1, 12))).astype(np.int32)
+            for _ in range(24)]
+    offs = np.concatenate([[0], np.cumsum([len(r) for r in rows])])
+    _log("max sizes: 8-digit integers")
+    out, dbg = ctx.eval_rows(np.concatenate(rows), offs, KIND_INT, digits, eos=eos, max_tokens=8,
+                             prefix=pre, debug_logits=True)
+    ref = orc.eval_rows(prefix, rows, KIND_INT, digits, eos=eos, max_tokens=8, keep_logits=True)
+    forced = orc.eval_rows(prefix, rows, KIND_INT, digits, eos=eos, max_tokens=8, keep_logits=True,
+                           forced=[out["tokens"][r][: out["n_tokens"][r]] for r in range(24)])
+    _log("max_tokens 8", compare(ref, out, dbg, "max_tokens 8", orc_forced=forced))
+    assert_typed(out, KIND_INT, 10, digits, eos=eos, max_tokens=8)
+    assert int(np.max(out["n_tokens"])) == 8
+    _log("max sizes: 2,100 rows")
+    rows = [rng.integers(0, TINY.vocab, size=int(rng.integers(1, 4))).astype(np.int32)
+            for _ in range(2100)]
+    offs = np.concatenate([[0], np.cumsum([len(r) for r in rows])])
+    allowed = rng.choice(TINY.vocab, 5, replace=False).astype(np.int32)
+    out, dbg = ctx.eval_rows(np.concatenate(rows), offs, KIND_ENUM, allowed, prefix=pre,
+                             debug_logits=True, no_dedup=True)
+    ref = orc.eval_rows(prefix, rows, KIND_ENUM, allowed, keep_logits=True)
+    st = compare(ref, out, dbg, "2100 rows")
+    _log("2100 rows", st)
+    assert st["exact_checked"] >= 1000
+    ctx.release_prefix(pre)
+
+
 def test_tiny_restricted_head(tiny, L):
     """Restricted head: only the allowed tokens' logits are computed; typed
     outputs and allowed-set log-probabilities match the oracle and the full
