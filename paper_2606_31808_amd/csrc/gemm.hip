@@ -477,19 +477,20 @@ hipError_t launch_epi(hipStream_t s, const GemmArgs& a) {
 // wave's token rows straight into registers instead was measured ~35%
 // slower: those loads, not LDS, bounded the head.  A 96 x 320 tile for
 // 257..320 rows was 7% faster there but changes the chunking.)
-template <int MI_, int F_>
+template <int MI_, int F_, int NS_>
 struct HeadCfg {
   static constexpr int MI = MI_, F = F_;
-  static constexpr int BK = 32, NW = 4, NS = 3;
+  static constexpr int BK = 32, NW = 4, NS = NS_;
   static constexpr int BM = 16 * MI, BN = NW * 16 * F;
   static constexpr int A_BYTES = BM * 64, T_BYTES = BN * 64;
   static constexpr int STAGE = A_BYTES + T_BYTES;
   static constexpr int LDS = NS * STAGE;
-  static_assert(LDS <= 80 * 1024, "two workgroups per CU");
+  static_assert(NS >= 2 && LDS <= 160 * 1024, "LDS of one CU");
+  static constexpr int OCC = LDS <= 80 * 1024 ? 2 : 1;  // workgroups per CU
   // 16 rows per instruction; surplus waves repeat the last vocabulary block
   static constexpr int A_LOADS = (MI + NW - 1) / NW;
   static constexpr int T_LOADS = F;  // a wave's own token blocks
-  static_assert(A_LOADS + T_LOADS <= 8, "the per-wave wait covers at most 8 loads in flight");
+  static_assert((NS - 2) * (A_LOADS + T_LOADS) <= 31, "loads in flight fit the run-time wait");
 };
 
 // 16-byte chunk swizzle of a 64-byte LDS row: the 8 lanes a ds_read_b128
@@ -497,9 +498,9 @@ struct HeadCfg {
 // distinct 16-byte bank groups of a 128-byte window
 LMOP_DEVICE int swz64(int row) { return (row >> 1) & 3; }
 
-template <int MI, int F>
-__global__ __launch_bounds__(256, 2) void head_kernel(const GemmArgs p) {
-  using C = HeadCfg<MI, F>;
+template <int MI, int F, int NS_>
+__global__ __launch_bounds__(256, (HeadCfg<MI, F, NS_>::OCC)) void head_kernel(const GemmArgs p) {
+  using C = HeadCfg<MI, F, NS_>;
   constexpr int BK = C::BK, BM = C::BM, BN = C::BN, NW = C::NW, NS = C::NS;
   constexpr int A_BYTES = C::A_BYTES, STAGE = C::STAGE;
   constexpr int A_LOADS = C::A_LOADS, T_LOADS = C::T_LOADS;
@@ -571,16 +572,17 @@ __global__ __launch_bounds__(256, 2) void head_kernel(const GemmArgs p) {
     for (int i = 0; i < MI; ++i) acc[f][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const bool wave_active = w0 < p.N;
-  issue(0, 0);
-  if (KT > 1) issue(1, 1);
+  // NS - 1 stages in flight ahead of the one being read
+#pragma unroll
+  for (int st = 0; st < NS - 1; ++st)
+    if (st < KT) issue(st, st);
   for (int kt = 0; kt < KT; ++kt) {
-    // this step's stage is complete once at most the next step's loads are in flight
-    if (kt + 1 < KT)
-      wait_vmcnt_upto8(my_loads);
-    else
-      wait_vmcnt<0>();
+    // this step's stage is complete once at most the later steps' loads
+    // (up to NS - 2 stages of them) are in flight
+    const int later = KT - 1 - kt < NS - 2 ? KT - 1 - kt : NS - 2;
+    wait_vmcnt_dyn(later * my_loads);
     barrier();
-    if (kt + 2 < KT) issue((kt + 2) % NS, kt + 2);
+    if (kt + NS - 1 < KT) issue((kt + NS - 1) % NS, kt + NS - 1);
     if (wave_active) {
       const char* sA = smem + (kt % NS) * STAGE;
       const char* sT = sA + A_BYTES;
@@ -639,25 +641,35 @@ __global__ __launch_bounds__(256, 2) void head_kernel(const GemmArgs p) {
     }
 }
 
-template <int MI, int F>
+template <int MI, int F, int NS>
 hipError_t launch_head(hipStream_t s, const GemmArgs& a) {
-  using C = HeadCfg<MI, F>;
+  using C = HeadCfg<MI, F, NS>;
   const int tiles = ((a.M + C::BM - 1) / C::BM) * ((a.N + C::BN - 1) / C::BN);
   if (tiles == 0) return hipSuccess;
   static const hipError_t attr = hipFuncSetAttribute(
-      (const void*)head_kernel<MI, F>, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+      (const void*)head_kernel<MI, F, NS>, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((head_kernel<MI, F>), dim3(tiles), dim3(256), C::LDS, s, a);
+  hipLaunchKernelGGL((head_kernel<MI, F, NS>), dim3(tiles), dim3(256), C::LDS, s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_gemm_f16(hipStream_t s, const GemmArgs& a, int epi) {
-  static_assert(HeadCfg<8, 4>::BM == kHeadVocabChunk, "partials per vocabulary chunk");
+  using H256 = HeadCfg<8, 4, 3>;  // 256-token tile, 3-stage ring
+  using H320 = HeadCfg<8, 5, 2>;  // 320-token tile, 2-stage ring
+  static_assert(H256::BM == kHeadVocabChunk && H320::BM == kHeadVocabChunk,
+                "partials per vocabulary chunk");
+  static_assert(H256::OCC == 2 && H320::OCC == 2, "two workgroups per CU");
   if (a.K % 32 != 0 || epi != EPI_HEAD || a.ldb % 8 != 0 || a.lda % 8 != 0)
     return hipErrorInvalidValue;
-  return launch_head<8, 4>(s, a);
+  // A workgroup's time barely depends on how many of its token rows are
+  // real, so the tile that needs fewer token tiles wins; a full 320-token
+  // tile runs about 10% longer than a full 256-token one.  Each logit's
+  // accumulation order is the same in both, so the choice never changes a bit.
+  const int t256 = (a.N + H256::BN - 1) / H256::BN, t320 = (a.N + H320::BN - 1) / H320::BN;
+  if (10 * t256 > 11 * t320) return launch_head<8, 5, 2>(s, a);
+  return launch_head<8, 4, 3>(s, a);
 }
 
 hipError_t launch_gemm_w4(hipStream_t s, const GemmArgs& a, int epi) {

@@ -622,11 +622,13 @@ def test_tiny_sampled_profiling(tiny, L):
     ctx.release_prefix(pre)
 
 
-def test_ragged_vocab_and_wide_batch(L):
+@pytest.mark.parametrize("n_rows", [300, 600])
+def test_ragged_vocab_and_wide_batch(L, n_rows):
     """A vocabulary that is not a multiple of the head's 128-entry chunk
-    (1,999 = 15 x 128 + 79) and a batch of 300 rows (two 256-row column
-    tiles in the head): logits and typed outputs against the oracle, every
-    row; the same bits when the rows are batched in small pieces."""
+    (1,999 = 15 x 128 + 79) and a batch of 300 or 600 rows, which the head
+    covers with one or two 320-token tiles (the second partly filled):
+    logits and typed outputs against the oracle, every row; the same bits
+    when the rows are batched in small pieces, which take the 256-token tile."""
     shape = dataclasses.replace(TINY, name="tiny_v1999", vocab=1999, n_layers=1, shape_id=7)
     w = make_weights(shape, seed=99)
     orc = OracleLM(w, shape)
@@ -635,19 +637,19 @@ def test_ragged_vocab_and_wide_batch(L):
     rng = np.random.default_rng(12)
     prefix = rng.integers(0, shape.vocab, size=40).astype(np.int32)
     rows = [rng.integers(0, shape.vocab, size=int(rng.integers(1, 6))).astype(np.int32)
-            for _ in range(300)]
+            for _ in range(n_rows)]
     offs = np.concatenate([[0], np.cumsum([len(r) for r in rows])])
     toks = np.concatenate(rows)
     # allowed tokens include the last vocabulary entries (the ragged chunk)
     allowed = np.array([1998, 1990, 1920, 5, 700], dtype=np.int32)
     pre = ctx.set_prefix(prefix)
-    _log("ragged vocab: eval 300 rows in one batch")
+    _log(f"ragged vocab: eval {n_rows} rows in one batch")
     out, dbg = ctx.eval_rows(toks, offs, KIND_ENUM, allowed, prefix=pre, debug_logits=True,
                              no_dedup=True)
     ref = orc.eval_rows(prefix, rows, KIND_ENUM, allowed, keep_logits=True)
     st = compare(ref, out, dbg, "ragged vocab")
     _log("ragged vocab", st)
-    assert st["exact_checked"] >= 200
+    assert st["exact_checked"] >= n_rows // 2
     assert_typed(out, KIND_ENUM, len(allowed), allowed)
     o2, d2 = ctx.eval_rows(toks, offs, KIND_ENUM, allowed, prefix=pre, debug_logits=True,
                            no_dedup=True, max_batch_tokens=37)
