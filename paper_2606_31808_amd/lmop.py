@@ -92,6 +92,11 @@ assert C.sizeof(lmop_result) == RESULT_DTYPE.itemsize
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_31808_amd.build`")
+    # torch ships its own HIP runtime under the same soname.  Loading it first
+    # makes the library bind to that one runtime: the streams and device
+    # pointers torch hands over are only valid there, and a second runtime
+    # loaded beside it finds no devices.
+    import torch  # noqa: F401
     lib = C.CDLL(LIB_PATH)
     vp, i32, st = C.c_void_p, C.c_int32, C.c_int
     sig = {

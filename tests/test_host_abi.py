@@ -277,3 +277,24 @@ def test_binding_constants_match_header():
     kinds = dict(re.findall(r"(LMOP_(?:BOOL|ENUM|INT|AUTOMATON))\s*=\s*(\d+)", hdr))
     assert kinds == {"LMOP_BOOL": "0", "LMOP_ENUM": "1", "LMOP_INT": "2", "LMOP_AUTOMATON": "3"}
     assert (L.LMOP_BOOL, L.LMOP_ENUM, L.LMOP_INT, L.LMOP_AUTOMATON) == (0, 1, 2, 3)
+
+
+def test_binding_shares_torchs_hip_runtime():
+    """Imported on its own, the binding still loads torch's HIP runtime before
+    the library, so the process maps exactly one libamdhip64: torch's."""
+    import json
+    import subprocess
+    import sys
+
+    import torch
+
+    code = ("import json, paper_2606_31808_amd.lmop\n"
+            "maps = open('/proc/self/maps').read().splitlines()\n"
+            "print(json.dumps(sorted({l.split()[-1] for l in maps if 'libamdhip64' in l})))")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    out = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True,
+                         check=True, timeout=300).stdout
+    paths = json.loads(out.strip().splitlines()[-1])
+    torch_lib = os.path.realpath(os.path.join(os.path.dirname(torch.__file__), "lib"))
+    assert len(paths) == 1, paths
+    assert os.path.realpath(paths[0]).startswith(torch_lib), paths
