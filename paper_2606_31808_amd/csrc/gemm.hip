@@ -467,16 +467,17 @@ hipError_t launch_epi(hipStream_t s, const GemmArgs& a) {
 // ---------------------------------------------------------------- LM head
 // z = W_lm . h for R token rows: the head weight W_lm fp16 [V][K] is the
 // vocabulary operand (M), the final-normalised rows h fp16 [R][K] the token
-// operand (N); both stream through a three-stage LDS ring by direct
-// global->LDS loads, 32 features per step in 64-byte LDS rows.  A workgroup
-// holds 16*MI = 128 vocabulary entries and 64*F = 256 token rows: four waves
-// side by side along the tokens (64 rows each) share the vocabulary tile;
-// 72 KB of LDS, two workgroups per CU.  The log-sum-exp partials are per
-// 128-entry vocabulary chunk whatever the number of rows, so a row's
-// log-probabilities do not depend on how rows are batched.  (Loading each
-// wave's token rows straight into registers instead was measured ~35%
-// slower: those loads, not LDS, bounded the head.  A 96 x 320 tile for
-// 257..320 rows was 7% faster there but changes the chunking.)
+// operand (N); both stream through an LDS ring by direct global->LDS loads,
+// 32 features per step in 64-byte LDS rows.  A workgroup holds 16*MI = 128
+// vocabulary entries and 64*F token rows: four waves side by side along the
+// tokens (16*F rows each) share the vocabulary tile.  Two shapes keep two
+// workgroups per CU: F = 4 (256 rows) with a 3-stage ring (72 KB of LDS)
+// and F = 5 (320 rows) with a 2-stage ring (56 KB); deeper rings that leave
+// one workgroup per CU ran about twice as long.  The log-sum-exp partials
+// are per 128-entry vocabulary chunk whatever the tile or the number of
+// rows, so a row's log-probabilities do not depend on how rows are batched.
+// (Loading each wave's token rows straight into registers instead was
+// measured ~35% slower: those loads, not LDS, bounded the head.)
 template <int MI_, int F_, int NS_>
 struct HeadCfg {
   static constexpr int MI = MI_, F = F_;
