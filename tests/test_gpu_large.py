@@ -13,7 +13,7 @@ import numpy as np
 import pytest
 import torch
 
-from oracle import OracleLM
+from oracle import KIND_ENUM, OracleLM
 from synth import SHAPES, make_weights, make_workload
 from tests.parity import assert_automaton, assert_typed, compare
 
@@ -233,6 +233,42 @@ def test_filter_8b_fp8_sampled_rows(L):
     wl = make_workload("filter_8b")
     pre = ctx.set_prefix(wl.prefix)
     _check_filter(ctx, orc, wl, pre, _sample(wl, 4, 3), "filter_8b fp8")
+    ctx.close()
+    del w, orc
+    torch.cuda.empty_cache()
+
+
+def test_head_tiles_8b_shape(L):
+    """The LM head at the 8B shape (V = 128,256, d = 4,096) on a model with no
+    decoder layers: 300 one-token rows in one batch (one 320-row head tile)
+    and in batches of at most 100 rows (the 256-row tile) give the same bits,
+    and sampled rows match the fp32 oracle."""
+    import dataclasses
+
+    shape = dataclasses.replace(SHAPES["8b"], n_layers=0)
+    w = make_weights(shape, seed=4321, device="cuda", n_layers=0)
+    torch.cuda.synchronize()
+    ctx = L.Context(shape, device=0, stream=torch.cuda.current_stream().cuda_stream)
+    ctx.load_weights(w)
+    rng = np.random.default_rng(5)
+    toks = rng.integers(0, shape.vocab, size=300).astype(np.int32)
+    offs = np.arange(301, dtype=np.int64)
+    allowed = rng.choice(shape.vocab, 24, replace=False).astype(np.int32)
+    _log("8B head: 300 rows in one batch, then in batches of 100")
+    full, _ = ctx.eval_rows(toks, offs, KIND_ENUM, allowed, no_dedup=True)
+    small, _ = ctx.eval_rows(toks, offs, KIND_ENUM, allowed, no_dedup=True, max_batch_tokens=100)
+    assert full.tobytes() == small.tobytes()
+    assert_typed(full, KIND_ENUM, len(allowed), allowed)
+    sample = [0, 77, 150, 256, 299]
+    st_toks = toks[sample]
+    out, dbg = ctx.eval_rows(st_toks, np.arange(len(sample) + 1, dtype=np.int64), KIND_ENUM,
+                             allowed, no_dedup=True, debug_logits=True)
+    _same_rows(full, out, sample, "8B head")
+    orc = OracleLM(w, shape, dtype=np.float32)
+    ref = orc.eval_rows(np.zeros(0, dtype=np.int32), [toks[i:i + 1] for i in sample], KIND_ENUM,
+                        allowed, keep_logits=True)
+    st = compare(ref, out, dbg, "8B head")
+    _log("8B head", st)
     ctx.close()
     del w, orc
     torch.cuda.empty_cache()
