@@ -331,6 +331,75 @@ def test_one_token_attention_block_is_two_linear_maps():
     assert np.allclose(orc.forward_sequence([33])[-1], want, atol=1e-13)
 
 
+def _attention_layer_by_scalar_loops(w, tokens):
+    """One decoder layer whose down projection is zero, written out with
+    scalar loops and the math module from the layer's definition: RMSNorm,
+    the q/k/v maps, rotate-half RoPE on q and k at positions 0, 1, 2, ...
+    (pair (m, m + hd/2) turned by pos * theta^(-2m/hd)), query head j reading
+    kv head floor(j * n_kv / n_q), a softmax over the keys at or before the
+    query, and the output map added to the residual."""
+    sh = MICRO
+    hd, half, nq, nkv = sh.head_dim, sh.head_dim // 2, sh.n_heads, sh.n_kv_heads
+    L = w.layers[0]
+    dq = lambda m: dequant(m.qweight.numpy(), m.scales.numpy(), m.k).tolist()
+    wq, wk, wv, wo = dq(L.wq), dq(L.wk), dq(L.wv), dq(L.wo)
+    emb = w.tok_embedding.double().numpy()
+    d = sh.d_model
+    xs, qs, ks, vs = [], [], [], []
+    for pos, t in enumerate(tokens):
+        x = [float(v) for v in emb[t]]
+        r = 1.0 / math.sqrt(sum(v * v for v in x) / d + sh.rms_eps)
+        h = [v * r for v in x]
+        lin = lambda W: [sum(W[n][c] * h[c] for c in range(d)) for n in range(len(W))]
+        q, k, v = lin(wq), lin(wk), lin(wv)
+
+        def rot(vec, heads):
+            out = list(vec)
+            for j in range(heads):
+                for m in range(half):
+                    a = pos * sh.rope_theta ** (-2.0 * m / hd)
+                    x1, x2 = vec[j * hd + m], vec[j * hd + m + half]
+                    out[j * hd + m] = x1 * math.cos(a) - x2 * math.sin(a)
+                    out[j * hd + m + half] = x1 * math.sin(a) + x2 * math.cos(a)
+            return out
+        xs.append(x)
+        qs.append(rot(q, nq))
+        ks.append(rot(k, nkv))
+        vs.append(v)
+    out = []
+    for i in range(len(tokens)):
+        o = [0.0] * (nq * hd)
+        for j in range(nq):
+            g = j * nkv // nq
+            sc = [sum(qs[i][j * hd + m] * ks[s][g * hd + m] for m in range(hd)) / math.sqrt(hd)
+                  for s in range(i + 1)]
+            top = max(sc)
+            e = [math.exp(v - top) for v in sc]
+            tot = sum(e)
+            for m in range(hd):
+                o[j * hd + m] = sum(e[s] / tot * vs[s][g * hd + m] for s in range(i + 1))
+        out.append([xs[i][n] + sum(wo[n][c] * o[c] for c in range(nq * hd)) for n in range(d)])
+    return np.array(out)
+
+
+def test_multi_token_attention_block_scalar_loops():
+    # three tokens: RoPE turns q and k (not v) at positions 1 and 2, the
+    # softmax weighs several keys, and the two kv heads serve four query heads
+    w = make_weights(MICRO, seed=16, n_layers=1)
+    _zero(w.layers[0].w_down)
+    orc = OracleLM(w, MICRO)
+    toks = [33, 7, 81]
+    want = _attention_layer_by_scalar_loops(w, toks)
+    assert np.allclose(orc.forward_sequence(toks), want, rtol=0, atol=1e-12)
+    # the same through row evaluation: a 1-token prefix and a 2-token suffix
+    res = orc.eval_rows(np.array(toks[:1]), [np.array(toks[1:])], KIND_ENUM, [1, 2, 3],
+                        keep_logits=True)
+    x = want[-1]
+    hn = x / math.sqrt(float(np.mean(x * x)) + MICRO.rms_eps)
+    z = hn @ w.lm_head.double().numpy().T
+    assert np.allclose(res["logits"][0][0], z, rtol=0, atol=1e-12)
+
+
 def test_mlp_block_closed_form():
     # attention output projection zeroed: the layer is x + swiglu(RMSNorm(x)) Wd^T
     w = make_weights(MICRO, seed=15, n_layers=1)
