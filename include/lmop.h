@@ -24,7 +24,9 @@
  *  - A ctx is not thread-safe; use one ctx per host thread and stream.
  *  - The caller owns every pointer it passes and may free it when the call
  *    returns.  The library owns its device memory (weights, prefix KV,
- *    activations) and frees it in lmop_release_prefix / lmop_destroy.
+ *    scratch) and frees it in lmop_release_prefix / lmop_destroy; scratch
+ *    comes from a caller-supplied workspace instead once lmop_set_workspace
+ *    has given one.
  *  - LMOP_ERR_DEVICE is sticky: after a HIP error the ctx refuses further
  *    work and must be destroyed.
  *  - All calls are synchronous with respect to the host: when they return,
@@ -62,7 +64,11 @@ typedef struct {
 } lmop_config;
 
 /* Creates a ctx on HIP device `device` whose work runs on `hip_stream`
- * (a hipStream_t; NULL = the library creates its own).  device = -1 creates
+ * (a hipStream_t; NULL = the library creates its own blocking stream, which
+ * is ordered after work on the null stream).  Device memory the caller
+ * passes (on_device weights, a workspace) is read in the ctx stream's order:
+ * work still writing it on another stream must be finished or ordered
+ * before the call (on the ctx's stream or the null stream).  device = -1 creates
  * a host-only ctx: every argument check runs, but calls that would touch a
  * GPU return LMOP_ERR_UNSUPPORTED after validation.  On failure *out is NULL
  * and lmop_last_error(NULL) describes the cause (per host thread). */
@@ -239,6 +245,35 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
                            const lmop_prefix* const* row_prefix, const int32_t* tokens,
                            const int64_t* offsets, int32_t n_rows, const lmop_type* type,
                            lmop_result* out, const lmop_eval_opts* opts);
+
+/* A caller-supplied workspace.  The paper's serving setup caps the GPU
+ * memory the LM may take (Appendix "vLLM Config", gpu_memory_utilization)
+ * and runs on a 16 GB GPU (Sec. 3.2 Setup); a caller that owns the device
+ * memory (e.g. a PyTorch allocation) hands the library one region instead of
+ * letting it allocate scratch.  After lmop_set_workspace(ctx, p, bytes) with
+ * p != NULL, every scratch buffer of lmop_set_prefix(es) and lmop_eval_rows
+ * (activations, head partials, the own-KV store of a batch or integer decode
+ * group) is carved from [p, p + bytes): the library frees the scratch it had
+ * allocated, sizes batches and decode groups to fit (max_batch_tokens
+ * becomes an upper bound), and a call fails with LMOP_ERR_OOM, the sizes in
+ * lmop_last_error, when not even one row (or one prefix) fits.  Weights and
+ * prefix KV stores remain the library's own allocations.  p: device memory
+ * of the ctx's device, 256-byte aligned; the caller keeps ownership, keeps
+ * it alive until the workspace is replaced or the ctx destroyed, and leaves
+ * it alone while a call runs (its contents are scratch).  (NULL, 0) returns
+ * to library-allocated scratch.  INVALID_ARG for a misaligned or non-device
+ * pointer, or one of p, bytes zero without the other. */
+lmop_status lmop_set_workspace(lmop_ctx* ctx, void* dev_ptr, size_t bytes);
+
+/* Device memory accounting of a ctx (for the 16 GB budget of Sec. 3.2). */
+typedef struct {
+  uint64_t device_bytes;    /* device memory the library holds now (weights, prefix KV
+                               stores, scratch it allocated itself)                      */
+  uint64_t device_peak;     /* the most it has held at once since lmop_create             */
+  uint64_t workspace_bytes; /* size of the caller's workspace (0: none)                   */
+  uint64_t workspace_peak;  /* the most of the workspace one call has used since it was set */
+} lmop_memory_stats;
+lmop_status lmop_get_memory(const lmop_ctx* ctx, lmop_memory_stats* out);
 
 /* Early deduplication (Sec. 2.4): rows with equal (key, suffix) get the
  * same representative, the first such row.  keys: NULL or host [n_rows]

@@ -9,6 +9,21 @@ namespace lmop {
 
 namespace {
 
+// --------------------------------------------------------------- fill
+// p[i] = value for i < n 32-bit words (clears scratch and KV stores with a
+// kernel, so no memset node lands in a caller's captured graph)
+__global__ __launch_bounds__(256) void fill_u32_kernel(uint32_t* __restrict__ p, size_t n,
+                                                       uint32_t value) {
+  const size_t stride = (size_t)gridDim.x * 256 * 4;
+  for (size_t i = ((size_t)blockIdx.x * 256 + threadIdx.x) * 4; i < n; i += stride) {
+    if (i + 4 <= n) {
+      *(uint4*)(p + i) = make_uint4(value, value, value, value);
+    } else {
+      for (size_t j = i; j < n; ++j) p[j] = value;
+    }
+  }
+}
+
 // --------------------------------------------------------------- embedding
 // x[t][:] = fp32(E[tok[t]][:]); one workgroup per token, 8 halves per thread-iteration
 __global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ tok,
@@ -302,6 +317,15 @@ __global__ __launch_bounds__(64) void head_finalize_kernel(const float2* __restr
 }
 
 }  // namespace
+
+hipError_t launch_fill_u32(hipStream_t s, void* p, size_t n_words, uint32_t value) {
+  if (n_words == 0) return hipSuccess;
+  if (((uintptr_t)p & 15) != 0) return hipErrorInvalidValue;
+  const size_t groups = (n_words + 1023) / 1024;
+  const int blocks = (int)(groups < 8192 ? groups : 8192);
+  hipLaunchKernelGGL(fill_u32_kernel, dim3(blocks), dim3(256), 0, s, (uint32_t*)p, n_words, value);
+  return hipGetLastError();
+}
 
 hipError_t launch_embed(hipStream_t s, const int32_t* tok, int T, const half_bits* emb, int d,
                         float* x) {

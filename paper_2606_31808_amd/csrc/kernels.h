@@ -99,6 +99,8 @@ hipError_t launch_repack_w8(hipStream_t s, const RepackSrc& src, const int32_t* 
                             PackedW& dst);
 
 // ---------------------------------------------------------------- elementwise
+// p[i] = value for n_words 32-bit words (p 16-byte aligned)
+hipError_t launch_fill_u32(hipStream_t s, void* p, size_t n_words, uint32_t value);
 hipError_t launch_embed(hipStream_t s, const int32_t* tok, int T, const half_bits* emb, int d,
                         float* x);
 // x_out[i] = x[idx[i]] (fp32, d), a_out[i] = a[idx[i]] (fp16, da)

@@ -14,6 +14,7 @@
 #include <cstring>
 #include <map>
 #include <memory>
+#include <mutex>
 #include <set>
 #include <string>
 #include <type_traits>
@@ -27,6 +28,9 @@ using namespace lmop;
 namespace {
 
 constexpr int kDefaultBatchTokens = 16384;
+// a library-allocated own-KV store above this size is released after each call
+constexpr size_t kKeepOwnKvBytes = size_t(1) << 30;
+
 constexpr int kMaxBatchRows = 2048;
 // own-KV bytes of one integer-decode group (also at most half the free memory)
 constexpr size_t kDecodeGroupBytes = size_t(24) << 30;
@@ -108,16 +112,40 @@ struct lmop_ctx {
   std::vector<void*> weight_allocs;
   float2* rope_tab = nullptr;
 
-  // workspace (grow-only)
+  // library-allocated scratch: named grow-only buffers
   std::map<std::string, std::pair<void*, size_t>> ws;
+
+  // device memory the library allocated itself (weights, prefix KV stores,
+  // scratch), with its peak since lmop_create
+  std::unordered_map<void*, size_t> alloc_sz;
+  size_t dev_bytes = 0, dev_peak = 0;
+  // the caller's workspace (lmop_set_workspace) and the most of it one call used
+  char* user_ws = nullptr;
+  size_t user_ws_bytes = 0, user_ws_peak = 0;
+  // While a call runs with `carving` set, every scratch buffer is a fixed
+  // region of [carve_base, carve_base + carve_size) laid out up front for the
+  // call (`carved`); carve_base is the caller's workspace or the library's
+  // static no-allocation array (a host-only ctx plans against the size
+  // alone).
+  bool carving = false;
+  char* carve_base = nullptr;
+  size_t carve_size = 0;
+  std::map<std::string, std::pair<void*, size_t>> carved;
+  // the current call allocates nothing: no device memory, no pinned host
+  // memory, no events
+  bool no_alloc = false;
 
   std::set<lmop_prefix*> prefixes;
 
   // pinned host staging for batch uploads and result readback: two slots, so
-  // that one batch's host-side packing overlaps the previous batch on the GPU
+  // that one batch's host-side packing overlaps the previous batch on the GPU.
+  // A no-allocation call stages through ordinary host memory instead.
   struct Staging {
-    char* p = nullptr;
+    char* p = nullptr;          // pinned buffer
     size_t bytes = 0;
+    std::vector<char> host;     // pageable buffer of no-allocation calls
+    char* cur = nullptr;        // the buffer of the current use
+    size_t cur_bytes = 0;
     size_t used = 0;            // bump offset within the current use
     hipEvent_t done = nullptr;  // recorded after the slot's last device access
     bool pending = false;
@@ -162,6 +190,8 @@ lmop_status fail(lmop_ctx* c, lmop_status st, const char* fmt, ...) {
 
 lmop_status dev_alloc(lmop_ctx* c, void** p, size_t bytes) {
   *p = nullptr;
+  if (c->no_alloc)
+    return fail(c, LMOP_ERR_STATE, "internal: a no-allocation call asked for %zu bytes", bytes);
   if (bytes == 0) bytes = 256;
   hipError_t e = hipMalloc(p, bytes);
   if (e != hipSuccess) {
@@ -169,27 +199,72 @@ lmop_status dev_alloc(lmop_ctx* c, void** p, size_t bytes) {
     (void)hipGetLastError();
     return fail(c, LMOP_ERR_OOM, "hipMalloc(%zu bytes) failed: %s", bytes, hipGetErrorString(e));
   }
+  c->alloc_sz[*p] = bytes;
+  c->dev_bytes += bytes;
+  c->dev_peak = std::max(c->dev_peak, c->dev_bytes);
   return LMOP_OK;
 }
 
-// named grow-only scratch buffer; `zero` clears it whenever it is (re)allocated
+// frees an allocation of dev_alloc (NULL is a no-op)
+hipError_t dev_free(lmop_ctx* c, void* p) {
+  if (!p) return hipSuccess;
+  auto it = c->alloc_sz.find(p);
+  if (it != c->alloc_sz.end()) {
+    c->dev_bytes -= it->second;
+    c->alloc_sz.erase(it);
+  }
+  return hipFree(p);
+}
+
+// scratch buffers start on 256-byte boundaries and are at least 256 bytes
+size_t scratch_round(size_t bytes) { return std::max<size_t>((bytes + 255) & ~(size_t)255, 256); }
+
+// Named scratch buffer of at least `count` elements.  Library-allocated
+// scratch grows and is kept (`zero` clears it whenever it is allocated);
+// carved scratch is the region the call's plan reserved under that name.
 template <typename T>
 lmop_status ws_get(lmop_ctx* c, const char* name, size_t count, T** out, bool zero = false) {
-  size_t bytes = std::max<size_t>(count * sizeof(T), 256);
+  const size_t bytes = scratch_round(count * sizeof(T));
+  if (c->carving) {
+    auto it = c->carved.find(name);
+    if (it == c->carved.end() || it->second.second < bytes)
+      return fail(c, LMOP_ERR_STATE, "internal: the scratch plan has no %zu bytes for '%s'",
+                  bytes, name);
+    *out = (T*)it->second.first;
+    return LMOP_OK;
+  }
   auto& slot = c->ws[name];
   if (slot.second < bytes) {
     if (slot.first) {
       HIP_OK(c, hipStreamSynchronize(c->stream));
-      HIP_OK(c, hipFree(slot.first));
+      HIP_OK(c, dev_free(c, slot.first));
     }
     slot = {nullptr, 0};
-    size_t want = bytes + bytes / 4;
+    size_t want = scratch_round(bytes + bytes / 4);
     void* p = nullptr;
     LMOP_TRY(dev_alloc(c, &p, want));
     slot = {p, want};
-    if (zero) HIP_OK(c, hipMemsetAsync(p, 0, want, c->stream));
+    if (zero) HIP_OK(c, launch_fill_u32(c->stream, p, want / 4, 0u));
   }
   *out = (T*)slot.first;
+  return LMOP_OK;
+}
+
+// Releases one library-allocated scratch buffer (after the stream is idle).
+lmop_status ws_release(lmop_ctx* c, const char* name) {
+  auto it = c->ws.find(name);
+  if (it == c->ws.end()) return LMOP_OK;
+  HIP_OK(c, hipStreamSynchronize(c->stream));
+  HIP_OK(c, dev_free(c, it->second.first));
+  c->ws.erase(it);
+  return LMOP_OK;
+}
+
+lmop_status ws_release_all(lmop_ctx* c) {
+  if (c->ws.empty()) return LMOP_OK;
+  HIP_OK(c, hipStreamSynchronize(c->stream));
+  for (auto& kv : c->ws) HIP_OK(c, dev_free(c, kv.second.first));
+  c->ws.clear();
   return LMOP_OK;
 }
 
@@ -202,30 +277,44 @@ lmop_status stage_begin(lmop_ctx* c, int k, size_t need) {
     HIP_OK(c, hipEventSynchronize(st.done));
     st.pending = false;
   }
-  if (!st.done) HIP_OK(c, hipEventCreateWithFlags(&st.done, hipEventDisableTiming));
-  if (st.bytes < need) {
-    if (st.p) HIP_OK(c, hipHostFree(st.p));
-    st.p = nullptr;
-    st.bytes = 0;
-    const size_t want = need + need / 4;
-    void* q = nullptr;
-    HIP_OK(c, hipHostMalloc(&q, want, hipHostMallocDefault));
-    st.p = (char*)q;
-    st.bytes = want;
+  if (!st.done) {
+    if (c->no_alloc)
+      return fail(c, LMOP_ERR_STATE, "internal: staging event missing in a no-allocation call");
+    HIP_OK(c, hipEventCreateWithFlags(&st.done, hipEventDisableTiming));
+  }
+  if (c->no_alloc) {
+    // ordinary host memory: the copies from and to it are ordered by the
+    // slot's event like the pinned ones
+    if (st.host.size() < need + 16) st.host.resize(need + need / 4 + 16);
+    st.cur = (char*)(((uintptr_t)st.host.data() + 15) & ~(uintptr_t)15);
+    st.cur_bytes = st.host.size() - (size_t)(st.cur - st.host.data());
+  } else {
+    if (st.bytes < need) {
+      if (st.p) HIP_OK(c, hipHostFree(st.p));
+      st.p = nullptr;
+      st.bytes = 0;
+      const size_t want = need + need / 4;
+      void* q = nullptr;
+      HIP_OK(c, hipHostMalloc(&q, want, hipHostMallocDefault));
+      st.p = (char*)q;
+      st.bytes = want;
+    }
+    st.cur = st.p;
+    st.cur_bytes = st.bytes;
   }
   st.used = 0;
   return LMOP_OK;
 }
 
-// Copies n elements into slot k (16-byte aligned) and returns the pinned copy.
+// Copies n elements into slot k (16-byte aligned) and returns the staged copy.
 template <typename T>
 lmop_status stage_put(lmop_ctx* c, int k, const T* src, size_t n, T** out) {
   auto& st = c->stage[k];
   const size_t off = (st.used + 15) & ~(size_t)15;
-  if (off + n * sizeof(T) > st.bytes)
+  if (off + n * sizeof(T) > st.cur_bytes)
     return fail(c, LMOP_ERR_STATE, "internal: staging slot overflow (%zu + %zu > %zu)", off,
-                n * sizeof(T), st.bytes);
-  *out = (T*)(st.p + off);
+                n * sizeof(T), st.cur_bytes);
+  *out = (T*)(st.cur + off);
   if (src && n) std::memcpy(*out, src, n * sizeof(T));
   st.used = off + n * sizeof(T);
   return LMOP_OK;
@@ -258,6 +347,7 @@ hipEvent_t take_event(lmop_ctx* c) {
     c->ev_free.pop_back();
     return e;
   }
+  if (c->no_alloc) return nullptr;  // that launch is counted, not timed
   hipEvent_t e = nullptr;
   if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
   return e;
@@ -482,7 +572,7 @@ lmop_status upload(lmop_ctx* c, const void* src, size_t bytes, bool on_device, v
 }
 
 void free_weights(lmop_ctx* c) {
-  for (void* p : c->weight_allocs) (void)hipFree(p);
+  for (void* p : c->weight_allocs) (void)dev_free(c, p);
   c->weight_allocs.clear();
   c->layers.clear();
   c->emb = c->head = nullptr;
@@ -545,7 +635,7 @@ lmop_status pack(lmop_ctx* c, const lmop_qmat* const* srcs, int n_src, const std
                            c->stream));
   LMOP_TRY(timed(c, "repack_w4", 0, 0, [&] { return launch_repack_w4(c->stream, rs, (const int32_t*)dmap, w); }));
   HIP_OK(c, hipStreamSynchronize(c->stream));
-  for (void* p : staging) HIP_OK(c, hipFree(p));
+  for (void* p : staging) HIP_OK(c, dev_free(c, p));
   *out = w;
   return LMOP_OK;
 }
@@ -600,7 +690,7 @@ lmop_status pack_fp8(lmop_ctx* c, const lmop_qmat* const* srcs, int n_src,
   LMOP_TRY(timed(c, "repack_w8", 0, 0,
                  [&] { return launch_repack_w8(c->stream, rs, (const int32_t*)dmap, w); }));
   HIP_OK(c, hipStreamSynchronize(c->stream));
-  for (void* p : staging) HIP_OK(c, hipFree(p));
+  for (void* p : staging) HIP_OK(c, dev_free(c, p));
   *out = w;
   return LMOP_OK;
 }
@@ -632,6 +722,202 @@ std::vector<int32_t> concat_map(const int* rows, int n_parts, int np) {
   for (int s = 0; s < n_parts; ++s)
     for (int r = 0; r < rows[s]; ++r) m[j++] = (s << 24) | r;
   return m;
+}
+
+// ---------------------------------------------------------------- scratch plan
+// own-KV slots: each row starts at a multiple of 8 (16-byte aligned V^T runs);
+// the store has 64 spare slots so a row's last 64-key block stays in bounds
+int own_store_cap(int used) { return round_up(used + 64, 64); }
+
+// The largest sizes one call's scratch buffers reach.  A call computes its
+// plan before any device work, so that scratch carved from a caller's
+// workspace (or the static no-allocation array) is laid out once, and
+// library-allocated scratch is grown once.
+struct Need {
+  size_t T = 0, R = 0, W = 0;  // tokens, rows, attention work items of one forward pass
+  size_t last = 0;             // tokens whose final hidden state one pass keeps
+  size_t own_kv = 0;           // bytes of the own-KV store
+  size_t head_rows = 0;        // rows of one head pass (0: no head)
+  bool restricted = false;     // restricted head: no vocabulary partials
+  bool dump = false;           // a [head_rows][vocab] logit dump
+  size_t n_sel = 0;            // allowed-token list (0: no type tables)
+  size_t state_mask = 0;       // bytes of the automaton's state-mask table
+};
+
+// (name, bytes) of every scratch buffer of a call with these maxima, in
+// layout order; the names are the ones ws_get asks for
+std::vector<std::pair<const char*, size_t>> scratch_items(const lmop_ctx* c, const Need& n) {
+  const size_t d = c->cfg.d_model, V = c->cfg.vocab;
+  const size_t n_chunks = (V + kHeadVocabChunk - 1) / kHeadVocabChunk;
+  std::vector<std::pair<const char*, size_t>> it;
+  auto add = [&](const char* name, size_t bytes) { it.emplace_back(name, scratch_round(bytes)); };
+  // a batch whose rows all have empty suffixes still reads one row of x
+  const size_t T = std::max<size_t>(n.T, 1);
+  add("tok", T * 4);
+  add("pos", T * 4);
+  add("slot", T * 4);
+  add("rows", n.R * sizeof(AttnRow));
+  add("work", n.W * sizeof(int2));
+  add("x", T * d * 4);
+  add("h", T * d * 2);
+  add("q", T * c->nq_dim * 2);
+  add("att", T * c->nq_dim * 2);
+  add("act", T * c->f64 * 2);
+  add("last", n.last * 4);
+  add("xlast", n.last * d * 4);
+  add("attlast", n.last * c->nq_dim * 2);
+  add("own_kv", n.own_kv);
+  if (n.head_rows > 0) {
+    const size_t R = n.head_rows;
+    add("head_rowptr", R * sizeof(void*));
+    add("head_hn", R * d * 2);
+    add("head_part", n.restricted ? sizeof(float2) : R * n_chunks * sizeof(float2));
+    add("head_zsel", R * n.n_sel * 4);
+    add("head_pick", R * sizeof(HeadPick));
+    add("head_state", R * 4);
+    if (n.dump) add("dump", R * V * 4);
+  }
+  if (n.n_sel > 0) {
+    add("sel", V * 4);
+    add("allowed", n.n_sel * 4);
+    if (n.state_mask > 0) add("state_mask", n.state_mask);
+  }
+  return it;
+}
+
+size_t scratch_total(const lmop_ctx* c, const Need& n) {
+  size_t t = 0;
+  for (auto& i : scratch_items(c, n)) t += i.second;
+  return t;
+}
+
+// Lays out every scratch buffer of the call in the carved region, or grows
+// the library-allocated ones to their largest size up front.  The own-KV
+// store must hold finite values wherever attention reads past a row's keys
+// (masked keys still multiply their values by 0), so carved memory, which
+// may hold anything, is cleared.
+lmop_status reserve_scratch(lmop_ctx* c, const Need& n) {
+  const auto items = scratch_items(c, n);
+  if (!c->carving) {
+    for (auto& i : items) {
+      char* p;
+      LMOP_TRY(ws_get(c, i.first, i.second, &p, std::strcmp(i.first, "own_kv") == 0));
+    }
+    return LMOP_OK;
+  }
+  c->carved.clear();
+  size_t off = 0;
+  for (auto& i : items) {
+    c->carved[i.first] = {c->carve_base + off, i.second};
+    off += i.second;
+  }
+  if (off > c->carve_size)
+    return fail(c, LMOP_ERR_OOM, "the call needs %zu bytes of scratch, the %s holds %zu", off,
+                c->no_alloc ? "no-allocation array" : "workspace", c->carve_size);
+  if (!c->no_alloc) c->user_ws_peak = std::max(c->user_ws_peak, off);
+  auto kv = c->carved.find("own_kv");
+  if (kv != c->carved.end())
+    HIP_OK(c, launch_fill_u32(c->stream, kv->second.first, kv->second.second / 4, 0u));
+  return LMOP_OK;
+}
+
+// Batches of consecutive entries within `budget` tokens and kMaxBatchRows
+// entries; an entry longer than the budget forms a batch of its own.
+std::vector<std::pair<size_t, size_t>> make_batches(const std::vector<int>& len, int budget) {
+  std::vector<std::pair<size_t, size_t>> out;
+  for (size_t u0 = 0; u0 < len.size();) {
+    size_t u1 = u0;
+    int T = 0;
+    while (u1 < len.size() && (int)(u1 - u0) < kMaxBatchRows) {
+      if (u1 > u0 && T + len[u1] > budget) break;
+      T += len[u1];
+      ++u1;
+    }
+    out.emplace_back(u0, u1);
+    u0 = u1;
+  }
+  return out;
+}
+
+int attn_tiles(int n_q, int G) { return (n_q * G + ATTN_QTILE - 1) / ATTN_QTILE; }
+
+// The forward-pass maxima of a list of batches over entries of len[]
+void batch_need(const std::vector<int>& len, const std::vector<std::pair<size_t, size_t>>& batches,
+                int G, Need* n) {
+  for (auto& b : batches) {
+    size_t T = 0, W = 0, last = 0;
+    for (size_t u = b.first; u < b.second; ++u) {
+      T += len[u];
+      W += attn_tiles(len[u], G);
+      last += len[u] > 0;
+    }
+    n->T = std::max(n->T, T);
+    n->R = std::max(n->R, b.second - b.first);
+    n->W = std::max(n->W, W);
+    n->last = std::max(n->last, last);
+  }
+}
+
+// Row batches and own-KV placement of one lmop_eval_rows call.
+struct Schedule {
+  std::vector<std::pair<size_t, size_t>> batches;  // ranges of the distinct rows
+  std::vector<int> base_of, group_of;              // per batch: first slot, decode group
+  std::vector<int> group_cap;                      // per group: slots of its store
+  Need need;
+  int budget = 0;
+};
+
+// Own-KV placement.  Integer and automaton types decode further tokens for
+// a group of consecutive batches at once: the group's batches keep their KV
+// in one store, so each decode step is one forward over all live rows of the
+// group instead of one small forward per batch.  A group is bounded by
+// `group_bytes`, by the store's slot limit and by the token budget (a decode
+// step has one token per live row).  Single-step types need no KV after the
+// first step: one batch per group.  Each row's slots start at a multiple of
+// 8 and leave room for `dec` decoded tokens.
+void make_groups(const std::vector<int>& len, int dec, int budget, size_t slot_bytes,
+                 size_t group_bytes, Schedule* s) {
+  const auto& batches = s->batches;
+  const int n_batches = (int)batches.size();
+  s->base_of.assign(n_batches, 0);
+  s->group_of.assign(n_batches, 0);
+  s->group_cap.clear();
+  for (int b = 0; b < n_batches;) {
+    int b1 = b, used = 0;
+    size_t rows = 0;
+    while (b1 < n_batches) {
+      int slots = 0;
+      for (size_t u = batches[b1].first; u < batches[b1].second; ++u)
+        slots = round_up(slots + len[u] + dec, 8);
+      const size_t r = batches[b1].second - batches[b1].first;
+      if (b1 > b && (dec == 0 || (size_t)own_store_cap(used + slots) * slot_bytes > group_bytes ||
+                     own_store_cap(used + slots) > kMaxStoreSlots || rows + r > (size_t)budget))
+        break;
+      s->base_of[b1] = used;
+      s->group_of[b1] = (int)s->group_cap.size();
+      used += slots;
+      rows += r;
+      ++b1;
+    }
+    s->group_cap.push_back(own_store_cap(used));
+    b = b1;
+  }
+}
+
+// Largest budget in [1, want] for which fits(budget) holds, trying `want`
+// first; fits() keeps the plan of the budget it was last called with, so the
+// winner is evaluated last.  0 if not even a budget of 1 fits.
+template <typename F>
+int fit_budget(int want, F&& fits) {
+  if (fits(want)) return want;
+  if (want <= 1 || !fits(1)) return 0;
+  int lo = 1, hi = want;  // fits(lo), !fits(hi)
+  while (hi - lo > 1) {
+    const int mid = lo + (hi - lo) / 2;
+    (fits(mid) ? lo : hi) = mid;
+  }
+  fits(lo);
+  return lo;
 }
 
 // ---------------------------------------------------------------- forward
@@ -808,12 +1094,8 @@ void fill_segments(const lmop_prefix* p, AttnRow& r) {
     }
 }
 
-// own-KV slots: each row starts at a multiple of 8 (16-byte aligned V^T runs);
-// the store has 64 spare slots so a row's last 64-key block stays in bounds
-int own_store_cap(int used) { return round_up(used + 64, 64); }
-
 void add_work(std::vector<int2>& work, int row, int n_q, int G) {
-  const int tiles = (n_q * G + ATTN_QTILE - 1) / ATTN_QTILE;
+  const int tiles = attn_tiles(n_q, G);
   for (int t = 0; t < tiles; ++t) work.push_back(make_int2(row, t));
 }
 
@@ -847,7 +1129,7 @@ lmop_status run_head(lmop_ctx* c, int k, int R, const std::vector<const float*>&
   }));
   if (restricted) {
     // only the allowed tokens' logits; the dump's other entries stay NaN
-    if (dump_dev) HIP_OK(c, hipMemsetAsync(dump_dev, 0xFF, (size_t)R * V * 4, c->stream));
+    if (dump_dev) HIP_OK(c, launch_fill_u32(c->stream, dump_dev, (size_t)R * V, 0xFFFFFFFFu));
     LMOP_TRY(timed(c, "head_restricted", 2.0 * R * n_sel * d,
                    (double)R * d * 2 + (double)n_sel * d * 2 + (double)R * n_sel * 4, [&] {
                      return launch_head_restricted(c->stream, hn, R, d, c->head, d_allowed, n_sel,
@@ -893,6 +1175,25 @@ lmop_status run_head(lmop_ctx* c, int k, int R, const std::vector<const float*>&
   return LMOP_OK;
 }
 
+// Runs f with every scratch buffer carved from [base, base + bytes) (carve
+// false: library-allocated scratch); no_alloc also forbids device, pinned and
+// event allocations for the duration.
+template <typename F>
+lmop_status with_scratch(lmop_ctx* ctx, bool carve, char* base, size_t bytes, bool no_alloc,
+                         F&& f) {
+  ctx->carving = carve;
+  ctx->carve_base = carve ? base : nullptr;
+  ctx->carve_size = carve ? bytes : 0;
+  ctx->no_alloc = no_alloc;
+  const lmop_status st = f();
+  ctx->carving = false;
+  ctx->carve_base = nullptr;
+  ctx->carve_size = 0;
+  ctx->no_alloc = false;
+  ctx->carved.clear();
+  return st;
+}
+
 }  // namespace
 
 // ====================================================================== ABI
@@ -922,7 +1223,9 @@ lmop_status lmop_create(const lmop_config* cfg, int32_t device, void* hip_stream
   auto bail = [&](lmop_status st) {
     g_create_error = cp->err;
     if (!cp->host_only) {
-      if (cp->rope_tab) (void)hipFree(cp->rope_tab);
+      (void)dev_free(cp, cp->rope_tab);
+      for (auto& stg : cp->stage)
+        if (stg.done) (void)hipEventDestroy(stg.done);
       if (cp->own_stream && cp->stream) (void)hipStreamDestroy(cp->stream);
     }
     return st;
@@ -954,10 +1257,17 @@ lmop_status lmop_create(const lmop_config* cfg, int32_t device, void* hip_stream
   if (hip_stream) {
     c->stream = (hipStream_t)hip_stream;
   } else {
-    if (hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking) != hipSuccess)
+    // a blocking stream: work the caller queued on the null stream (torch's
+    // default stream) completes before the library's work starts
+    if (hipStreamCreateWithFlags(&c->stream, hipStreamDefault) != hipSuccess)
       return bail(fail(cp, LMOP_ERR_DEVICE, "hipStreamCreate failed"));
     c->own_stream = true;
   }
+  // the staging slots' events exist before any call, so that a
+  // no-allocation call creates none
+  for (auto& stg : c->stage)
+    if (hipEventCreateWithFlags(&stg.done, hipEventDisableTiming) != hipSuccess)
+      return bail(fail(cp, LMOP_ERR_DEVICE, "hipEventCreate failed"));
   // rotary table: cos/sin of pos * theta^(-2i/hd) in double, stored fp32
   const int half = cf.head_dim / 2;
   std::vector<float2> tab((size_t)cf.max_seq * half);
@@ -982,8 +1292,8 @@ const char* lmop_last_error(const lmop_ctx* ctx) {
 
 static void destroy_prefix_storage(lmop_prefix* p) {
   if (p->store && --p->store->refs == 0) {
-    if (p->store->kv) (void)hipFree(p->store->kv);
-    if (p->store->hidden) (void)hipFree(p->store->hidden);
+    (void)dev_free(p->ctx, p->store->kv);
+    (void)dev_free(p->ctx, p->store->hidden);
     delete p->store;
   }
   p->store = nullptr;
@@ -1004,9 +1314,8 @@ void lmop_destroy(lmop_ctx* ctx) {
   ctx->prefixes.clear();
   if (!ctx->host_only) {
     free_weights(ctx);
-    for (auto& kv : ctx->ws)
-      if (kv.second.first) (void)hipFree(kv.second.first);
-    if (ctx->rope_tab) (void)hipFree(ctx->rope_tab);
+    for (auto& kv : ctx->ws) (void)dev_free(ctx, kv.second.first);
+    (void)dev_free(ctx, ctx->rope_tab);
     for (auto& s : ctx->spans) {
       (void)hipEventDestroy(s.a);
       (void)hipEventDestroy(s.b);
@@ -1171,8 +1480,8 @@ static lmop_status make_prefixes(lmop_ctx* ctx, const lmop_prefix* parent, const
     auto fail_free = [&](lmop_status st) {
       // work already queued may still write the store
       (void)hipStreamSynchronize(ctx->stream);
-      if (store->kv) (void)hipFree(store->kv);
-      if (store->hidden) (void)hipFree(store->hidden);
+      (void)dev_free(ctx, store->kv);
+      (void)dev_free(ctx, store->hidden);
       delete store;
       return st;
     };
@@ -1186,15 +1495,34 @@ static lmop_status make_prefixes(lmop_ctx* ctx, const lmop_prefix* parent, const
     if (st != LMOP_OK) return fail_free(st);
     store->hidden = (float*)hid;
     // slots no prefix uses are read (masked) by attention: keep them finite
-    if (hipMemsetAsync(kv, 0, kv_bytes, ctx->stream) != hipSuccess)
-      return fail_free(fail(ctx, LMOP_ERR_DEVICE, "hipMemsetAsync of a prefix KV store failed"));
+    if (launch_fill_u32(ctx->stream, kv, kv_bytes / 4, 0u) != hipSuccess)
+      return fail_free(fail(ctx, LMOP_ERR_DEVICE, "clearing a prefix KV store failed"));
     const int G = cf.n_heads / cf.n_kv_heads;
-    for (int i0 = 0; i0 < n && st == LMOP_OK;) {
-      // prefixes [i0, i1) in one forward pass, within the default token budget
-      int i1 = i0, T = 0;
-      while (i1 < n && (i1 == i0 || T + len[i1] <= kDefaultBatchTokens) &&
-             i1 - i0 < kMaxBatchRows)
-        T += len[i1++];
+    // prefixes in forward passes within the default token budget, or within
+    // the largest budget whose scratch fits the carved region
+    std::vector<std::pair<size_t, size_t>> passes;
+    Need need;
+    auto plan = [&](int b) {
+      passes = make_batches(len, b);
+      need = Need();
+      batch_need(len, passes, G, &need);
+      return !ctx->carving || scratch_total(ctx, need) <= ctx->carve_size;
+    };
+    if (ctx->carving) {
+      if (fit_budget(kDefaultBatchTokens, plan) == 0)
+        return fail_free(fail(ctx, LMOP_ERR_OOM,
+                              "the workspace (%zu bytes) cannot hold the scratch of one prefix "
+                              "pass (%zu bytes)",
+                              ctx->carve_size, scratch_total(ctx, need)));
+    } else {
+      plan(kDefaultBatchTokens);
+    }
+    st = reserve_scratch(ctx, need);
+    if (st != LMOP_OK) return fail_free(st);
+    for (size_t pi = 0; pi < passes.size() && st == LMOP_OK; ++pi) {
+      const int i0 = (int)passes[pi].first, i1 = (int)passes[pi].second;
+      int T = 0;
+      for (int i = i0; i < i1; ++i) T += len[i];
       const int R = i1 - i0;
       std::vector<int32_t> tok(T), pos(T), slot(T), last(R);
       std::vector<AttnRow> rows(R);
@@ -1246,7 +1574,6 @@ static lmop_status make_prefixes(lmop_ctx* ctx, const lmop_prefix* parent, const
       }
       if (st == LMOP_OK) st = stage_mark(ctx, 0);
       if (st == LMOP_OK) st = sync(ctx);
-      i0 = i1;
     }
     if (st != LMOP_OK) return fail_free(st);
     store->refs = n;
@@ -1294,7 +1621,8 @@ lmop_status lmop_set_prefix(lmop_ctx* ctx, const lmop_prefix* parent, const int3
     return fail(ctx, LMOP_ERR_INVALID_ARG, "prefix length %d exceeds max_seq %d",
                 prefix_total(parent) + n_tokens, ctx->cfg.max_seq);
   const int64_t offs[2] = {0, n_tokens};
-  return make_prefixes(ctx, parent, tokens, offs, 1, out);
+  return with_scratch(ctx, ctx->user_ws_bytes > 0, ctx->user_ws, ctx->user_ws_bytes, false,
+                      [&] { return make_prefixes(ctx, parent, tokens, offs, 1, out); });
 }
 
 lmop_status lmop_set_prefixes(lmop_ctx* ctx, const lmop_prefix* parent, const int32_t* tokens,
@@ -1316,7 +1644,8 @@ lmop_status lmop_set_prefixes(lmop_ctx* ctx, const lmop_prefix* parent, const in
                   (long long)(prefix_total(parent) + len), ctx->cfg.max_seq);
   }
   LMOP_TRY(check_tokens(ctx, tokens, offsets[n], "prefix"));
-  return make_prefixes(ctx, parent, tokens, offsets, n, out);
+  return with_scratch(ctx, ctx->user_ws_bytes > 0, ctx->user_ws, ctx->user_ws_bytes, false,
+                      [&] { return make_prefixes(ctx, parent, tokens, offsets, n, out); });
 }
 
 static void maybe_free_prefix(lmop_ctx* ctx, lmop_prefix* p) {
@@ -1360,11 +1689,12 @@ lmop_status lmop_dedup_rows(const int32_t* tokens, const int64_t* offsets, int32
   return LMOP_OK;
 }
 
-lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
-                           const lmop_prefix* const* row_prefix, const int32_t* tokens,
-                           const int64_t* offsets, int32_t n_rows, const lmop_type* type,
-                           lmop_result* out, const lmop_eval_opts* opts) {
-  LMOP_TRY(enter(ctx));
+// lmop_eval_rows with the scratch mode the ctx is in (library-allocated,
+// carved from the caller's workspace, or carved from the static array)
+static lmop_status eval_rows_impl(lmop_ctx* ctx, const lmop_prefix* prefix,
+                                  const lmop_prefix* const* row_prefix, const int32_t* tokens,
+                                  const int64_t* offsets, int32_t n_rows, const lmop_type* type,
+                                  lmop_result* out, const lmop_eval_opts* opts) {
   if (!ctx->loaded) return fail(ctx, LMOP_ERR_STATE, "lmop_load_weights has not succeeded");
   if (n_rows < 0) return fail(ctx, LMOP_ERR_INVALID_ARG, "n_rows < 0");
   LMOP_TRY(check_type(ctx, type));
@@ -1404,8 +1734,6 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
   const int limit = opts ? opts->limit : 0;
   const int64_t limit_value = opts ? opts->limit_value : 0;
   if (limit < 0) return fail(ctx, LMOP_ERR_INVALID_ARG, "limit < 0");
-  if (ctx->host_only)
-    return fail(ctx, LMOP_ERR_UNSUPPORTED, "host-only ctx: arguments are valid, no device to run");
 
   const bool restricted = (flags & LMOP_HEAD_RESTRICTED) != 0;
   int budget = opts && opts->max_batch_tokens > 0 ? opts->max_batch_tokens : kDefaultBatchTokens;
@@ -1461,13 +1789,6 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
   const int n_sel = (int)allowed.size();
   const int n_allowed0 = is_aut ? n_sel : type->n_tokens;
   for (int i = 0; i < n_sel; ++i) sel[allowed[i]] = i;
-  int32_t *d_sel, *d_allowed;
-  LMOP_TRY(ws_get(ctx, "sel", V, &d_sel));
-  LMOP_TRY(ws_get(ctx, "allowed", n_sel, &d_allowed));
-  HIP_OK(ctx, hipMemcpyAsync(d_sel, sel.data(), V * 4, hipMemcpyHostToDevice, ctx->stream));
-  HIP_OK(ctx, hipMemcpyAsync(d_allowed, allowed.data(), n_sel * 4, hipMemcpyHostToDevice,
-                             ctx->stream));
-  uint8_t* d_state_mask = nullptr;
   std::vector<uint8_t> state_mask;
   if (is_aut) {
     const int S = aut->n_states;
@@ -1478,68 +1799,11 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
       if (aut->accepting[st] && type->eos_token >= 0)
         state_mask[(size_t)st * n_sel + n_sel - 1] = 1;
     }
-    LMOP_TRY(ws_get(ctx, "state_mask", state_mask.size(), &d_state_mask));
-    HIP_OK(ctx, hipMemcpyAsync(d_state_mask, state_mask.data(), state_mask.size(),
-                               hipMemcpyHostToDevice, ctx->stream));
   }
-  HIP_OK(ctx, hipStreamSynchronize(ctx->stream));
 
   const int G = cf.n_heads / cf.n_kv_heads;
   const int d = cf.d_model;
   std::vector<lmop_result> res(n_rows);
-  // batches: consecutive runs of distinct rows within the token budget
-  std::vector<std::pair<size_t, size_t>> batches;
-  for (size_t u0 = 0; u0 < uniq.size();) {
-    size_t u1 = u0;
-    int T = 0;
-    while (u1 < uniq.size() && (int)(u1 - u0) < kMaxBatchRows) {
-      const int len = (int)(offsets[uniq[u1] + 1] - offsets[uniq[u1]]);
-      if (u1 > u0 && T + len > budget) break;
-      T += len;
-      ++u1;
-    }
-    batches.emplace_back(u0, u1);
-    u0 = u1;
-  }
-
-  // Own-KV placement.  Integer types decode their further tokens for a group
-  // of consecutive batches at once: the group's batches keep their KV in one
-  // store, so each decode step is one forward over all live rows of the
-  // group instead of one small forward per batch.  A group is bounded by the
-  // store's size and by the token budget (a decode step has one token per
-  // live row).  Other types need no KV after the first step: one batch each.
-  const size_t slot_bytes = (size_t)cf.n_layers * 2 * ctx->nkv_dim * 2;
-  size_t group_bytes = kDecodeGroupBytes;
-  if (dec > 0) {
-    size_t free_b = 0, total_b = 0;
-    if (hipMemGetInfo(&free_b, &total_b) == hipSuccess)
-      group_bytes = std::max<size_t>(std::min(group_bytes, free_b / 2), 1);
-  }
-  const int n_batches = (int)batches.size();
-  std::vector<int> base_of(n_batches), group_of(n_batches);
-  std::vector<int> group_cap;
-  for (int b = 0; b < n_batches;) {
-    int b1 = b, used = 0;
-    size_t rows = 0;
-    std::vector<int> base;
-    while (b1 < n_batches) {
-      int slots = 0;
-      for (size_t u = batches[b1].first; u < batches[b1].second; ++u)
-        slots = round_up(slots + (int)(offsets[uniq[u] + 1] - offsets[uniq[u]]) + dec, 8);
-      const size_t r = batches[b1].second - batches[b1].first;
-      if (b1 > b && (dec == 0 || (size_t)own_store_cap(used + slots) * slot_bytes > group_bytes ||
-                     own_store_cap(used + slots) > kMaxStoreSlots || rows + r > (size_t)budget))
-        break;
-      base_of[b1] = used;
-      group_of[b1] = (int)group_cap.size();
-      used += slots;
-      rows += r;
-      ++b1;
-    }
-    group_cap.push_back(own_store_cap(used));
-    b = b1;
-  }
-
   // per distinct row (index into uniq): own tokens, slot of own token 0 in
   // its group's store, last chosen token
   std::vector<int> row_len(uniq.size()), own_slot(uniq.size());
@@ -1547,6 +1811,100 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
   std::vector<int32_t> row_state(uniq.size(), 0);  // automaton state
   for (size_t u = 0; u < uniq.size(); ++u)
     row_len[u] = (int)(offsets[uniq[u] + 1] - offsets[uniq[u]]);
+
+  // The plan: batches within the token budget, decode groups, scratch sizes.
+  // Library-allocated scratch takes the requested budget and decode groups
+  // of at most kDecodeGroupBytes (and half the free memory); carved scratch
+  // takes the largest budget whose plan fits, the own-KV store getting what
+  // the other buffers leave.
+  const size_t slot_bytes = (size_t)cf.n_layers * 2 * ctx->nkv_dim * 2;
+  const int tiles1 = attn_tiles(1, G);
+  Schedule sch;
+  auto plan = [&](int b, size_t group_bytes) {
+    sch = Schedule();
+    sch.budget = b;
+    sch.batches = make_batches(row_len, b);
+    Need& n = sch.need;
+    batch_need(row_len, sch.batches, G, &n);
+    n.head_rows = n.R;
+    n.restricted = restricted;
+    n.dump = dbg != nullptr;
+    n.n_sel = (size_t)n_sel;
+    n.state_mask = state_mask.size();
+    if (dec > 0) {
+      // a decode step over every live row of a group: at most the group's rows
+      const size_t ub = std::max(n.R, std::min((size_t)b, uniq.size()));
+      Need other = n;
+      other.T = std::max(other.T, ub);
+      other.R = other.head_rows = std::max(other.R, ub);
+      other.W = std::max(other.W, ub * tiles1);
+      if (ctx->carving) {
+        const size_t rest = scratch_total(ctx, other);
+        if (rest + 256 >= ctx->carve_size) return false;
+        group_bytes = ctx->carve_size - rest - 256;
+      }
+    }
+    make_groups(row_len, dec, b, slot_bytes, group_bytes, &sch);
+    size_t kv_slots = 0;
+    for (size_t g = 0; g < sch.group_cap.size(); ++g) {
+      kv_slots = std::max(kv_slots, (size_t)sch.group_cap[g]);
+      if (dec > 0) {
+        size_t rows = 0;
+        for (size_t bi = 0; bi < sch.batches.size(); ++bi)
+          if ((size_t)sch.group_of[bi] == g) rows += sch.batches[bi].second - sch.batches[bi].first;
+        n.T = std::max(n.T, rows);
+        n.R = std::max(n.R, rows);
+        n.W = std::max(n.W, rows * tiles1);
+        n.head_rows = std::max(n.head_rows, rows);
+      }
+    }
+    n.own_kv = kv_slots * slot_bytes;
+    return !ctx->carving || scratch_total(ctx, n) <= ctx->carve_size;
+  };
+  if (ctx->carving) {
+    if (fit_budget(budget, [&](int b) { return plan(b, 0); }) == 0) {
+      const int longest = row_len.empty() ? 0 : *std::max_element(row_len.begin(), row_len.end());
+      return fail(ctx, LMOP_ERR_OOM,
+                  "the %s (%zu bytes) cannot hold the scratch of one batch: a row of %d tokens "
+                  "needs %zu bytes",
+                  ctx->no_alloc ? "no-allocation scratch array" : "workspace", ctx->carve_size,
+                  longest, scratch_total(ctx, sch.need));
+    }
+  } else {
+    size_t group_bytes = kDecodeGroupBytes;
+    if (dec > 0 && !ctx->host_only) {
+      size_t free_b = 0, total_b = 0;
+      if (hipMemGetInfo(&free_b, &total_b) == hipSuccess)
+        group_bytes = std::max<size_t>(std::min(group_bytes, free_b / 2), 1);
+    }
+    plan(budget, group_bytes);
+  }
+  if (ctx->host_only)
+    return fail(ctx, LMOP_ERR_UNSUPPORTED,
+                "host-only ctx: arguments are valid and the plan fits (%zu batches, %zu bytes of "
+                "scratch), no device to run",
+                sch.batches.size(), scratch_total(ctx, sch.need));
+  LMOP_TRY(reserve_scratch(ctx, sch.need));
+  const auto& batches = sch.batches;
+  const auto& base_of = sch.base_of;
+  const auto& group_of = sch.group_of;
+  const auto& group_cap = sch.group_cap;
+  budget = sch.budget;
+
+  int32_t *d_sel, *d_allowed;
+  LMOP_TRY(ws_get(ctx, "sel", V, &d_sel));
+  LMOP_TRY(ws_get(ctx, "allowed", n_sel, &d_allowed));
+  HIP_OK(ctx, hipMemcpyAsync(d_sel, sel.data(), V * 4, hipMemcpyHostToDevice, ctx->stream));
+  HIP_OK(ctx, hipMemcpyAsync(d_allowed, allowed.data(), n_sel * 4, hipMemcpyHostToDevice,
+                             ctx->stream));
+  uint8_t* d_state_mask = nullptr;
+  if (is_aut) {
+    LMOP_TRY(ws_get(ctx, "state_mask", state_mask.size(), &d_state_mask));
+    HIP_OK(ctx, hipMemcpyAsync(d_state_mask, state_mask.data(), state_mask.size(),
+                               hipMemcpyHostToDevice, ctx->stream));
+  }
+  HIP_OK(ctx, hipStreamSynchronize(ctx->stream));
+  const int n_batches = (int)batches.size();
 
   // A batch between enqueue and collect: where its first step's picks land.
   struct InFlight {
@@ -1813,6 +2171,57 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
       std::memcpy(dbg + (size_t)r * steps * V, dbg + (size_t)rep[r] * steps * V,
                   (size_t)steps * V * sizeof(float));
   }
+  // a large library-allocated own-KV store is returned after the call
+  if (!ctx->carving) {
+    auto it = ctx->ws.find("own_kv");
+    if (it != ctx->ws.end() && it->second.second > kKeepOwnKvBytes)
+      LMOP_TRY(ws_release(ctx, "own_kv"));
+  }
+  return LMOP_OK;
+}
+
+lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
+                           const lmop_prefix* const* row_prefix, const int32_t* tokens,
+                           const int64_t* offsets, int32_t n_rows, const lmop_type* type,
+                           lmop_result* out, const lmop_eval_opts* opts) {
+  LMOP_TRY(enter(ctx));
+  return with_scratch(ctx, ctx->user_ws_bytes > 0, ctx->user_ws, ctx->user_ws_bytes, false, [&] {
+    return eval_rows_impl(ctx, prefix, row_prefix, tokens, offsets, n_rows, type, out, opts);
+  });
+}
+
+lmop_status lmop_set_workspace(lmop_ctx* ctx, void* dev_ptr, size_t bytes) {
+  LMOP_TRY(enter(ctx));
+  if ((dev_ptr == nullptr) != (bytes == 0))
+    return fail(ctx, LMOP_ERR_INVALID_ARG, "a workspace needs both a pointer and a size");
+  if (((uintptr_t)dev_ptr & 255) != 0)
+    return fail(ctx, LMOP_ERR_INVALID_ARG, "the workspace must be 256-byte aligned");
+  if (dev_ptr && !ctx->host_only) {
+    hipPointerAttribute_t at;
+    if (hipPointerGetAttributes(&at, dev_ptr) != hipSuccess || at.type != hipMemoryTypeDevice ||
+        at.device != ctx->device) {
+      (void)hipGetLastError();
+      return fail(ctx, LMOP_ERR_INVALID_ARG, "the workspace is not device memory of device %d",
+                  ctx->device);
+    }
+  }
+  if (!ctx->host_only) {
+    // the previous workspace (or library scratch) may still be read
+    HIP_OK(ctx, hipStreamSynchronize(ctx->stream));
+    if (dev_ptr) LMOP_TRY(ws_release_all(ctx));
+  }
+  ctx->user_ws = (char*)dev_ptr;
+  ctx->user_ws_bytes = bytes;
+  ctx->user_ws_peak = 0;
+  return LMOP_OK;
+}
+
+lmop_status lmop_get_memory(const lmop_ctx* ctx, lmop_memory_stats* out) {
+  if (!ctx || !out) return LMOP_ERR_INVALID_ARG;
+  out->device_bytes = ctx->dev_bytes;
+  out->device_peak = ctx->dev_peak;
+  out->workspace_bytes = ctx->user_ws_bytes;
+  out->workspace_peak = ctx->user_ws_peak;
   return LMOP_OK;
 }
 

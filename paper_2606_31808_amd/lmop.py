@@ -28,7 +28,8 @@ LMOP_HEAD_RESTRICTED = 2
 EXPORTED = (
     "lmop_create", "lmop_destroy", "lmop_last_error", "lmop_status_string", "lmop_load_weights",
     "lmop_set_prefix", "lmop_set_prefixes", "lmop_release_prefix", "lmop_prefix_length", "lmop_eval_rows",
-    "lmop_dedup_rows", "lmop_set_profiling", "lmop_get_kernel_stats",
+    "lmop_dedup_rows", "lmop_set_profiling", "lmop_get_kernel_stats", "lmop_set_workspace",
+    "lmop_get_memory",
 )
 
 
@@ -79,6 +80,11 @@ class lmop_eval_opts(C.Structure):
                 ("limit_value", C.c_int64), ("row_mask", C.POINTER(C.c_uint8))]
 
 
+class lmop_memory_stats(C.Structure):
+    _fields_ = [("device_bytes", C.c_uint64), ("device_peak", C.c_uint64),
+                ("workspace_bytes", C.c_uint64), ("workspace_peak", C.c_uint64)]
+
+
 class lmop_kernel_stat(C.Structure):
     _fields_ = [("name", C.c_char * 48), ("launches", C.c_int64), ("timed_launches", C.c_int64),
                 ("total_ms", C.c_double), ("flops", C.c_double), ("bytes", C.c_double)]
@@ -113,6 +119,8 @@ def _load():
         "lmop_eval_rows": (st, [vp, vp, C.POINTER(vp), C.POINTER(C.c_int32),
                                 C.POINTER(C.c_int64), i32, C.POINTER(lmop_type), vp,
                                 C.POINTER(lmop_eval_opts)]),
+        "lmop_set_workspace": (st, [vp, vp, C.c_size_t]),
+        "lmop_get_memory": (st, [vp, C.POINTER(lmop_memory_stats)]),
         "lmop_dedup_rows": (st, [C.POINTER(C.c_int32), C.POINTER(C.c_int64), i32,
                                  C.POINTER(C.c_int64), C.POINTER(C.c_int32),
                                  C.POINTER(C.c_int32)]),
@@ -303,6 +311,18 @@ def lmop_dedup_rows(tokens, offsets, keys=None):
     return rep, int(nu.value)
 
 
+def lmop_set_workspace(ctx, ptr: int, nbytes: int) -> None:
+    """Scratch carved from the caller's device memory [ptr, ptr + nbytes)
+    (e.g. a torch tensor's data_ptr()); (0, 0) returns to library scratch."""
+    _check(_lib.lmop_set_workspace(ctx, C.c_void_p(ptr or None), C.c_size_t(nbytes)), ctx)
+
+
+def lmop_get_memory(ctx) -> dict:
+    m = lmop_memory_stats()
+    _check(_lib.lmop_get_memory(ctx, C.byref(m)), ctx)
+    return {k: int(getattr(m, k)) for k, _ in lmop_memory_stats._fields_}
+
+
 def lmop_set_profiling(ctx, period) -> None:
     """period: False/0 off, True/1 time every launch, N time every N-th launch
     of each kernel."""
@@ -367,6 +387,12 @@ class Context:
         return lmop_eval_rows(self.ctx, tokens, offsets, kind, allowed, eos, max_tokens, prefix,
                               row_prefix, flags, max_batch_tokens, debug_logits, self.vocab,
                               limit, limit_value, row_mask)
+
+    def set_workspace(self, ptr: int, nbytes: int):
+        lmop_set_workspace(self.ctx, ptr, nbytes)
+
+    def memory(self) -> dict:
+        return lmop_get_memory(self.ctx)
 
     def set_profiling(self, period):
         lmop_set_profiling(self.ctx, period)

@@ -363,6 +363,29 @@ def test_tiny_automaton_equals_enum_and_int(tiny, L):
     ctx.release_prefix(pre)
 
 
+def _take(ref, rows):
+    """The oracle's results for the listed rows only."""
+    out = {k: np.asarray(v)[rows] for k, v in ref.items() if k != "logits"}
+    if "logits" in ref:
+        out["logits"] = [ref["logits"][r] for r in rows]
+    return out
+
+
+def _check_limit_vs_oracle(ref, out, dbg, k, v, label):
+    """Against the oracle: the k-th row (table order) whose oracle value is v
+    is where the scan must stop, and every row up to it is evaluated when the
+    oracle's margins there exceed 0.1 (their values are then certain); every
+    evaluated row's logits are within the tolerance of the oracle's."""
+    ev = np.nonzero(out["n_tokens"] > 0)[0]
+    st = compare(_take(ref, ev), out[ev], dbg[ev], label)
+    hits = np.nonzero(ref["value"] == v)[0]
+    stop = int(hits[k - 1]) if len(hits) >= k else len(out) - 1
+    if np.all(ref["margin"][: stop + 1] > 0.1):
+        assert np.all(out["n_tokens"][: stop + 1] > 0), f"{label}: a row before the stop skipped"
+        assert np.sum(out["value"][ev] == v) >= min(k, len(hits)), label
+    return st, stop
+
+
 def _check_limit(full, out, k, v, label):
     """Rows up to the k-th with value v equal the full evaluation bit for bit;
     later rows are either evaluated (and equal) or marked skipped."""
@@ -387,14 +410,18 @@ def test_tiny_limit_early_exit(tiny, L):
     # duplicates (dedup) and small batches, so the stop comes early
     idx = np.array(list(range(64)) + [3, 3, 10, 5, 63, 0])
     sub = wl.subset(idx)
-    full, _ = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, prefix=pre,
-                            max_batch_tokens=64)
-    v = int(np.bincount(full["value"]).argmax())
+    full, dfull = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, prefix=pre,
+                                max_batch_tokens=64, debug_logits=True)
+    ref = orc.eval_workload(sub, keep_logits=True)
+    compare(ref, full, dfull, "limit: whole table")
+    # the wanted value is the oracle's most frequent one
+    v = int(np.bincount(ref["value"]).argmax())
     for k in (1, 4, 9):
-        out, _ = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, prefix=pre,
-                               max_batch_tokens=64, limit=k, limit_value=v)
+        out, dbg = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, prefix=pre,
+                                 max_batch_tokens=64, limit=k, limit_value=v, debug_logits=True)
         n_eval = _check_limit(full, out, k, v, f"limit {k}")
-        _log(f"limit {k}: {n_eval} of {len(idx)} rows evaluated")
+        st, stop = _check_limit_vs_oracle(ref, out, dbg, k, v, f"limit {k} vs oracle")
+        _log(f"limit {k}: {n_eval} of {len(idx)} rows evaluated, oracle stop row {stop}, {st}")
         assert n_eval < len(idx)
     # more than the table holds: every row is evaluated
     out, _ = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, prefix=pre,
@@ -410,10 +437,17 @@ def test_tiny_limit_early_exit(tiny, L):
     eos = int(next(t for t in range(TINY.vocab) if t not in digits))
     fi, _ = ctx.eval_rows(sub.tokens, sub.offsets, KIND_INT, digits, eos=eos, max_tokens=3,
                           prefix=pre, max_batch_tokens=64)
-    vi = int(np.bincount(fi["value"]).argmax())
-    oi, _ = ctx.eval_rows(sub.tokens, sub.offsets, KIND_INT, digits, eos=eos, max_tokens=3,
-                          prefix=pre, max_batch_tokens=64, limit=2, limit_value=vi)
+    refi = orc.eval_rows(wl.prefix, [sub.suffix(r) for r in range(sub.n_rows)], KIND_INT, digits,
+                         eos=eos, max_tokens=3, keep_logits=True)
+    vi = int(np.bincount(refi["value"]).argmax())
+    oi, di = ctx.eval_rows(sub.tokens, sub.offsets, KIND_INT, digits, eos=eos, max_tokens=3,
+                           prefix=pre, max_batch_tokens=64, limit=2, limit_value=vi,
+                           debug_logits=True)
     _check_limit(fi, oi, 2, vi, "int limit")
+    ev = np.nonzero(oi["n_tokens"] > 0)[0]
+    if all(list(oi["tokens"][r][: oi["n_tokens"][r]]) == list(refi["tokens"][r][: refi["n_tokens"][r]])
+           for r in ev):
+        _check_limit_vs_oracle(refi, oi, di, 2, vi, "int limit vs oracle")
     ctx.release_prefix(pre)
 
 
@@ -451,9 +485,20 @@ def test_tiny_cascade_row_mask(tiny, L):
     first, _ = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, prefix=pre)
     keep = first["value"] == 1
     assert 0 < keep.sum() < len(idx)
+    # the first predicate's mask agrees with the oracle's wherever the
+    # oracle's margin decides it
+    ref1 = orc.eval_workload(sub)
+    sure = ref1["margin"] > 0.1
+    assert np.array_equal(keep[sure], ref1["value"][sure] == 1)
     opts2 = np.random.default_rng(41).choice(TINY.vocab, 6, replace=False).astype(np.int32)
     second, d2 = ctx.eval_rows(sub.tokens, sub.offsets, KIND_ENUM, opts2, prefix=pre,
                                row_mask=keep, debug_logits=True)
+    # the rows the mask keeps against the oracle's second predicate on them
+    kept_rows = np.nonzero(keep)[0]
+    ref2 = orc.eval_rows(wl.prefix, [sub.suffix(int(r)) for r in kept_rows], KIND_ENUM, opts2,
+                         keep_logits=True)
+    _log("cascade second predicate vs oracle",
+         compare(ref2, second[kept_rows], d2[kept_rows], "cascade second"))
     alone = sub.subset(np.nonzero(keep)[0])
     ref, dref = ctx.eval_rows(alone.tokens, alone.offsets, KIND_ENUM, opts2, prefix=pre,
                               debug_logits=True)
@@ -870,3 +915,64 @@ def test_tiny_dedup_and_batch_invariance(tiny, L):
     op, dp = _run(ctx, pw, pre)
     assert np.array_equal(op, full[perm]) and np.array_equal(dp, dfull[perm])
     ctx.release_prefix(pre)
+
+
+def test_tiny_workspace(tiny, L):
+    """Scratch carved from a caller's torch allocation: the same bits as
+    library-allocated scratch, also when the workspace is small enough to
+    force smaller batches and decode groups; the library allocates no scratch
+    of its own meanwhile; a workspace too small for one row is LMOP_ERR_OOM
+    with a readable message."""
+    w, orc, ref_ctx = tiny
+    wl = make_workload("filter_tiny")
+    digits = np.random.default_rng(3).choice(TINY.vocab, 10, replace=False).astype(np.int32)
+    eos = int(next(t for t in range(TINY.vocab) if t not in digits))
+    pre_ref = ref_ctx.set_prefix(wl.prefix)
+    want_b, dwant_b = ref_ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, prefix=pre_ref,
+                                        debug_logits=True)
+    want_i, dwant_i = ref_ctx.eval_rows(wl.tokens, wl.offsets, KIND_INT, digits, eos=eos,
+                                        max_tokens=4, prefix=pre_ref, debug_logits=True)
+    ref_ctx.release_prefix(pre_ref)
+    ctx = L.Context(TINY, device=0, stream=torch.cuda.current_stream().cuda_stream)
+    ctx.load_weights(w)
+    held = ctx.memory()["device_bytes"]  # weights and the rotary table
+    for mib in (64, 2):
+        # NaN bit patterns everywhere: whatever must start at zero is cleared
+        buf = torch.full((mib << 18,), float("nan"), dtype=torch.float32, device="cuda")
+        torch.cuda.synchronize()
+        ctx.set_workspace(buf.data_ptr(), buf.numel() * 4)
+        pre = ctx.set_prefix(wl.prefix)
+        with_prefix = ctx.memory()["device_bytes"]
+        got_b, dgot_b = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, prefix=pre,
+                                      debug_logits=True)
+        got_i, dgot_i = ctx.eval_rows(wl.tokens, wl.offsets, KIND_INT, digits, eos=eos,
+                                      max_tokens=4, prefix=pre, debug_logits=True)
+        assert got_b.tobytes() == want_b.tobytes() and np.array_equal(dgot_b, dwant_b), mib
+        assert got_i.tobytes() == want_i.tobytes(), mib
+        assert np.array_equal(dgot_i, dwant_i, equal_nan=True), mib
+        mem = ctx.memory()
+        assert mem["device_bytes"] == with_prefix  # no scratch of the library's own
+        assert 0 < mem["workspace_peak"] <= mem["workspace_bytes"] == mib << 20
+        _log(f"workspace {mib} MiB: peak {mem['workspace_peak']} bytes, library holds "
+             f"{mem['device_bytes']} (weights {held})")
+        ctx.release_prefix(pre)
+        ctx.set_workspace(0, 0)
+        del buf
+    small = torch.empty(1 << 14, dtype=torch.float32, device="cuda")
+    ctx.set_workspace(small.data_ptr(), small.numel() * 4)
+    pre = None
+    with pytest.raises(L.LmopError) as ei:
+        pre = ctx.set_prefix(wl.prefix)
+    assert ei.value.status == L.LMOP_ERR_OOM and "workspace" in str(ei.value)
+    ctx.set_workspace(0, 0)
+    pre = ctx.set_prefix(wl.prefix)
+    ctx.set_workspace(small.data_ptr(), small.numel() * 4)
+    with pytest.raises(L.LmopError) as ei:
+        ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, prefix=pre)
+    assert ei.value.status == L.LMOP_ERR_OOM and "bytes" in str(ei.value)
+    # the ctx stays usable after the failed call
+    ctx.set_workspace(0, 0)
+    again, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, prefix=pre)
+    assert again.tobytes() == want_b.tobytes()
+    ctx.release_prefix(pre)
+    ctx.close()

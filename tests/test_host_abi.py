@@ -70,13 +70,11 @@ def test_state_and_weight_validation(tiny_w):
     _expect(L.LMOP_ERR_INVALID_ARG, ctx.load_weights, bad)
     import dataclasses
     l0 = tiny_w.layers[0]
-    wrong = dataclasses.replace(l0, wo=l0.wq)  # same shape only because d == nq*hd here
     tiny_w.layers[0] = dataclasses.replace(l0, w_down=l0.w_gate)
     try:
         _expect(L.LMOP_ERR_INVALID_ARG, ctx.load_weights, tiny_w)
     finally:
         tiny_w.layers[0] = l0
-    del wrong
     ctx.load_weights(tiny_w)
 
 
@@ -298,3 +296,36 @@ def test_binding_shares_torchs_hip_runtime():
     torch_lib = os.path.realpath(os.path.join(os.path.dirname(torch.__file__), "lib"))
     assert len(paths) == 1, paths
     assert os.path.realpath(paths[0]).startswith(torch_lib), paths
+
+
+def test_workspace_validation_and_plan(tiny_w):
+    """lmop_set_workspace checks its arguments; on a host-only ctx the call
+    still plans its batches against the workspace, so a workspace too small
+    for one row is LMOP_ERR_OOM, and one that holds a row but not the
+    default token budget is a valid (smaller-batch) plan."""
+    from synth import make_workload
+    ctx = _host_ctx()
+    ctx.load_weights(tiny_w)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.set_workspace, 0x1000, 0)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.set_workspace, 0, 4096)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.set_workspace, 0x1010, 4096)
+    wl = make_workload("filter_tiny")
+    args = (wl.tokens, wl.offsets, wl.kind, wl.allowed)
+    # no device is touched: the pointer is only a number to a host-only ctx
+    ctx.set_workspace(1 << 20, 64 << 10)
+    msg = _expect(L.LMOP_ERR_OOM, ctx.eval_rows, *args)
+    assert "workspace" in msg and "bytes" in msg
+    ctx.set_workspace(1 << 20, 2 << 20)
+    msg = _expect(L.LMOP_ERR_UNSUPPORTED, ctx.eval_rows, *args)
+    n_small = int(msg.split(" batches")[0].split("(")[-1])
+    ctx.set_workspace(1 << 20, 1 << 30)
+    msg = _expect(L.LMOP_ERR_UNSUPPORTED, ctx.eval_rows, *args)
+    n_big = int(msg.split(" batches")[0].split("(")[-1])
+    assert n_big == 1 and n_small > 1  # the whole table fits one default batch
+    # integer outputs: decode groups are sized from the workspace too
+    digits = np.arange(10, 20, dtype=np.int32)
+    _expect(L.LMOP_ERR_UNSUPPORTED, ctx.eval_rows, wl.tokens, wl.offsets, L.LMOP_INT, digits,
+            eos=5, max_tokens=4)
+    ctx.set_workspace(0, 0)
+    mem = ctx.memory()
+    assert mem["workspace_bytes"] == 0 and mem["device_bytes"] == 0
