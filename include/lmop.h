@@ -246,6 +246,28 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
                            const int64_t* offsets, int32_t n_rows, const lmop_type* type,
                            lmop_result* out, const lmop_eval_opts* opts);
 
+/* Scratch for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation):
+ * lmop_eval_rows with every scratch buffer (activations, head partials, the
+ * own-KV store of a batch or decode group) in the library's static device
+ * array of LMOP_NOALLOC_SCRATCH_BYTES, one per GPU, held from the first
+ * lmop_create on that GPU until the process ends.  The call makes no device,
+ * pinned-host or event allocation and no memset (it clears what must start at
+ * zero with a kernel); batches are sized to fit the array.  Results equal
+ * lmop_eval_rows bit for bit.  Weights and prefixes must already be loaded
+ * and set (those calls allocate).  Kernel timing (lmop_set_profiling) counts
+ * its launches but times only those for which released events are at hand.
+ * Every call on one GPU, from any ctx, shares that GPU's array: calls that
+ * overlap on one GPU (two host threads, two ctxs) race and must be
+ * serialised by the caller.  LMOP_ERR_OOM (with the sizes in
+ * lmop_last_error) if the scratch of a batch holding the longest row, or the
+ * type's tables, exceed the array; otherwise as lmop_eval_rows. */
+#define LMOP_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
+lmop_status lmop_eval_rows_noalloc(lmop_ctx* ctx, const lmop_prefix* prefix,
+                                   const lmop_prefix* const* row_prefix, const int32_t* tokens,
+                                   const int64_t* offsets, int32_t n_rows, const lmop_type* type,
+                                   lmop_result* out, const lmop_eval_opts* opts);
+
 /* A caller-supplied workspace.  The paper's serving setup caps the GPU
  * memory the LM may take (Appendix "vLLM Config", gpu_memory_utilization)
  * and runs on a 16 GB GPU (Sec. 3.2 Setup); a caller that owns the device

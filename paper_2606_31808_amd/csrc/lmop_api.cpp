@@ -30,7 +30,9 @@ namespace {
 constexpr int kDefaultBatchTokens = 16384;
 // a library-allocated own-KV store above this size is released after each call
 constexpr size_t kKeepOwnKvBytes = size_t(1) << 30;
-
+// Scratch of lmop_eval_rows_noalloc: a static device array, one per GPU the
+// library runs on, held until the process ends
+constexpr size_t kNoAllocScratchBytes = size_t(256) << 20;
 constexpr int kMaxBatchRows = 2048;
 // own-KV bytes of one integer-decode group (also at most half the free memory)
 constexpr size_t kDecodeGroupBytes = size_t(24) << 30;
@@ -41,6 +43,11 @@ constexpr int kMaxBatchBudget = 1 << 21;
 
 int round_up(int x, int m) { return (x + m - 1) / m * m; }
 int64_t round_up64(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// The scratch of lmop_eval_rows_noalloc.  In host code this name is not a
+// device address: each ctx looks up the array's address on its own device
+// once (bind_static_scratch) and passes that address to the kernels.
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
 
 struct LayerW {
   float* attn_norm = nullptr;
@@ -134,6 +141,8 @@ struct lmop_ctx {
   // the current call allocates nothing: no device memory, no pinned host
   // memory, no events
   bool no_alloc = false;
+  // device address of the static no-allocation array on this ctx's device
+  void* static_scratch = nullptr;
 
   std::set<lmop_prefix*> prefixes;
 
@@ -1214,6 +1223,28 @@ const char* lmop_status_string(lmop_status s) {
 
 static thread_local std::string g_create_error;
 
+// Device address of the static scratch array on each device, looked up once
+// per device with that device current.
+static std::mutex g_scratch_mu;
+static std::map<int, void*> g_scratch_ptr;
+
+static lmop_status bind_static_scratch(lmop_ctx* c) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  auto it = g_scratch_ptr.find(c->device);
+  if (it == g_scratch_ptr.end()) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || ptr == nullptr) {
+      (void)hipGetLastError();
+      return fail(c, LMOP_ERR_DEVICE, "hipGetSymbolAddress of the scratch array failed: %s",
+                  hipGetErrorString(e));
+    }
+    it = g_scratch_ptr.emplace(c->device, ptr).first;
+  }
+  c->static_scratch = it->second;
+  return LMOP_OK;
+}
+
 lmop_status lmop_create(const lmop_config* cfg, int32_t device, void* hip_stream, lmop_ctx** out) {
   g_create_error.clear();
   if (!out) return LMOP_ERR_INVALID_ARG;
@@ -1263,6 +1294,8 @@ lmop_status lmop_create(const lmop_config* cfg, int32_t device, void* hip_stream
       return bail(fail(cp, LMOP_ERR_DEVICE, "hipStreamCreate failed"));
     c->own_stream = true;
   }
+  st = bind_static_scratch(cp);
+  if (st != LMOP_OK) return bail(st);
   // the staging slots' events exist before any call, so that a
   // no-allocation call creates none
   for (auto& stg : c->stage)
@@ -2186,6 +2219,19 @@ lmop_status lmop_eval_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
                            lmop_result* out, const lmop_eval_opts* opts) {
   LMOP_TRY(enter(ctx));
   return with_scratch(ctx, ctx->user_ws_bytes > 0, ctx->user_ws, ctx->user_ws_bytes, false, [&] {
+    return eval_rows_impl(ctx, prefix, row_prefix, tokens, offsets, n_rows, type, out, opts);
+  });
+}
+
+lmop_status lmop_eval_rows_noalloc(lmop_ctx* ctx, const lmop_prefix* prefix,
+                                   const lmop_prefix* const* row_prefix, const int32_t* tokens,
+                                   const int64_t* offsets, int32_t n_rows, const lmop_type* type,
+                                   lmop_result* out, const lmop_eval_opts* opts) {
+  LMOP_TRY(enter(ctx));
+  if (!ctx->host_only && !ctx->static_scratch)
+    return fail(ctx, LMOP_ERR_STATE, "the static scratch array is not bound on device %d",
+                ctx->device);
+  return with_scratch(ctx, true, (char*)ctx->static_scratch, kNoAllocScratchBytes, true, [&] {
     return eval_rows_impl(ctx, prefix, row_prefix, tokens, offsets, n_rows, type, out, opts);
   });
 }

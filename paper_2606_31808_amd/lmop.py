@@ -29,8 +29,10 @@ EXPORTED = (
     "lmop_create", "lmop_destroy", "lmop_last_error", "lmop_status_string", "lmop_load_weights",
     "lmop_set_prefix", "lmop_set_prefixes", "lmop_release_prefix", "lmop_prefix_length", "lmop_eval_rows",
     "lmop_dedup_rows", "lmop_set_profiling", "lmop_get_kernel_stats", "lmop_set_workspace",
-    "lmop_get_memory",
+    "lmop_get_memory", "lmop_eval_rows_noalloc",
 )
+# size of the static device array lmop_eval_rows_noalloc carves its scratch from
+LMOP_NOALLOC_SCRATCH_BYTES = 256 << 20
 
 
 class lmop_config(C.Structure):
@@ -119,6 +121,9 @@ def _load():
         "lmop_eval_rows": (st, [vp, vp, C.POINTER(vp), C.POINTER(C.c_int32),
                                 C.POINTER(C.c_int64), i32, C.POINTER(lmop_type), vp,
                                 C.POINTER(lmop_eval_opts)]),
+        "lmop_eval_rows_noalloc": (st, [vp, vp, C.POINTER(vp), C.POINTER(C.c_int32),
+                                        C.POINTER(C.c_int64), i32, C.POINTER(lmop_type), vp,
+                                        C.POINTER(lmop_eval_opts)]),
         "lmop_set_workspace": (st, [vp, vp, C.c_size_t]),
         "lmop_get_memory": (st, [vp, C.POINTER(lmop_memory_stats)]),
         "lmop_dedup_rows": (st, [C.POINTER(C.c_int32), C.POINTER(C.c_int64), i32,
@@ -249,11 +254,12 @@ def lmop_prefix_length(prefix) -> int:
 def lmop_eval_rows(ctx, tokens, offsets, kind: int, allowed: Sequence[int], eos: int = -1,
                    max_tokens: int = 1, prefix=None, row_prefix=None, flags: int = 0,
                    max_batch_tokens: int = 0, debug_logits: bool = False, vocab: int = 0,
-                   limit: int = 0, limit_value: int = 1, row_mask=None):
+                   limit: int = 0, limit_value: int = 1, row_mask=None, no_alloc: bool = False):
     """Returns a structured numpy array of lmop_result (value, logprob, logprob_full,
     n_tokens, tokens) and, with debug_logits, fp32 logits [n_rows][steps][vocab].
     For LMOP_AUTOMATON, `allowed` is an object with n_states, edge_offset,
-    edge_token, edge_next and accepting arrays."""
+    edge_token, edge_next and accepting arrays.  no_alloc calls
+    lmop_eval_rows_noalloc (scratch in the library's static array) instead."""
     toks = _i32(tokens)
     offs = _i64(offsets)
     n = len(offs) - 1
@@ -288,8 +294,9 @@ def lmop_eval_rows(ctx, tokens, offsets, kind: int, allowed: Sequence[int], eos:
     if row_prefix is not None:
         rp = (C.c_void_p * max(n, 1))(*[r.value if isinstance(r, C.c_void_p) else r
                                         for r in row_prefix])
-    _check(_lib.lmop_eval_rows(ctx, prefix, rp, _ptr(toks, C.c_int32), _ptr(offs, C.c_int64), n,
-                               C.byref(ty), out.ctypes.data, C.byref(opts)), ctx)
+    fn = _lib.lmop_eval_rows_noalloc if no_alloc else _lib.lmop_eval_rows
+    _check(fn(ctx, prefix, rp, _ptr(toks, C.c_int32), _ptr(offs, C.c_int64), n, C.byref(ty),
+              out.ctypes.data, C.byref(opts)), ctx)
     del keep
     return out, dbg
 
@@ -309,6 +316,11 @@ def lmop_dedup_rows(tokens, offsets, keys=None):
     if st != LMOP_OK:
         raise LmopError(st, "invalid CSR arguments")
     return rep, int(nu.value)
+
+
+def lmop_eval_rows_noalloc(ctx, tokens, offsets, kind: int, allowed, **kw):
+    """lmop_eval_rows_noalloc: lmop_eval_rows with no device allocation."""
+    return lmop_eval_rows(ctx, tokens, offsets, kind, allowed, no_alloc=True, **kw)
 
 
 def lmop_set_workspace(ctx, ptr: int, nbytes: int) -> None:
@@ -382,11 +394,11 @@ class Context:
 
     def eval_rows(self, tokens, offsets, kind, allowed, eos=-1, max_tokens=1, prefix=None,
                   row_prefix=None, no_dedup=False, max_batch_tokens=0, debug_logits=False,
-                  head_restricted=False, limit=0, limit_value=1, row_mask=None):
+                  head_restricted=False, limit=0, limit_value=1, row_mask=None, no_alloc=False):
         flags = (LMOP_NO_DEDUP if no_dedup else 0) | (LMOP_HEAD_RESTRICTED if head_restricted else 0)
         return lmop_eval_rows(self.ctx, tokens, offsets, kind, allowed, eos, max_tokens, prefix,
                               row_prefix, flags, max_batch_tokens, debug_logits, self.vocab,
-                              limit, limit_value, row_mask)
+                              limit, limit_value, row_mask, no_alloc)
 
     def set_workspace(self, ptr: int, nbytes: int):
         lmop_set_workspace(self.ctx, ptr, nbytes)

@@ -329,3 +329,13 @@ def test_workspace_validation_and_plan(tiny_w):
     ctx.set_workspace(0, 0)
     mem = ctx.memory()
     assert mem["workspace_bytes"] == 0 and mem["device_bytes"] == 0
+    # the no-allocation entry point validates exactly like lmop_eval_rows
+    _expect(L.LMOP_ERR_UNSUPPORTED, ctx.eval_rows, *args, no_alloc=True)
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.eval_rows, [1, TINY.vocab], [0, 2], L.LMOP_BOOL, [1, 2],
+            no_alloc=True)
+    # a row too long for the static array: 256 MiB / ~6 KB per tiny-model token
+    big = L.Context(TINY, device=-1, max_seq=1 << 17)
+    big.load_weights(tiny_w)
+    msg = _expect(L.LMOP_ERR_OOM, big.eval_rows, np.ones(100000, np.int32), [0, 100000],
+                  L.LMOP_BOOL, [1, 2], no_alloc=True)
+    assert "no-allocation" in msg
