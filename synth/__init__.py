@@ -23,4 +23,5 @@ from .workloads import (  # noqa: F401
     automaton_of_list,
     automaton_of_record,
     KIND_AUTOMATON,
+    parity_rows,
 )

@@ -393,6 +393,18 @@ class Workload:
         return int(self.offsets[-1])
 
 
+def parity_rows(wl: "Workload", n: int, seed: int) -> List[int]:
+    """n row indices of a table for a parity sample: its longest row, its
+    shortest, the first and the last, the rest drawn uniformly (seeded)."""
+    lens = np.diff(wl.offsets)
+    rng = np.random.default_rng(seed)
+    pick = {int(np.argmax(lens)), int(np.argmin(lens)), 0, wl.n_rows - 1}
+    n = min(n, wl.n_rows)
+    while len(pick) < n:
+        pick.add(int(rng.integers(0, wl.n_rows)))
+    return sorted(pick)
+
+
 def _csr(parts):
     lens = np.array([len(p) for p in parts], dtype=np.int64)
     offs = np.zeros(len(parts) + 1, dtype=np.int64)

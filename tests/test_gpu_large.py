@@ -14,7 +14,7 @@ import pytest
 import torch
 
 from oracle import KIND_ENUM, OracleLM
-from synth import SHAPES, make_weights, make_workload
+from synth import SHAPES, make_weights, make_workload, parity_rows
 from tests.parity import assert_automaton, assert_typed, compare
 
 pytestmark = pytest.mark.gpu
@@ -67,7 +67,7 @@ def _check_filter(ctx, orc, wl, pre, sample, label):
     out, dbg = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, prefix=pre,
                              debug_logits=True)
     _same_rows(full, out, sample, label)
-    _log(f"{label}: oracle on {len(sample)} rows")
+    _log(f"{label}: oracle on {len(sample)} rows ({sub.n_suffix_tokens} suffix tokens)")
     ref = orc.eval_workload(sub, keep_logits=True)
     st = compare(ref, out, dbg, label)
     _log(label, st)
@@ -75,12 +75,23 @@ def _check_filter(ctx, orc, wl, pre, sample, label):
 
 
 def _sample(wl, n, seed):
-    lens = np.diff(wl.offsets)
-    rng = np.random.default_rng(seed)
-    pick = {int(np.argmax(lens)), int(np.argmin(lens)), 0, wl.n_rows - 1}
-    while len(pick) < n:
-        pick.add(int(rng.integers(0, wl.n_rows)))
-    return sorted(pick)
+    return parity_rows(wl, n, seed)
+
+
+def _forced(orc, sub, out, ref):
+    """The oracle teacher-forced on the library's tokens, for the rows whose
+    token path left the oracle's after a sub-margin step (None elsewhere)."""
+    R = sub.n_rows
+    div = [r for r in range(R)
+           if list(out["tokens"][r][: out["n_tokens"][r]]) != list(ref["tokens"][r][: ref["n_tokens"][r]])]
+    if not div:
+        return None
+    f = orc.eval_workload(sub, rows=div, keep_logits=True,
+                          forced=[out["tokens"][r][: out["n_tokens"][r]] for r in div])
+    logits = [None] * R
+    for j, r in enumerate(div):
+        logits[r] = f["logits"][j]
+    return {"logits": logits}
 
 
 def test_filter_1b_sampled_rows(L):
@@ -88,7 +99,7 @@ def test_filter_1b_sampled_rows(L):
     orc = OracleLM(w, SHAPES["1b"], dtype=np.float32, cache_dequant=True)
     wl = make_workload("filter_1b")
     pre = ctx.set_prefix(wl.prefix)
-    _check_filter(ctx, orc, wl, pre, _sample(wl, 12, 1), "filter_1b")
+    _check_filter(ctx, orc, wl, pre, _sample(wl, 256, 1), "filter_1b")
     ctx.close()
     del w, orc
     torch.cuda.empty_cache()
@@ -98,7 +109,7 @@ def test_filter_8b_sampled_rows(m8b):
     w, ctx, orc = m8b
     wl = make_workload("filter_8b")
     pre = ctx.set_prefix(wl.prefix)
-    _check_filter(ctx, orc, wl, pre, _sample(wl, 5, 2), "filter_8b")
+    _check_filter(ctx, orc, wl, pre, _sample(wl, 64, 2), "filter_8b")
     ctx.release_prefix(pre)
 
 
@@ -113,7 +124,7 @@ def test_filter_8b_restricted_head(m8b):
                             head_restricted=True)
     assert_typed(full, wl.kind, len(wl.allowed), wl.allowed)
     assert np.all(np.isnan(full["logprob_full"]))
-    sample = _sample(wl, 4, 5)
+    sample = _sample(wl, 16, 5)
     sub = wl.subset(sample)
     out, dbg = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, prefix=pre,
                              debug_logits=True, head_restricted=True)
@@ -135,17 +146,14 @@ def test_options_8b_sampled_rows(m8b, L):
     _log(f"options_8b: full table ({wl.n_rows} rows)")
     full, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.automaton, **kw)
     assert_automaton(full, wl.automaton, wl.eos, wl.max_tokens)
-    sample = _sample(wl, 5, 7)
+    sample = _sample(wl, 16, 7)
     sub = wl.subset(sample)
     out, dbg = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.automaton, debug_logits=True,
                              **kw)
     _same_rows(full, out, sample, "options_8b")
     _log(f"options_8b: oracle on {len(sample)} rows")
     ref = orc.eval_workload(sub, keep_logits=True)
-    forced = orc.eval_workload(sub, keep_logits=True,
-                               forced=[out["tokens"][r][: out["n_tokens"][r]]
-                                       for r in range(len(sample))])
-    st = compare(ref, out, dbg, "options_8b", orc_forced=forced)
+    st = compare(ref, out, dbg, "options_8b", orc_forced=_forced(orc, sub, out, ref))
     _log("options_8b", st)
     ctx.release_prefix(pre)
 
@@ -162,26 +170,30 @@ def test_map_int_8b_dedup_and_sampled_rows(m8b, L):
     rep, n_unique = L.lmop_dedup_rows(wl.tokens, wl.offsets)
     assert 2300 < n_unique < 3000
     assert np.array_equal(full, full[rep])
-    # a sample of distinct suffixes, each with two of its duplicate rows
+    # 64 distinct suffixes (the longest and shortest among them), each with
+    # up to two of its duplicate rows
     rng = np.random.default_rng(3)
-    reps = rng.choice(np.unique(rep), 5, replace=False)
+    reps_all = np.unique(rep)
+    lens = np.diff(wl.offsets)[reps_all]
+    reps = {int(reps_all[np.argmax(lens)]), int(reps_all[np.argmin(lens)]), int(rep[0]),
+            int(rep[-1])}
+    while len(reps) < 64:
+        reps.add(int(rng.choice(reps_all)))
     rows, uniq = [], []
-    for r in reps:
+    for r in sorted(reps):
         dup = np.nonzero(rep == r)[0]
         uniq.append(len(rows))
         rows.extend(dup[:2].tolist())
+    assert len(rows) > len(uniq)  # some suffixes do repeat
     sub = wl.subset(rows)
     out, dbg = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed, eos=wl.eos,
                              max_tokens=wl.max_tokens, prefix=pre, debug_logits=True)
     _same_rows(full, out, rows, "map_int_8b")
     sub_u = wl.subset([rows[j] for j in uniq])
-    _log(f"map_int_8b: oracle on {len(uniq)} rows")
+    _log(f"map_int_8b: oracle on {len(uniq)} distinct rows")
     ref = orc.eval_workload(sub_u, keep_logits=True)
-    forced = None
-    toks = [out["tokens"][j][: out["n_tokens"][j]] for j in uniq]
-    if any(list(t) != list(ref["tokens"][k][: ref["n_tokens"][k]]) for k, t in enumerate(toks)):
-        forced = orc.eval_workload(sub_u, keep_logits=True, forced=toks)
-    st = compare(ref, out[uniq], dbg[uniq], "map_int_8b", orc_forced=forced)
+    st = compare(ref, out[uniq], dbg[uniq], "map_int_8b",
+                 orc_forced=_forced(orc, sub_u, out[uniq], ref))
     _log("map_int_8b", st)
     ctx.release_prefix(pre)
 
@@ -196,7 +208,12 @@ def test_join_8b_sampled_pairs(m8b):
     _log(f"join_8b: full table ({wl.n_rows} pairs)")
     full, _ = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, row_prefix=row_prefix)
     assert_typed(full, wl.kind, 2, wl.allowed)
-    rows = [0, 199, 200 * 57 + 3, 200 * 57 + 150, 200 * 199 + 7, 200 * 199 + 199]
+    # 4 left values (first, last, two seeded) x 16 right values (first, last,
+    # 14 seeded): 64 pairs over 4 child prefixes
+    rng = np.random.default_rng(6)
+    lefts = sorted({0, 199} | set(rng.choice(np.arange(1, 199), 2, replace=False).tolist()))
+    rights = sorted({0, 199} | set(rng.choice(np.arange(1, 199), 14, replace=False).tolist()))
+    rows = [200 * a + b for a in lefts for b in rights]
     sub = wl.subset(rows)
     out, dbg = ctx.eval_rows(sub.tokens, sub.offsets, sub.kind, sub.allowed,
                              row_prefix=[row_prefix[r] for r in rows], debug_logits=True)
@@ -232,7 +249,7 @@ def test_filter_8b_fp8_sampled_rows(L):
     orc = OracleLM(w, shape, dtype=np.float32, cache_dequant=False)
     wl = make_workload("filter_8b")
     pre = ctx.set_prefix(wl.prefix)
-    _check_filter(ctx, orc, wl, pre, _sample(wl, 4, 3), "filter_8b fp8")
+    _check_filter(ctx, orc, wl, pre, _sample(wl, 8, 3), "filter_8b fp8")
     ctx.close()
     del w, orc
     torch.cuda.empty_cache()
@@ -269,6 +286,40 @@ def test_head_tiles_8b_shape(L):
                         allowed, keep_logits=True)
     st = compare(ref, out, dbg, "8B head")
     _log("8B head", st)
+    ctx.close()
+    del w, orc
+    torch.cuda.empty_cache()
+
+
+def test_llmqa_8b_width_past_4096_positions(L):
+    """LLMQA (Sec. 2.3.1: one prompt over a whole data subset) at the 8B
+    width with 2 layers: one 256 + 8,192-token prompt, so RoPE angles,
+    own-KV slots and attention walks run past position 4,096, against the
+    fp32 oracle (the multi-token option decoded under its trie)."""
+    import dataclasses
+    shape = dataclasses.replace(SHAPES["8b"], n_layers=2)
+    w = make_weights(shape, seed=1234, device="cuda", n_layers=2)
+    torch.cuda.synchronize()
+    ctx = L.Context(shape, device=0, stream=torch.cuda.current_stream().cuda_stream,
+                    max_seq=9216)
+    ctx.load_weights(w)
+    wl = make_workload("qa_8b")
+    assert len(wl.prefix) + wl.n_suffix_tokens > 8192
+    pre = ctx.set_prefix(wl.prefix)
+    kw = dict(eos=wl.eos, max_tokens=wl.max_tokens, prefix=pre, debug_logits=True)
+    _log("llmqa 8B-width: eval")
+    out, dbg = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.automaton, **kw)
+    assert_automaton(out, wl.automaton, wl.eos, wl.max_tokens)
+    # a batch budget below the prompt's length gives the same bits
+    o1, d1 = ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.automaton, max_batch_tokens=1000,
+                           **kw)
+    assert o1.tobytes() == out.tobytes() and np.array_equal(d1, dbg, equal_nan=True)
+    _log("llmqa 8B-width: oracle")
+    orc = OracleLM(w, shape, dtype=np.float32)
+    ref = orc.eval_workload(wl, keep_logits=True)
+    st = compare(ref, out, dbg, "llmqa 8B width", orc_forced=_forced(orc, wl, out, ref))
+    _log("llmqa 8B width", st)
+    ctx.release_prefix(pre)
     ctx.close()
     del w, orc
     torch.cuda.empty_cache()
