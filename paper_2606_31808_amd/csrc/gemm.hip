@@ -469,26 +469,25 @@ hipError_t launch_epi(hipStream_t s, const GemmArgs& a) {
 // vocabulary operand (M), the final-normalised rows h fp16 [R][K] the token
 // operand (N); both stream through an LDS ring by direct global->LDS loads,
 // 32 features per step in 64-byte LDS rows.  A workgroup holds 16*MI = 128
-// vocabulary entries and 64*F token rows: four waves side by side along the
-// tokens (16*F rows each) share the vocabulary tile.  Two shapes keep two
-// workgroups per CU: F = 4 (256 rows) with a 3-stage ring (72 KB of LDS)
-// and F = 5 (320 rows) with a 2-stage ring (56 KB); deeper rings that leave
-// one workgroup per CU ran about twice as long.  The log-sum-exp partials
-// are per 128-entry vocabulary chunk whatever the tile or the number of
-// rows, so a row's log-probabilities do not depend on how rows are batched.
-// (Loading each wave's token rows straight into registers instead was
-// measured ~35% slower: those loads, not LDS, bounded the head.)
-template <int MI_, int F_, int NS_>
+// vocabulary entries and NW*16*F token rows: NW waves side by side along the
+// tokens (16*F rows each) share the vocabulary tile.  Every shape keeps two
+// workgroups per CU (a ring of at most 80 KB): rings deeper than that, which
+// leave one workgroup per CU, ran about twice as long.  The log-sum-exp
+// partials are per 128-entry vocabulary chunk whatever the tile or the
+// number of rows, so a row's log-probabilities do not depend on how rows are
+// batched.  (Loading each wave's token rows straight into registers instead
+// was measured ~35% slower: those loads, not LDS, bounded the head.)
+template <int MI_, int F_, int NW_, int NS_>
 struct HeadCfg {
-  static constexpr int MI = MI_, F = F_;
-  static constexpr int BK = 32, NW = 4, NS = NS_;
+  static constexpr int MI = MI_, F = F_, NW = NW_, NS = NS_;
+  static constexpr int BK = 32;
   static constexpr int BM = 16 * MI, BN = NW * 16 * F;
   static constexpr int A_BYTES = BM * 64, T_BYTES = BN * 64;
   static constexpr int STAGE = A_BYTES + T_BYTES;
   static constexpr int LDS = NS * STAGE;
   static_assert(NS >= 2 && LDS <= 160 * 1024, "LDS of one CU");
   static constexpr int OCC = LDS <= 80 * 1024 ? 2 : 1;  // workgroups per CU
-  // 16 rows per instruction; surplus waves repeat the last vocabulary block
+  // the vocabulary tile's 16-row blocks, dealt to the waves round-robin
   static constexpr int A_LOADS = (MI + NW - 1) / NW;
   static constexpr int T_LOADS = F;  // a wave's own token blocks
   static_assert((NS - 2) * (A_LOADS + T_LOADS) <= 31, "loads in flight fit the run-time wait");
@@ -499,9 +498,10 @@ struct HeadCfg {
 // distinct 16-byte bank groups of a 128-byte window
 LMOP_DEVICE int swz64(int row) { return (row >> 1) & 3; }
 
-template <int MI, int F, int NS_>
-__global__ __launch_bounds__(256, (HeadCfg<MI, F, NS_>::OCC)) void head_kernel(const GemmArgs p) {
-  using C = HeadCfg<MI, F, NS_>;
+template <int MI, int F, int NW_, int NS_>
+__global__ __launch_bounds__(64 * NW_, (HeadCfg<MI, F, NW_, NS_>::OCC)) void head_kernel(
+    const GemmArgs p) {
+  using C = HeadCfg<MI, F, NW_, NS_>;
   constexpr int BK = C::BK, BM = C::BM, BN = C::BN, NW = C::NW, NS = C::NS;
   constexpr int A_BYTES = C::A_BYTES, STAGE = C::STAGE;
   constexpr int A_LOADS = C::A_LOADS, T_LOADS = C::T_LOADS;
@@ -532,24 +532,26 @@ __global__ __launch_bounds__(256, (HeadCfg<MI, F, NS_>::OCC)) void head_kernel(c
   const f16* H = (const f16*)p.bh;
 
   // one instruction fills 16 rows x 64 bytes: lane L writes row L/4, chunk
-  // L%4, and reads the swizzled source chunk for it.  A wave loads only its
-  // 16-row blocks that hold a token row (the rest of its LDS rows are stale
-  // and feed only results that are never stored), so the number of loads it
-  // has in flight per K step is its own constant.
+  // L%4, and reads the swizzled source chunk for it.  A wave loads its share
+  // of the vocabulary blocks and only its own 16-row token blocks that hold
+  // a token row (the rest of its LDS rows are stale and feed only results
+  // that are never stored), so the number of loads it has in flight per K
+  // step is its own constant.
   const int rr = lane >> 2, pc = lane & 3;
   int tb = (p.N - w0 + 15) / 16;
   tb = tb < 0 ? 0 : (tb > T_LOADS ? T_LOADS : tb);
   // wave-uniform, so a skipped load is a scalar branch, never an issued
   // instruction with no active lane
   const int t_blocks = __builtin_amdgcn_readfirstlane(tb);
-  const int my_loads = A_LOADS + t_blocks;
+  const int a_blocks = (MI - wave + NW - 1) / NW;  // q = wave + NW*i < MI
+  const int my_loads = a_blocks + t_blocks;
   auto issue = [&](int st, int kt) {
     char* sA = smem + st * STAGE;
     char* sT = sA + A_BYTES;
 #pragma unroll
     for (int i = 0; i < A_LOADS; ++i) {
-      int q = wave + NW * i;
-      if (q >= MI) q = MI - 1;
+      const int q = wave + NW * i;
+      if (q >= MI) break;
       const int r = q * 16 + rr;
       int gm = m0 + r;
       gm = gm < p.M ? gm : p.M - 1;
@@ -642,23 +644,24 @@ __global__ __launch_bounds__(256, (HeadCfg<MI, F, NS_>::OCC)) void head_kernel(c
     }
 }
 
-template <int MI, int F, int NS>
+template <int MI, int F, int NW, int NS>
 hipError_t launch_head(hipStream_t s, const GemmArgs& a) {
-  using C = HeadCfg<MI, F, NS>;
+  using C = HeadCfg<MI, F, NW, NS>;
   const int tiles = ((a.M + C::BM - 1) / C::BM) * ((a.N + C::BN - 1) / C::BN);
   if (tiles == 0) return hipSuccess;
   static const hipError_t attr = hipFuncSetAttribute(
-      (const void*)head_kernel<MI, F, NS>, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+      (const void*)head_kernel<MI, F, NW, NS>, hipFuncAttributeMaxDynamicSharedMemorySize,
+      C::LDS);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((head_kernel<MI, F, NS>), dim3(tiles), dim3(256), C::LDS, s, a);
+  hipLaunchKernelGGL((head_kernel<MI, F, NW, NS>), dim3(tiles), dim3(64 * NW), C::LDS, s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_gemm_f16(hipStream_t s, const GemmArgs& a, int epi) {
-  using H256 = HeadCfg<8, 4, 3>;  // 256-token tile, 3-stage ring
-  using H320 = HeadCfg<8, 5, 2>;  // 320-token tile, 2-stage ring
+  using H256 = HeadCfg<8, 4, 4, 3>;  // 256-token tile, 3-stage ring
+  using H320 = HeadCfg<8, 5, 4, 2>;  // 320-token tile, 2-stage ring
   static_assert(H256::BM == kHeadVocabChunk && H320::BM == kHeadVocabChunk,
                 "partials per vocabulary chunk");
   static_assert(H256::OCC == 2 && H320::OCC == 2, "two workgroups per CU");
@@ -669,8 +672,8 @@ hipError_t launch_gemm_f16(hipStream_t s, const GemmArgs& a, int epi) {
   // tile runs about 10% longer than a full 256-token one.  Each logit's
   // accumulation order is the same in both, so the choice never changes a bit.
   const int t256 = (a.N + H256::BN - 1) / H256::BN, t320 = (a.N + H320::BN - 1) / H320::BN;
-  if (10 * t256 > 11 * t320) return launch_head<8, 5, 2>(s, a);
-  return launch_head<8, 4, 3>(s, a);
+  if (10 * t256 > 11 * t320) return launch_head<8, 5, 4, 2>(s, a);
+  return launch_head<8, 4, 4, 3>(s, a);
 }
 
 hipError_t launch_gemm_w4(hipStream_t s, const GemmArgs& a, int epi) {
