@@ -205,6 +205,25 @@ __global__ void repack_fp8_kernel(RepackSrc src, const int32_t* __restrict__ col
   *(uint4*)(qpack + item * 16) = make_uint4(w[0], w[1], w[2], w[3]);
 }
 
+// --------------------------------------------------------------- head weight tiling
+// One thread per 16-byte chunk of the tiled head weight: tile t, K step s,
+// row r, chunk c holds features 32s + 8c .. +7 of vocabulary row 128t + r
+// (zero past the vocabulary).
+__global__ __launch_bounds__(256) void repack_head_kernel(const f16* __restrict__ src, int V,
+                                                          int d, f16* __restrict__ dst,
+                                                          size_t n_chunks) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_chunks) return;
+  const int c = (int)(i & 3);
+  const int r = (int)((i >> 2) % kHeadTileRows);
+  const size_t ts = (i >> 2) / kHeadTileRows;  // tile * (d / 32) + step
+  const int ks = (int)(ts % (size_t)(d / 32));
+  const int v = (int)(ts / (size_t)(d / 32)) * kHeadTileRows + r;
+  f16x8 x = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (v < V) x = *(const f16x8*)(src + (size_t)v * d + ks * 32 + c * 8);
+  *(f16x8*)(dst + i * 8) = x;
+}
+
 // --------------------------------------------------------------- restricted head
 // Logits of the allowed tokens only: one workgroup per row, one wave per
 // allowed token at a time; each lane sums 8-feature runs with a stride of
@@ -219,10 +238,10 @@ __global__ __launch_bounds__(256) void head_restricted_kernel(const f16* __restr
   const f16* h = hn + (size_t)r * d;
   for (int i = wave; i < n_sel; i += 4) {
     const int tok = allowed[i];
-    const f16* w = W + (size_t)tok * d;
     float acc = 0.f;
     for (int k = lane * 8; k < d; k += 512) {
-      const f16x8 a = *(const f16x8*)(h + k), b = *(const f16x8*)(w + k);
+      const f16x8 a = *(const f16x8*)(h + k);
+      const f16x8 b = *(const f16x8*)(W + head_tiled_index(tok, k, d));
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc += (float)a[j] * (float)b[j];
     }
@@ -384,6 +403,16 @@ hipError_t launch_repack_w8(hipStream_t s, const RepackSrc& src, const int32_t* 
   const int blocks = (int)((total + 255) / 256);
   hipLaunchKernelGGL(repack_fp8_kernel, dim3(blocks), dim3(256), 0, s, src, colsrc, dst.np, kg_n,
                      (uint8_t*)dst.qpack, dst.sscale);
+  return hipGetLastError();
+}
+
+hipError_t launch_repack_head(hipStream_t s, const half_bits* src, int V, int d, half_bits* dst) {
+  if (d % 32 != 0) return hipErrorInvalidValue;
+  const size_t vp = (size_t)(V + kHeadTileRows - 1) / kHeadTileRows * kHeadTileRows;
+  const size_t n_chunks = vp * d / 8;
+  const size_t blocks = (n_chunks + 255) / 256;
+  hipLaunchKernelGGL(repack_head_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
+                     (const f16*)src, V, d, (f16*)dst, n_chunks);
   return hipGetLastError();
 }
 

@@ -160,33 +160,45 @@ __global__ __launch_bounds__((64 * NW_), Occ<MI>::value) void gemm_kernel(const 
   const int PFW = KT < BM / NW ? KT : BM / NW;
 
   // ---- global -> LDS issue of one K step into stage st; every wave issues
-  // exactly C::LOADS instructions, which the vmcnt waits below rely on
+  // exactly C::LOADS instructions, which the vmcnt waits below rely on.
+  // Each load is a base in scalar registers (moved by kt) plus a per-lane
+  // 32-bit byte offset computed once, and an LDS destination in a scalar
+  // register.
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_ptr_t)smem;
+  uint32_t aoff[C::A_LOADS];
+#pragma unroll
+  for (int i = 0; i < C::A_LOADS; ++i) {
+    int q = wave + NW * i;  // 8 rows per instruction
+    if (q >= BM / 8) q = BM / 8 - 1;  // surplus waves repeat the last rows
+    const int r = q * 8 + (lane >> 3);
+    const int chunk = (lane & 7) ^ swz(r);
+    const int gm = m0 + r < p.M ? r : p.M - 1 - m0;  // row within the tile, clamped
+    aoff[i] = (uint32_t)(gm * p.lda + chunk * 8) * 2u;
+  }
+  const char* abase = (const char*)(A + (size_t)m0 * p.lda);
+  const size_t nb0 = (size_t)(n0 >> 6);
+  // int4 scales: lane group pi = lane / 8 fetches pair pi's 128 bytes
+  const uint32_t soff = (uint32_t)(((lane >> 4) * KG + ((lane >> 3) & 1)) * 128 + (lane & 7) * 16);
   auto issue = [&](int st, int kt) {
-    char* sA = smem + st * C::STAGE;
-    char* sB = sA + C::A_BYTES;
-    char* sS = sB + C::B_BYTES;
+    const uint32_t sA = lds0 + (uint32_t)(st * C::STAGE);
+    const uint32_t sB = sA + C::A_BYTES;
+    const uint32_t sS = sB + C::B_BYTES;
 #pragma unroll
     for (int i = 0; i < C::A_LOADS; ++i) {
-      int q = wave + NW * i;  // 8 rows per instruction
-      if (q >= BM / 8) q = BM / 8 - 1;  // surplus waves repeat the last rows
-      const int r = q * 8 + (lane >> 3);
-      const int chunk = (lane & 7) ^ swz(r);
-      int gm = m0 + r;
-      gm = gm < p.M ? gm : p.M - 1;
-      g2l16(A + (size_t)gm * p.lda + kt * BK + chunk * 8, sA + q * 1024);
+      int q = wave + NW * i;
+      if (q >= BM / 8) q = BM / 8 - 1;
+      g2l16_m0(abase + kt * BK * 2, aoff[i], sA + (uint32_t)q * 1024u);
     }
     if constexpr (INT4) {
-      const size_t nb0 = (size_t)(n0 >> 6);
 #pragma unroll
       for (int i = 0; i < C::B_LOADS; ++i) {  // (64-column block, group) pairs
         const int q = wave + NW * i;
-        const size_t blk = (nb0 + (q >> 1)) * KG + kt * 2 + (q & 1);
-        g2l16((const char*)p.bq + blk * 1024 + lane * 16, sB + q * 1024);
+        const char* b = (const char*)p.bq + ((nb0 + (q >> 1)) * KG + kt * 2 + (q & 1)) * 1024;
+        g2l16_m0(b, (uint32_t)lane * 16u, sB + (uint32_t)q * 1024u);
       }
       {  // scales: 8 pairs x 128 B = one 1 KB instruction, spread over the waves
-        const int pi = lane >> 3;
-        const size_t blk = (nb0 + (pi >> 1)) * KG + kt * 2 + (pi & 1);
-        if ((lane >> 4) == wave) g2l16((const char*)p.bs + blk * 128 + (lane & 7) * 16, sS);
+        const char* b = (const char*)p.bs + (nb0 * KG + kt * 2) * 128;
+        if ((lane >> 4) == wave) g2l16_m0(b, soff, sS);
       }
       if constexpr (EPI == EPI_ADD_F32) {
         // the residual row r of the tile (1 KB: this wave's 256 columns),
@@ -197,18 +209,19 @@ __global__ __launch_bounds__((64 * NW_), Occ<MI>::value) void gemm_kernel(const 
           gm = gm < p.M ? gm : p.M - 1;
           int col = n0 + lane * 4;
           col = col + 4 <= p.n_out ? col : p.n_out - 4;
-          g2l16(p.X + (size_t)gm * p.ldx + col, smem + C::NS * C::STAGE + wave * 1024);
+          g2l16_m0((const char*)(p.X + (size_t)gm * p.ldx), (uint32_t)col * 4u,
+                   lds0 + (uint32_t)(C::NS * C::STAGE + wave * 1024));
         }
       }
     } else if constexpr (WF == WF_FP8) {
       // 1 KB chunks: (64-column block, group) pair q >> 1, half q & 1
-      const size_t nb0 = (size_t)(n0 >> 6);
 #pragma unroll
       for (int i = 0; i < C::B_LOADS; ++i) {
         const int q = wave + NW * i;
         const int pr = q >> 1;
         const size_t blk = (nb0 + (pr >> 1)) * KG + kt * 2 + (pr & 1);
-        g2l16((const char*)p.bq + (blk * 2 + (q & 1)) * 1024 + lane * 16, sB + q * 1024);
+        g2l16_m0((const char*)p.bq + (blk * 2 + (q & 1)) * 1024, (uint32_t)lane * 16u,
+                 sB + (uint32_t)q * 1024u);
       }
     }
   };
@@ -465,8 +478,9 @@ hipError_t launch_epi(hipStream_t s, const GemmArgs& a) {
 }
 
 // ---------------------------------------------------------------- LM head
-// z = W_lm . h for R token rows: the head weight W_lm fp16 [V][K] is the
-// vocabulary operand (M), the final-normalised rows h fp16 [R][K] the token
+// z = W_lm . h for R token rows: the head weight W_lm fp16 (tiled, see
+// kHeadTileRows) is the vocabulary operand (M), the final-normalised rows h
+// fp16 [R][K] the token
 // operand (N); both stream through an LDS ring by direct global->LDS loads,
 // 32 features per step in 64-byte LDS rows.  A workgroup holds 16*MI = 128
 // vocabulary entries and NW*16*F token rows: NW waves side by side along the
@@ -486,11 +500,14 @@ struct HeadCfg {
   static constexpr int STAGE = A_BYTES + T_BYTES;
   static constexpr int LDS = NS * STAGE;
   static_assert(NS >= 2 && LDS <= 160 * 1024, "LDS of one CU");
+  static_assert(BM == kHeadTileRows, "a workgroup's vocabulary rows are one weight tile");
   static constexpr int OCC = LDS <= 80 * 1024 ? 2 : 1;  // workgroups per CU
   // the vocabulary tile's 16-row blocks, dealt to the waves round-robin
   static constexpr int A_LOADS = (MI + NW - 1) / NW;
   static constexpr int T_LOADS = F;  // a wave's own token blocks
-  static_assert((NS - 2) * (A_LOADS + T_LOADS) <= 31, "loads in flight fit the run-time wait");
+  // every wave issues the same loads every step, so the waits are constants
+  static constexpr int LOADS = A_LOADS + T_LOADS;
+  static_assert((NS - 2) * LOADS <= 63, "loads in flight fit the vmcnt counter");
 };
 
 // 16-byte chunk swizzle of a 64-byte LDS row: the 8 lanes a ds_read_b128
@@ -532,40 +549,47 @@ __global__ __launch_bounds__(64 * NW_, (HeadCfg<MI, F, NW_, NS_>::OCC)) void hea
   const f16* H = (const f16*)p.bh;
 
   // one instruction fills 16 rows x 64 bytes: lane L writes row L/4, chunk
-  // L%4, and reads the swizzled source chunk for it.  A wave loads its share
-  // of the vocabulary blocks and only its own 16-row token blocks that hold
-  // a token row (the rest of its LDS rows are stale and feed only results
-  // that are never stored), so the number of loads it has in flight per K
-  // step is its own constant.
+  // L%4, and reads the swizzled source chunk for it.  Every wave issues the
+  // same number of loads each step, so its waits are compile-time counts (a
+  // count known only at run time costs a branch tree per step): rows past
+  // the table's end load its last row again (L2 hits; they feed only results
+  // that are never stored), and vocabulary blocks beyond MI, when the waves
+  // do not divide them evenly, repeat the last block.
+  // Each load is a block base in scalar registers (at step kt) plus a
+  // per-lane 32-bit byte offset computed once, and an LDS destination in a
+  // scalar register.  The head weight is tiled (kHeadTileRows rows x 32
+  // features, 8 KB per vocabulary tile and K step, rows past the vocabulary
+  // zero), so a vocabulary block of one step is 1 KB of contiguous memory.
   const int rr = lane >> 2, pc = lane & 3;
-  int tb = (p.N - w0 + 15) / 16;
-  tb = tb < 0 ? 0 : (tb > T_LOADS ? T_LOADS : tb);
-  // wave-uniform, so a skipped load is a scalar branch, never an issued
-  // instruction with no active lane
-  const int t_blocks = __builtin_amdgcn_readfirstlane(tb);
-  const int a_blocks = (MI - wave + NW - 1) / NW;  // q = wave + NW*i < MI
-  const int my_loads = a_blocks + t_blocks;
+  uint32_t aoff[A_LOADS], toff[T_LOADS];
+#pragma unroll
+  for (int i = 0; i < A_LOADS; ++i) {
+    int q = wave + NW * i;
+    if (q >= MI) q = MI - 1;
+    const int r = q * 16 + rr;
+    aoff[i] = (uint32_t)(r * 64 + (pc ^ swz64(r)) * 16);
+  }
+#pragma unroll
+  for (int i = 0; i < T_LOADS; ++i) {
+    const int r = (wave * T_LOADS + i) * 16 + rr;  // the wave's own rows
+    const int gn = n0 + r < p.N ? r : p.N - 1 - n0;
+    toff[i] = (uint32_t)(gn * p.ldb + (pc ^ swz64(r)) * 8) * 2u;
+  }
+  const char* wbase = (const char*)(W + (size_t)mt * KT * (kHeadTileRows * 32));
+  const char* hbase = (const char*)(H + (size_t)n0 * p.ldb);
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_ptr_t)smem;
   auto issue = [&](int st, int kt) {
-    char* sA = smem + st * STAGE;
-    char* sT = sA + A_BYTES;
+    const uint32_t sA = lds0 + (uint32_t)(st * STAGE);
+    const uint32_t sT = sA + A_BYTES;
 #pragma unroll
     for (int i = 0; i < A_LOADS; ++i) {
-      const int q = wave + NW * i;
-      if (q >= MI) break;
-      const int r = q * 16 + rr;
-      int gm = m0 + r;
-      gm = gm < p.M ? gm : p.M - 1;
-      g2l16(W + (size_t)gm * p.lda + kt * BK + (pc ^ swz64(r)) * 8, sA + q * 1024);
+      int q = wave + NW * i;
+      if (q >= MI) q = MI - 1;
+      g2l16_m0(wbase + (size_t)kt * (kHeadTileRows * 64), aoff[i], sA + (uint32_t)q * 1024u);
     }
 #pragma unroll
-    for (int i = 0; i < T_LOADS; ++i) {
-      if (i >= t_blocks) break;
-      const int q = wave * T_LOADS + i;  // the wave's own rows
-      const int r = q * 16 + rr;
-      int gn = n0 + r;
-      gn = gn < p.N ? gn : p.N - 1;
-      g2l16(H + (size_t)gn * p.ldb + kt * BK + (pc ^ swz64(r)) * 8, sT + q * 1024);
-    }
+    for (int i = 0; i < T_LOADS; ++i)
+      g2l16_m0(hbase + kt * BK * 2, toff[i], sT + (uint32_t)(wave * T_LOADS + i) * 1024u);
   };
 
   f32x4 acc[F][MI];
@@ -581,9 +605,11 @@ __global__ __launch_bounds__(64 * NW_, (HeadCfg<MI, F, NW_, NS_>::OCC)) void hea
     if (st < KT) issue(st, st);
   for (int kt = 0; kt < KT; ++kt) {
     // this step's stage is complete once at most the later steps' loads
-    // (up to NS - 2 stages of them) are in flight
-    const int later = KT - 1 - kt < NS - 2 ? KT - 1 - kt : NS - 2;
-    wait_vmcnt_dyn(later * my_loads);
+    // (NS - 2 stages of them) are in flight; near the end, none
+    if (kt + NS - 2 < KT)
+      wait_vmcnt<(NS - 2) * C::LOADS>();
+    else
+      wait_vmcnt<0>();
     barrier();
     if (kt + NS - 1 < KT) issue((kt + NS - 1) % NS, kt + NS - 1);
     if (wave_active) {
@@ -665,8 +691,10 @@ hipError_t launch_gemm_f16(hipStream_t s, const GemmArgs& a, int epi) {
   static_assert(H256::BM == kHeadVocabChunk && H320::BM == kHeadVocabChunk,
                 "partials per vocabulary chunk");
   static_assert(H256::OCC == 2 && H320::OCC == 2, "two workgroups per CU");
-  if (a.K % 32 != 0 || epi != EPI_HEAD || a.ldb % 8 != 0 || a.lda % 8 != 0)
+  if (a.K % 32 != 0 || epi != EPI_HEAD || a.ldb % 8 != 0)
     return hipErrorInvalidValue;
+  // per-lane token-row offsets are 32-bit byte offsets within one tile's rows
+  if ((size_t)512 * a.ldb * 2 >= (size_t(1) << 31)) return hipErrorInvalidValue;
   // A workgroup's time barely depends on how many of its token rows are
   // real, so the tile that needs fewer token tiles wins; a full 320-token
   // tile runs about 10% longer than a full 256-token one.  Each logit's

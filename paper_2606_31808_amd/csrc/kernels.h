@@ -30,7 +30,7 @@ enum Epilogue : int {
   EPI_STORE_F16 = 0,  // C[m][n] = fp16(acc)
   EPI_ADD_F32 = 1,    // X[m][n] += acc (residual stream)
   EPI_SWIGLU = 2,     // fused [gate|up] blocks of 32: C[m][j] = fp16(silu(gate_j) * up_j)
-  EPI_HEAD = 3,       // LM head (A = head weight, B = hidden rows): per token and 128-entry
+  EPI_HEAD = 3,       // LM head (A = tiled head weight, B = hidden rows): per token and 128-entry
                       // vocabulary slice (max, sum exp), allowed-token logits, debug dump
   EPI_QKV = 4         // fused q|k|v: RoPE on q, k; q -> qout, k -> K store, v -> V^T store
 };
@@ -81,6 +81,17 @@ hipError_t launch_gemm_f16(hipStream_t s, const GemmArgs& a, int epi);  // head 
 // the head writes one (max, sum exp) partial per row and chunk of this many
 // vocabulary entries, for any number of rows
 constexpr int kHeadVocabChunk = 128;
+// The LM head weight as the library keeps it: tiles of kHeadTileRows
+// vocabulary rows x 32 features, [ceil(V / 128)][d / 32][128][32] fp16, rows
+// past the vocabulary zero; tile (t, s) is 8 KB of contiguous memory.
+constexpr int kHeadTileRows = 128;
+// element (v, k) of the tiled head weight
+__host__ __device__ inline size_t head_tiled_index(int v, int k, int d) {
+  return (((size_t)(v / kHeadTileRows) * (d / 32) + k / 32) * kHeadTileRows + v % kHeadTileRows) *
+             32 + k % 32;
+}
+// row-major fp16 [V][d] -> tiled (d a multiple of 32)
+hipError_t launch_repack_head(hipStream_t s, const half_bits* src, int V, int d, half_bits* dst);
 
 // Repacks one source matrix's rows into columns of a packed weight.
 // colsrc[j] (device, [np]): (source index << 24) | source row, or -1 (zero column).
@@ -153,8 +164,8 @@ struct HeadPick {
   float pad[3];
 };
 // per row: combine partials -> LSE over V; pick among zsel[:n_allowed]
-// zsel[r][i] = hn[r] . W[allowed[i]] (fp16 rows of width d, fp32 sums) for
-// the n_sel allowed tokens only; with dump, also dump[r][allowed[i]]
+// zsel[r][i] = hn[r] . W[allowed[i]] (W the tiled head weight, fp32 sums)
+// for the n_sel allowed tokens only; with dump, also dump[r][allowed[i]]
 hipError_t launch_head_restricted(hipStream_t s, const half_bits* hn, int R, int d,
                                   const half_bits* W, const int32_t* allowed, int n_sel,
                                   float* zsel, float* dump, int ld_dump);

@@ -1147,7 +1147,7 @@ lmop_status run_head(lmop_ctx* c, int k, int R, const std::vector<const float*>&
   } else {
     {
       GemmArgs ga{};
-      ga.A = c->head;
+      ga.A = c->head;  // tiled
       ga.lda = d;
       ga.M = V;
       ga.N = R;
@@ -1422,8 +1422,27 @@ lmop_status lmop_load_weights(lmop_ctx* ctx, const lmop_weights* w) {
   void* p = nullptr;
   LMOP_TRY(upload(ctx, w->tok_embedding, V * d * 2, od, &p));
   ctx->emb = (uint16_t*)p;
-  LMOP_TRY(upload(ctx, w->lm_head, V * d * 2, od, &p));
-  ctx->head = (uint16_t*)p;
+  {  // the LM head, repacked into its tiles
+    const void* src = w->lm_head;
+    void* staged = nullptr;
+    if (!od) {
+      LMOP_TRY(dev_alloc(ctx, &staged, V * d * 2));
+      HIP_OK(ctx, hipMemcpyAsync(staged, w->lm_head, V * d * 2, hipMemcpyHostToDevice,
+                                 ctx->stream));
+      src = staged;
+    }
+    const size_t vp = (V + kHeadTileRows - 1) / kHeadTileRows * kHeadTileRows;
+    LMOP_TRY(dev_alloc(ctx, &p, vp * d * 2));
+    ctx->weight_allocs.push_back(p);
+    ctx->head = (uint16_t*)p;
+    LMOP_TRY(timed(ctx, "repack_head", 0, 0, [&] {
+      return launch_repack_head(ctx->stream, (const half_bits*)src, (int)V, d, ctx->head);
+    }));
+    if (staged) {
+      HIP_OK(ctx, hipStreamSynchronize(ctx->stream));
+      HIP_OK(ctx, dev_free(ctx, staged));
+    }
+  }
   LMOP_TRY(upload(ctx, w->final_norm, (size_t)d * 4, od, &p));
   ctx->final_norm = (float*)p;
   ctx->layers.resize(cf.n_layers);
