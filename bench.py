@@ -174,7 +174,7 @@ def mfma_summary(root):
                     "4": "W4A16 GEMM, QKV + RoPE (qkv)", "0": "W4A16 GEMM, fp16 store"}.get(epi, epi)
         if "gemm_kernel<" in name:
             return "W8A16 GEMM (FP8 weights)"
-        if "head_kernel" in name:
+        if "head2_kernel" in name or "head_kernel" in name:
             return "LM head GEMM"
         if "attn_kernel" in name:
             return "attention"

@@ -478,59 +478,55 @@ hipError_t launch_epi(hipStream_t s, const GemmArgs& a) {
 }
 
 // ---------------------------------------------------------------- LM head
-// z = W_lm . h for R token rows: the head weight W_lm fp16 (tiled, see
-// kHeadTileRows) is the vocabulary operand (M), the final-normalised rows h
-// fp16 [R][K] the token
-// operand (N); both stream through an LDS ring by direct global->LDS loads,
-// 32 features per step in 64-byte LDS rows.  A workgroup holds 16*MI = 128
-// vocabulary entries and NW*16*F token rows: NW waves side by side along the
-// tokens (16*F rows each) share the vocabulary tile.  Every shape keeps two
-// workgroups per CU (a ring of at most 80 KB): rings deeper than that, which
-// leave one workgroup per CU, ran about twice as long.  The log-sum-exp
-// partials are per 128-entry vocabulary chunk whatever the tile or the
-// number of rows, so a row's log-probabilities do not depend on how rows are
-// batched.  (Loading each wave's token rows straight into registers instead
-// was measured ~35% slower: those loads, not LDS, bounded the head.)
-template <int MI_, int F_, int NW_, int NS_>
-struct HeadCfg {
-  static constexpr int MI = MI_, F = F_, NW = NW_, NS = NS_;
-  static constexpr int BK = 32;
-  static constexpr int BM = 16 * MI, BN = NW * 16 * F;
-  static constexpr int A_BYTES = BM * 64, T_BYTES = BN * 64;
-  static constexpr int STAGE = A_BYTES + T_BYTES;
-  static constexpr int LDS = NS * STAGE;
-  static_assert(NS >= 2 && LDS <= 160 * 1024, "LDS of one CU");
-  static_assert(BM == kHeadTileRows, "a workgroup's vocabulary rows are one weight tile");
-  static constexpr int OCC = LDS <= 80 * 1024 ? 2 : 1;  // workgroups per CU
-  // the vocabulary tile's 16-row blocks, dealt to the waves round-robin
-  static constexpr int A_LOADS = (MI + NW - 1) / NW;
-  static constexpr int T_LOADS = F;  // a wave's own token blocks
-  // every wave issues the same loads every step, so the waits are constants
-  static constexpr int LOADS = A_LOADS + T_LOADS;
-  static_assert((NS - 2) * LOADS <= 63, "loads in flight fit the vmcnt counter");
-};
-
 // 16-byte chunk swizzle of a 64-byte LDS row: the 8 lanes a ds_read_b128
 // serves together (rows c .. c+7 of a fragment, one chunk) fall on 8
 // distinct 16-byte bank groups of a 128-byte window
 LMOP_DEVICE int swz64(int row) { return (row >> 1) & 3; }
 
-template <int MI, int F, int NW_, int NS_>
-__global__ __launch_bounds__(64 * NW_, (HeadCfg<MI, F, NW_, NS_>::OCC)) void head_kernel(
-    const GemmArgs p) {
-  using C = HeadCfg<MI, F, NW_, NS_>;
-  constexpr int BK = C::BK, BM = C::BM, BN = C::BN, NW = C::NW, NS = C::NS;
+// ---------------------------------------------------------------- LM head
+// z = W_lm . h for R token rows: the head weight W_lm fp16 (tiled, see
+// kHeadTileRows) is the vocabulary operand (M), the final-normalised rows h
+// fp16 [R][K] the token operand (N); both stream through an LDS ring by
+// direct global->LDS loads, 32 features per step in 64-byte LDS rows.  A
+// workgroup of 8 waves holds two vocabulary tiles (256 rows) and 64*F token
+// rows: wave w computes vocabulary tile w / 4 of the pair for token-row
+// group w % 4 (16*F rows).  The two tiles share the token rows in LDS, so
+// token rows cross from L2 once per 256 vocabulary rows, and one workgroup
+// per CU affords a ring of NS stages (four: three steps of loads in flight).
+// Per token and 128-entry vocabulary chunk the epilogue writes (max, sum
+// exp) and the allowed tokens' logits; the chunking never depends on the
+// tile or the number of rows, so a row's log-probabilities do not depend on
+// how rows are batched.  (One 128-row vocabulary tile per 4-wave workgroup,
+// two workgroups per CU, ran 12-14% longer; token rows loaded straight into
+// registers ran ~35% longer than through the ring.)
+template <int F_, int NS_>
+struct Head2Cfg {
+  static constexpr int F = F_, NS = NS_, NW = 8, BK = 32, MI = 8;
+  static constexpr int BM = 2 * kHeadTileRows, BN = 4 * 16 * F;
+  static constexpr int A_BYTES = BM * 64, T_BYTES = BN * 64;
+  static constexpr int STAGE = A_BYTES + T_BYTES;
+  static constexpr int LDS = NS * STAGE;
+  static_assert(NS >= 2 && LDS <= 160 * 1024, "LDS of one CU");
+  static constexpr int T_BLOCKS = BN / 16;
+  static constexpr int T_MAX = (T_BLOCKS + NW - 1) / NW;  // token blocks of the first waves
+  static constexpr int T_FULL = T_BLOCKS % NW == 0 ? NW : T_BLOCKS % NW;  // waves with T_MAX
+  static constexpr int LOADS_HI = 2 + T_MAX, LOADS_LO = 2 + T_MAX - 1;
+  static_assert((NS - 2) * LOADS_HI <= 63, "loads in flight fit the vmcnt counter");
+};
+
+template <int F, int NS_>
+__global__ __launch_bounds__(512, 1) void head2_kernel(const GemmArgs p) {
+  using C = Head2Cfg<F, NS_>;
+  constexpr int BK = C::BK, BM = C::BM, BN = C::BN, NS = C::NS, MI = C::MI;
   constexpr int A_BYTES = C::A_BYTES, STAGE = C::STAGE;
-  constexpr int A_LOADS = C::A_LOADS, T_LOADS = C::T_LOADS;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, c = lane & 15;
+  const int half = wave >> 2, grp_t = wave & 3;
 
-  // XCD-aware tile order as in gemm_kernel: the token tiles of one
-  // vocabulary tile run side by side on one XCD, so the head weight streams
-  // from HBM about once
+  // XCD-aware tile order as in gemm_kernel
   const int ntm = (p.M + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
   const int total = ntm * ntn;
   const int b = blockIdx.x;
@@ -542,54 +538,49 @@ __global__ __launch_bounds__(64 * NW_, (HeadCfg<MI, F, NW_, NS_>::OCC)) void hea
   const int gsz = (ntm - grp * GM) < GM ? (ntm - grp * GM) : GM;
   const int mt = grp * GM + within % gsz;
   const int nt = within / gsz;
-  const int m0 = mt * BM, n0 = nt * BN;
-  const int w0 = n0 + wave * 16 * F;  // this wave's first token row
+  const int n0 = nt * BN;
+  const int w0 = n0 + grp_t * 16 * F;  // this wave's first token row
   const int KT = p.K / BK;
+  const int n_tiles = (p.M + kHeadTileRows - 1) / kHeadTileRows;
   const f16* W = (const f16*)p.A;
   const f16* H = (const f16*)p.bh;
 
-  // one instruction fills 16 rows x 64 bytes: lane L writes row L/4, chunk
-  // L%4, and reads the swizzled source chunk for it.  Every wave issues the
-  // same number of loads each step, so its waits are compile-time counts (a
-  // count known only at run time costs a branch tree per step): rows past
-  // the table's end load its last row again (L2 hits; they feed only results
-  // that are never stored), and vocabulary blocks beyond MI, when the waves
-  // do not divide them evenly, repeat the last block.
-  // Each load is a block base in scalar registers (at step kt) plus a
-  // per-lane 32-bit byte offset computed once, and an LDS destination in a
-  // scalar register.  The head weight is tiled (kHeadTileRows rows x 32
-  // features, 8 KB per vocabulary tile and K step, rows past the vocabulary
-  // zero), so a vocabulary block of one step is 1 KB of contiguous memory.
+  // loads: wave w fetches 16-row block w of both vocabulary tiles (the
+  // second clamped to the last tile of the weight) and token blocks w, w+8,
+  // ...; the first T_FULL waves have one token block more, so the waits
+  // take one of two compile-time counts
   const int rr = lane >> 2, pc = lane & 3;
-  uint32_t aoff[A_LOADS], toff[T_LOADS];
+  const int ra = wave * 16 + rr;
+  const uint32_t aoff = (uint32_t)(ra * 64 + (pc ^ swz64(ra)) * 16);
+  const char* wbase[2];
 #pragma unroll
-  for (int i = 0; i < A_LOADS; ++i) {
-    int q = wave + NW * i;
-    if (q >= MI) q = MI - 1;
-    const int r = q * 16 + rr;
-    aoff[i] = (uint32_t)(r * 64 + (pc ^ swz64(r)) * 16);
+  for (int h = 0; h < 2; ++h) {
+    const int t = 2 * mt + h < n_tiles ? 2 * mt + h : n_tiles - 1;
+    wbase[h] = (const char*)(W + (size_t)t * KT * (kHeadTileRows * 32));
   }
+  uint32_t toff[C::T_MAX];
 #pragma unroll
-  for (int i = 0; i < T_LOADS; ++i) {
-    const int r = (wave * T_LOADS + i) * 16 + rr;  // the wave's own rows
+  for (int i = 0; i < C::T_MAX; ++i) {
+    int q = wave + 8 * i;
+    if (q >= C::T_BLOCKS) q = C::T_BLOCKS - 1;
+    const int r = q * 16 + rr;
     const int gn = n0 + r < p.N ? r : p.N - 1 - n0;
     toff[i] = (uint32_t)(gn * p.ldb + (pc ^ swz64(r)) * 8) * 2u;
   }
-  const char* wbase = (const char*)(W + (size_t)mt * KT * (kHeadTileRows * 32));
   const char* hbase = (const char*)(H + (size_t)n0 * p.ldb);
   const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_ptr_t)smem;
+  const bool t_hi = wave < C::T_FULL;
   auto issue = [&](int st, int kt) {
     const uint32_t sA = lds0 + (uint32_t)(st * STAGE);
     const uint32_t sT = sA + A_BYTES;
 #pragma unroll
-    for (int i = 0; i < A_LOADS; ++i) {
-      int q = wave + NW * i;
-      if (q >= MI) q = MI - 1;
-      g2l16_m0(wbase + (size_t)kt * (kHeadTileRows * 64), aoff[i], sA + (uint32_t)q * 1024u);
-    }
+    for (int h = 0; h < 2; ++h)
+      g2l16_m0(wbase[h] + (size_t)kt * (kHeadTileRows * 64), aoff,
+               sA + (uint32_t)(h * kHeadTileRows * 64 + wave * 1024));
 #pragma unroll
-    for (int i = 0; i < T_LOADS; ++i)
-      g2l16_m0(hbase + kt * BK * 2, toff[i], sT + (uint32_t)(wave * T_LOADS + i) * 1024u);
+    for (int i = 0; i < C::T_MAX; ++i)
+      if (i < C::T_MAX - 1 || t_hi)
+        g2l16_m0(hbase + kt * BK * 2, toff[i], sT + (uint32_t)(wave + 8 * i) * 1024u);
   };
 
   f32x4 acc[F][MI];
@@ -599,22 +590,25 @@ __global__ __launch_bounds__(64 * NW_, (HeadCfg<MI, F, NW_, NS_>::OCC)) void hea
     for (int i = 0; i < MI; ++i) acc[f][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const bool wave_active = w0 < p.N;
-  // NS - 1 stages in flight ahead of the one being read
 #pragma unroll
   for (int st = 0; st < NS - 1; ++st)
     if (st < KT) issue(st, st);
   for (int kt = 0; kt < KT; ++kt) {
     // this step's stage is complete once at most the later steps' loads
     // (NS - 2 stages of them) are in flight; near the end, none
-    if (kt + NS - 2 < KT)
-      wait_vmcnt<(NS - 2) * C::LOADS>();
-    else
+    if (kt + NS - 2 < KT) {
+      if (t_hi)
+        wait_vmcnt<(NS - 2) * C::LOADS_HI>();
+      else
+        wait_vmcnt<(NS - 2) * C::LOADS_LO>();
+    } else {
       wait_vmcnt<0>();
+    }
     barrier();
     if (kt + NS - 1 < KT) issue((kt + NS - 1) % NS, kt + NS - 1);
     if (wave_active) {
-      const char* sA = smem + (kt % NS) * STAGE;
-      const char* sT = sA + A_BYTES;
+      const char* sA = smem + (kt % NS) * STAGE + half * (kHeadTileRows * 64);
+      const char* sT = smem + (kt % NS) * STAGE + A_BYTES;
       f16x8 a[MI], t[F];
 #pragma unroll
       for (int i = 0; i < MI; ++i) {
@@ -623,7 +617,7 @@ __global__ __launch_bounds__(64 * NW_, (HeadCfg<MI, F, NW_, NS_>::OCC)) void hea
       }
 #pragma unroll
       for (int f = 0; f < F; ++f) {
-        const int r = wave * 16 * F + 16 * f + c;
+        const int r = grp_t * 16 * F + 16 * f + c;
         t[f] = *(const f16x8*)(sT + r * 64 + ((g ^ swz64(r)) * 16));
       }
 #pragma unroll
@@ -633,12 +627,12 @@ __global__ __launch_bounds__(64 * NW_, (HeadCfg<MI, F, NW_, NS_>::OCC)) void hea
     }
   }
 
-  // acc[f][i][r] = z[vocabulary m0 + 16i + c][token w0 + 16f + 4g + r].
-  // Per token and this workgroup's vocabulary chunk mt: (max, sum exp(z -
-  // max)), plus the logits of the allowed tokens
-  const int mrow = m0 + c;
+  // acc[f][i][r] = z[vocabulary m0 + 16i + c][token w0 + 16f + 4g + r]
+  const int chunk = 2 * mt + half;
+  const int n_chunks = n_tiles;
+  if (chunk >= n_chunks) return;  // a pair's second tile past the vocabulary
+  const int mrow = chunk * kHeadTileRows + c;
   const int ncol = w0 + 4 * g;
-  const int n_chunks = ntm;
 #pragma unroll
   for (int f = 0; f < F; ++f)
 #pragma unroll
@@ -666,31 +660,28 @@ __global__ __launch_bounds__(64 * NW_, (HeadCfg<MI, F, NW_, NS_>::OCC)) void hea
       }
 #pragma unroll
       for (int o = 1; o < 16; o <<= 1) sm += shfl_xor(sm, o);
-      if (c == 0 && n < p.N) p.part[(size_t)n * n_chunks + mt] = make_float2(mx, sm);
+      if (c == 0 && n < p.N) p.part[(size_t)n * n_chunks + chunk] = make_float2(mx, sm);
     }
 }
 
-template <int MI, int F, int NW, int NS>
-hipError_t launch_head(hipStream_t s, const GemmArgs& a) {
-  using C = HeadCfg<MI, F, NW, NS>;
+template <int F, int NS>
+hipError_t launch_head2(hipStream_t s, const GemmArgs& a) {
+  using C = Head2Cfg<F, NS>;
   const int tiles = ((a.M + C::BM - 1) / C::BM) * ((a.N + C::BN - 1) / C::BN);
   if (tiles == 0) return hipSuccess;
   static const hipError_t attr = hipFuncSetAttribute(
-      (const void*)head_kernel<MI, F, NW, NS>, hipFuncAttributeMaxDynamicSharedMemorySize,
-      C::LDS);
+      (const void*)head2_kernel<F, NS>, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((head_kernel<MI, F, NW, NS>), dim3(tiles), dim3(64 * NW), C::LDS, s, a);
+  hipLaunchKernelGGL((head2_kernel<F, NS>), dim3(tiles), dim3(512), C::LDS, s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_gemm_f16(hipStream_t s, const GemmArgs& a, int epi) {
-  using H256 = HeadCfg<8, 4, 4, 3>;  // 256-token tile, 3-stage ring
-  using H320 = HeadCfg<8, 5, 4, 2>;  // 320-token tile, 2-stage ring
-  static_assert(H256::BM == kHeadVocabChunk && H320::BM == kHeadVocabChunk,
-                "partials per vocabulary chunk");
-  static_assert(H256::OCC == 2 && H320::OCC == 2, "two workgroups per CU");
+  using H256 = Head2Cfg<4, 4>;  // 256-token tile
+  using H320 = Head2Cfg<5, 4>;  // 320-token tile
+  static_assert(kHeadTileRows == kHeadVocabChunk, "partials per vocabulary chunk");
   if (a.K % 32 != 0 || epi != EPI_HEAD || a.ldb % 8 != 0)
     return hipErrorInvalidValue;
   // per-lane token-row offsets are 32-bit byte offsets within one tile's rows
@@ -700,8 +691,8 @@ hipError_t launch_gemm_f16(hipStream_t s, const GemmArgs& a, int epi) {
   // tile runs about 10% longer than a full 256-token one.  Each logit's
   // accumulation order is the same in both, so the choice never changes a bit.
   const int t256 = (a.N + H256::BN - 1) / H256::BN, t320 = (a.N + H320::BN - 1) / H320::BN;
-  if (10 * t256 > 11 * t320) return launch_head<8, 5, 4, 2>(s, a);
-  return launch_head<8, 4, 4, 3>(s, a);
+  if (10 * t256 > 11 * t320) return launch_head2<5, 4>(s, a);
+  return launch_head2<4, 4>(s, a);
 }
 
 hipError_t launch_gemm_w4(hipStream_t s, const GemmArgs& a, int epi) {
