@@ -245,6 +245,90 @@ def head_roofline(stats):
             "bytes_per_launch": s["bytes"] / s["timed"]}
 
 
+DECODE_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_gemm_map_int_8b_traffic.json")
+
+
+def decode_roofline(stats):
+    """Integer/automaton decode steps: one forward over every live row of a
+    decode group per step, so each decode-step GEMM streams all its weights
+    for the few thousand rows still decoding.  The bound is whichever roof
+    the launch's algorithmic intensity (FLOP per algorithmic byte: the
+    weights at 0.5625 B per int4 parameter with its scale, plus activations
+    in and out) puts it under: MFMA above the ridge (2.5 PFLOP/s over
+    8 TB/s = 312.5 FLOP/B), HBM below it.  Both rates are reported, with the
+    counter-measured bytes per launch when the committed PMC summary was
+    taken on the current GEMM source."""
+    names = [n for n in stats if n.startswith("decode_gemm_")]
+    ms = sum(stats[n]["ms"] for n in names)
+    timed = sum(stats[n]["timed"] for n in names)
+    if ms <= 0 or timed == 0:
+        return None
+    by = sum(stats[n]["bytes"] for n in names)
+    fl = sum(stats[n]["flops"] for n in names)
+    gbs = by / (ms * 1e-3) / 1e9
+    tfl = fl / (ms * 1e-3) / 1e12
+    ridge = PEAK_F16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    mfma = fl / by > ridge
+    traffic = None
+    try:
+        with open(DECODE_TRAFFIC_FILE) as f:
+            t = json.load(f)
+        if t.get("gemm_src_sha256_16") == _src_hash():
+            traffic = t["bytes_per_launch"]
+    except (OSError, ValueError):
+        pass
+    ach, peak, unit = (tfl, PEAK_F16_TFLOPS, "TFLOP/s") if mfma else (gbs, PEAK_HBM_GBS, "GB/s")
+    return {"kernel": "decode-step W4A16 GEMMs (qkv, o, gate/up, down)",
+            "bound": "mfma" if mfma else "hbm", "achieved": ach, "peak": peak, "unit": unit,
+            "frac": ach / peak, "flop_per_byte": fl / by, "tflops": tfl, "gbs": gbs,
+            "launches": sum(stats[n]["launches"] for n in names),
+            "timed_launches": timed, "avg_launch_ms": ms / timed,
+            "algorithmic_bytes_per_launch": by / timed, "traffic": traffic}
+
+
+def decode_pmc_summary(root):
+    """HBM bytes per decode-step GEMM launch of map_int_8b from two rocprofv3
+    --pmc runs of one step (FETCH_SIZE under root/pmc_dec_fetch, WRITE_SIZE
+    under root/pmc_dec_write, bench lines in their .log) and the plain-copy
+    calibration runs (root/pmc_copy_fetch, root/pmc_copy_write).  The decode
+    steps of one decode group follow all of its prefill batches, so with one
+    group (the default memory budget) the decode launches are the last
+    W4A16 GEMM dispatches of the step."""
+    import csv
+    import glob
+
+    def rows(d):
+        out = []
+        for fn in glob.glob(os.path.join(root, d, "*counter_collection.csv")):
+            out.extend(csv.DictReader(open(fn)))
+        return out
+
+    def dec_mean(d, counter):
+        line = _bench_line(os.path.join(root, d + ".log"))
+        n = line["decode_roofline"]["launches"]
+        sel = _timed_gemm_rows([r for r in rows(d) if r["Counter_Name"] == counter], n)
+        assert len(sel) == n, (d, len(sel), n)
+        return sum(float(r["Counter_Value"]) for r in sel) / n, n, line
+
+    def copy_mean(d, counter):
+        v = [float(r["Counter_Value"]) for r in rows(d)
+             if r["Counter_Name"] == counter and "copy" in r["Kernel_Name"].lower()]
+        return sum(v) / len(v)
+
+    f_kib, n, line = dec_mean("pmc_dec_fetch", "FETCH_SIZE")
+    w_kib, _, _ = dec_mean("pmc_dec_write", "WRITE_SIZE")
+    kf = COPY_BYTES / (copy_mean("pmc_copy_fetch", "FETCH_SIZE") * 1024.0)
+    kw = COPY_BYTES / (copy_mean("pmc_copy_write", "WRITE_SIZE") * 1024.0)
+    out = {"gemm_src_sha256_16": _src_hash(), "workload": "map_int_8b", "launches": n,
+           "fetch_bytes_per_launch": f_kib * 1024.0 * kf, "write_bytes_per_launch": w_kib * 1024.0 * kw,
+           "bytes_per_launch": f_kib * 1024.0 * kf + w_kib * 1024.0 * kw,
+           "algorithmic_bytes_per_launch": line["decode_roofline"]["algorithmic_bytes_per_launch"],
+           "avg_launch_ms_under_counters": line["decode_roofline"]["avg_launch_ms"]}
+    with open(DECODE_TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
+
+
 def pass_rooflines(stats):
     """The other passes of a step: attention against MFMA (its FLOPs are the
     visible query-key pairs the host counts), RMSNorm against HBM (fp32 in,
@@ -383,11 +467,16 @@ def main():
                     help="summarise the rocprofv3 --pmc runs under DIR and exit")
     ap.add_argument("--mfma-summary", metavar="DIR",
                     help="summarise an SQ_VALU_MFMA_BUSY_CYCLES pass under DIR/pmc_mfma and exit")
+    ap.add_argument("--decode-pmc-summary", metavar="DIR",
+                    help="summarise the decode-step GEMM counter runs under DIR and exit")
     ap.add_argument("--trace-summary", metavar="DIR",
                     help="summarise the rocprofv3 --kernel-trace run under DIR and exit")
     args = ap.parse_args()
     if args.pmc_summary:
         pmc_summary(args.pmc_summary)
+        return
+    if args.decode_pmc_summary:
+        decode_pmc_summary(args.decode_pmc_summary)
         return
     if args.trace_summary:
         trace_summary(args.trace_summary)
@@ -534,6 +623,7 @@ def main():
                         "second_ms": cascade.get("second_ms")}} if args.cascade else {}),
         "roofline": gemm_roofline(stats),
         "head_roofline": head_roofline(stats),
+        **({"decode_roofline": dec} if (dec := decode_roofline(stats)) else {}),
         "pass_rooflines": pass_rooflines(stats),
         "load_weights_s": t_load, "set_prefix_ms": t_prefix * 1e3,
         # device memory: what the library held at most (weights, prefix KV,

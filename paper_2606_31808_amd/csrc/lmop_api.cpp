@@ -716,9 +716,10 @@ hipError_t launch_gemm_packed(const lmop_ctx* c, GemmArgs& ga, const PackedW& W,
 }
 
 // timing names and weight bytes per parameter of the loaded format
-const char* gemm_name(const lmop_ctx* c, const char* proj) {
+const char* gemm_name(const lmop_ctx* c, const char* proj, bool decode = false) {
   static thread_local std::string n;
-  n = std::string(c->wfmt == LMOP_W_FP8_E4M3 ? "gemm_w8a16_" : "gemm_w4a16_") + proj;
+  n = std::string(decode ? "decode_" : "") +
+      (c->wfmt == LMOP_W_FP8_E4M3 ? "gemm_w8a16_" : "gemm_w4a16_") + proj;
   return n.c_str();
 }
 double weight_bytes(const lmop_ctx* c, double n, double k) {
@@ -942,6 +943,9 @@ struct Batch {
   int n_last = 0;
   // keys visible to the batch's query tokens, summed (for the attention FLOP count)
   double visible_keys = 0;
+  // a decode step (one token per live row): its launches are timed under
+  // "decode_"-prefixed names, apart from the prefill passes
+  bool decode = false;
 };
 
 // One pass of all layers over the T tokens whose ids/positions/slots and row
@@ -973,7 +977,7 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
   for (int l = 0; l < cf.n_layers; ++l) {
     const LayerW& L = c->layers[l];
     const double nbytes_norm = (double)T * d * 6;
-    LMOP_TRY(timed(c, "rmsnorm", 0, nbytes_norm, [&] {
+    LMOP_TRY(timed(c, b.decode ? "decode_rmsnorm" : "rmsnorm", 0, nbytes_norm, [&] {
       return launch_rmsnorm(c->stream, x, d, nullptr, T, L.attn_norm, d, cf.rms_eps, h, d);
     }));
     uint16_t* kc = b.own_kv + l * kv_layer;
@@ -998,7 +1002,7 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
       const double flops = 2.0 * T * L.qkv.n * L.qkv.k;
       const double bytes = (double)T * L.qkv.k * 2 + weight_bytes(c, L.qkv.n, L.qkv.k) +
                            (double)T * L.qkv.n * 2;
-      LMOP_TRY(timed(c, gemm_name(c, "qkv"), flops, bytes,
+      LMOP_TRY(timed(c, gemm_name(c, "qkv", b.decode), flops, bytes,
                      [&] { return launch_gemm_packed(c, ga, L.qkv, EPI_QKV); }));
     }
     AttnArgs aa{};
@@ -1017,7 +1021,8 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
     aa.hd = hd;
     // per visible (query token, key) pair and query head: q.k and p.v, 2 FLOP per dim each
     const double attn_flops = 4.0 * hd * cf.n_heads * b.visible_keys;
-    LMOP_TRY(timed(c, "attention", attn_flops, 0, [&] { return launch_attention(c->stream, aa); }));
+    LMOP_TRY(timed(c, b.decode ? "decode_attention" : "attention", attn_flops, 0,
+                   [&] { return launch_attention(c->stream, aa); }));
     // in the last layer only the selected tokens continue (their K/V are written above)
     int M = T;
     float* xr = x;
@@ -1048,11 +1053,11 @@ lmop_status forward(lmop_ctx* c, const Batch& b) {
       const double flops = 2.0 * M * W.n * W.k;
       const double bytes = (double)M * W.k * 2 + weight_bytes(c, W.n, W.k) +
                            (double)M * W.n * (epi == EPI_ADD_F32 ? 8 : 2);
-      return timed(c, gemm_name(c, name), flops, bytes,
+      return timed(c, gemm_name(c, name, b.decode), flops, bytes,
                    [&] { return launch_gemm_packed(c, ga, W, epi); });
     };
     LMOP_TRY(gemm2("o", ar, c->nq_dim, L.o, EPI_ADD_F32, nullptr, 0, d));
-    LMOP_TRY(timed(c, "rmsnorm", 0, (double)M * d * 6, [&] {
+    LMOP_TRY(timed(c, b.decode ? "decode_rmsnorm" : "rmsnorm", 0, (double)M * d * 6, [&] {
       return launch_rmsnorm(c->stream, xr, d, nullptr, M, L.mlp_norm, d, cf.rms_eps, h, d);
     }));
     LMOP_TRY(gemm2("gateup", h, d, L.gu, EPI_SWIGLU, act, c->f64, c->f64));
@@ -2147,6 +2152,7 @@ static lmop_status eval_rows_impl(lmop_ctx* ctx, const lmop_prefix* prefix,
       sb.n_work = (int)sw.size();
       sb.own_kv = own_kv;
       sb.own_cap = group_cap[gi];
+      sb.decode = true;
       for (int q = 0; q < nl; ++q) sb.visible_keys += sp[q] + 1;  // position + 1 keys
       LMOP_TRY(forward(ctx, sb));
       float* x;
