@@ -28,9 +28,13 @@
  *    comes from a caller-supplied workspace instead once lmop_set_workspace
  *    has given one.
  *  - LMOP_ERR_DEVICE is sticky: after a HIP error the ctx refuses further
- *    work and must be destroyed.
+ *    work and must be destroyed.  For tests of that rule, the environment
+ *    variable LMOP_INJECT_LAUNCH_FAILURE=<kernel name>:<n>, read by
+ *    lmop_create, makes the n-th launch of that kernel on the ctx fail as a
+ *    HIP launch error would, without launching it.
  *  - All calls are synchronous with respect to the host: when they return,
- *    their device work on the ctx stream has completed.
+ *    their device work on the ctx stream has completed, also when they
+ *    return an error.
  */
 #ifndef LMOP_H
 #define LMOP_H

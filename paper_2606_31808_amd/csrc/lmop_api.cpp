@@ -11,6 +11,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstdint>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <memory>
@@ -103,6 +104,10 @@ struct lmop_ctx {
   bool own_stream = false;
   std::string err;
   bool dead = false;
+  // testing hook (LMOP_INJECT_LAUNCH_FAILURE=<name>:<n>): the n-th launch
+  // timed under <name> fails as a HIP launch error would, without launching
+  std::string inject_name;
+  long inject_at = 0, inject_count = 0;
   bool loaded = false;
   uint64_t generation = 0;
   int64_t next_prefix_id = 1;
@@ -376,6 +381,8 @@ lmop_status timed(lmop_ctx* c, const char* name, double flops, double bytes, F&&
       a = b = nullptr;
     }
   }
+  if (!c->inject_name.empty() && c->inject_name == name && ++c->inject_count == c->inject_at)
+    return fail(c, LMOP_ERR_DEVICE, "launch of %s failed: injected failure", name);
   hipError_t e = launch();
   if (e != hipSuccess) return fail(c, LMOP_ERR_DEVICE, "launch of %s failed: %s", name,
                                    hipGetErrorString(e));
@@ -1200,6 +1207,9 @@ lmop_status with_scratch(lmop_ctx* ctx, bool carve, char* base, size_t bytes, bo
   ctx->carve_size = carve ? bytes : 0;
   ctx->no_alloc = no_alloc;
   const lmop_status st = f();
+  // on any error, let the work already queued finish before returning, so
+  // that none of it still reads or writes the caller's buffers or workspace
+  if (st != LMOP_OK && !ctx->host_only && ctx->stream) (void)hipStreamSynchronize(ctx->stream);
   ctx->carving = false;
   ctx->carve_base = nullptr;
   ctx->carve_size = 0;
@@ -1276,6 +1286,13 @@ lmop_status lmop_create(const lmop_config* cfg, int32_t device, void* hip_stream
   c->qkv_n = c->nq_dim + 2 * c->nkv_dim;
   c->f64 = round_up(cf.d_ff, 64);
   c->device = device;
+  if (const char* inj = getenv("LMOP_INJECT_LAUNCH_FAILURE")) {
+    const char* colon = strrchr(inj, ':');
+    if (colon && colon != inj) {
+      c->inject_name.assign(inj, colon - inj);
+      c->inject_at = atol(colon + 1);
+    }
+  }
   if (device < 0) {
     c->host_only = true;
     *out = c.release();

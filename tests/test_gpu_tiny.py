@@ -976,3 +976,39 @@ def test_tiny_workspace(tiny, L):
     assert again.tobytes() == want_b.tobytes()
     ctx.release_prefix(pre)
     ctx.close()
+
+
+@pytest.mark.gpu
+def test_tiny_device_error_is_sticky(tiny, L, monkeypatch):
+    """A HIP launch failure in the middle of a forward pass (forced from the
+    host: the library's launch-failure hook fails the 3rd attention launch
+    without launching it) returns LMOP_ERR_DEVICE naming the kernel; every
+    later call on that ctx is refused with the same status and the first
+    cause; a fresh ctx on the same device still gives the reference bits."""
+    w, orc, ref_ctx = tiny
+    wl = make_workload("filter_tiny")
+    pre_ref = ref_ctx.set_prefix(wl.prefix)
+    want = ref_ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, prefix=pre_ref)
+    ref_ctx.release_prefix(pre_ref)
+    monkeypatch.setenv("LMOP_INJECT_LAUNCH_FAILURE", "attention:3")
+    ctx = L.Context(TINY, device=0, stream=torch.cuda.current_stream().cuda_stream)
+    monkeypatch.delenv("LMOP_INJECT_LAUNCH_FAILURE")
+    ctx.load_weights(w)
+    pre = ctx.set_prefix(wl.prefix)  # two attention launches (two layers)
+    with pytest.raises(L.LmopError) as ei:
+        ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, prefix=pre)
+    assert ei.value.status == L.LMOP_ERR_DEVICE
+    assert "attention" in str(ei.value) and "injected" in str(ei.value)
+    for call in (lambda: ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, prefix=pre),
+                 lambda: ctx.set_prefix(wl.prefix)):
+        with pytest.raises(L.LmopError) as ei2:
+            call()
+        assert ei2.value.status == L.LMOP_ERR_DEVICE
+        assert "earlier error" in str(ei2.value) and "injected" in str(ei2.value)
+    ctx.close()
+    fresh = L.Context(TINY, device=0, stream=torch.cuda.current_stream().cuda_stream)
+    fresh.load_weights(w)
+    pre = fresh.set_prefix(wl.prefix)
+    got = fresh.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, prefix=pre)
+    assert got[0].tobytes() == want[0].tobytes()
+    fresh.close()
