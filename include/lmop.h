@@ -291,6 +291,36 @@ lmop_status lmop_eval_rows_noalloc(lmop_ctx* ctx, const lmop_prefix* prefix,
  * pointer, or one of p, bytes zero without the other. */
 lmop_status lmop_set_workspace(lmop_ctx* ctx, void* dev_ptr, size_t bytes);
 
+/* What lmop_eval_rows would do with the same arguments, without doing it:
+ * validation, deduplication and the batch / decode-group plan run, no device
+ * work is queued and nothing is allocated (a host-only ctx plans as well).
+ * For sizing a workspace against a memory cap (Sec. 3.2, Appendix "vLLM
+ * Config").  The plan is the one the call would use now: against the
+ * workspace if one is set, else against library-allocated scratch.
+ * opts->debug_logits only counts as NULL or not (a non-NULL pointer plans
+ * the scratch of the logit dump; nothing is written to it).  Errors as
+ * lmop_eval_rows (LMOP_ERR_OOM if the workspace cannot hold one row);
+ * INVALID_ARG if plan is NULL. */
+typedef struct {
+  int32_t unique_rows;      /* rows evaluated: distinct (prefix, suffix) rows the row mask keeps */
+  int32_t batches;          /* forward passes of the rows' first step                     */
+  int32_t batch_tokens;     /* token budget of a pass in this plan                        */
+  int32_t max_batch_tokens; /* suffix tokens of the largest pass                          */
+  int32_t decode_groups;    /* groups of passes decoded together (integer and automaton
+                               types: every further step is one pass per group)           */
+  int32_t pad_;
+  uint64_t scratch_bytes;   /* device scratch of the plan, own-KV store included          */
+  uint64_t own_kv_bytes;    /* of which the own-KV store (keys and values of the rows'
+                               own tokens)                                                 */
+  uint64_t min_workspace_bytes; /* the smallest workspace that runs the call (with the
+                                   smallest batches and decode groups); one byte less is
+                                   LMOP_ERR_OOM                                           */
+} lmop_eval_plan;
+lmop_status lmop_plan_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
+                           const lmop_prefix* const* row_prefix, const int32_t* tokens,
+                           const int64_t* offsets, int32_t n_rows, const lmop_type* type,
+                           const lmop_eval_opts* opts, lmop_eval_plan* plan);
+
 /* Device memory accounting of a ctx (for the 16 GB budget of Sec. 3.2). */
 typedef struct {
   uint64_t device_bytes;    /* device memory the library holds now (weights, prefix KV

@@ -108,6 +108,8 @@ struct lmop_ctx {
   // timed under <name> fails as a HIP launch error would, without launching
   std::string inject_name;
   long inject_at = 0, inject_count = 0;
+  // set by lmop_plan_rows: eval_rows_impl stops after planning and fills it
+  lmop_eval_plan* plan_out = nullptr;
   bool loaded = false;
   uint64_t generation = 0;
   int64_t next_prefix_id = 1;
@@ -1773,7 +1775,8 @@ static lmop_status eval_rows_impl(lmop_ctx* ctx, const lmop_prefix* prefix,
   if (n_rows < 0) return fail(ctx, LMOP_ERR_INVALID_ARG, "n_rows < 0");
   LMOP_TRY(check_type(ctx, type));
   if (n_rows == 0) return LMOP_OK;
-  if (!offsets || !out) return fail(ctx, LMOP_ERR_INVALID_ARG, "NULL offsets or out");
+  if (!offsets || (!out && !ctx->plan_out))
+    return fail(ctx, LMOP_ERR_INVALID_ARG, "NULL offsets or out");
   if (offsets[0] != 0) return fail(ctx, LMOP_ERR_INVALID_ARG, "offsets[0] != 0");
   for (int r = 0; r < n_rows; ++r)
     if (offsets[r + 1] < offsets[r])
@@ -1952,6 +1955,40 @@ static lmop_status eval_rows_impl(lmop_ctx* ctx, const lmop_prefix* prefix,
         group_bytes = std::max<size_t>(std::min(group_bytes, free_b / 2), 1);
     }
     plan(budget, group_bytes);
+  }
+  if (ctx->plan_out) {
+    lmop_eval_plan& pl = *ctx->plan_out;
+    pl.unique_rows = (int32_t)uniq.size();
+    pl.batches = (int32_t)sch.batches.size();
+    pl.batch_tokens = sch.budget;
+    for (auto& bt : sch.batches) {
+      int t = 0;
+      for (size_t u = bt.first; u < bt.second; ++u) t += row_len[u];
+      pl.max_batch_tokens = std::max(pl.max_batch_tokens, t);
+    }
+    pl.decode_groups = (int32_t)sch.group_cap.size();
+    pl.scratch_bytes = scratch_total(ctx, sch.need);
+    pl.own_kv_bytes = sch.need.own_kv;
+    // the smallest workspace whose carved plan fits: a bisection over sizes
+    // (a larger workspace never fits fewer rows), to the byte
+    const bool was_carving = ctx->carving;
+    const size_t was_size = ctx->carve_size;
+    ctx->carving = true;
+    auto fits = [&](size_t W) {
+      ctx->carve_size = W;
+      return fit_budget(budget, [&](int b) { return plan(b, 0); }) != 0;
+    };
+    size_t hi = std::max<size_t>((size_t)pl.scratch_bytes, (size_t)1 << 20);
+    while (!fits(hi) && hi < ((size_t)1 << 50)) hi *= 2;
+    size_t lo = 0;
+    while (hi - lo > 1) {
+      const size_t mid = lo + (hi - lo) / 2;
+      (fits(mid) ? hi : lo) = mid;
+    }
+    pl.min_workspace_bytes = hi;
+    ctx->carving = was_carving;
+    ctx->carve_size = was_size;
+    return LMOP_OK;
   }
   if (ctx->host_only)
     return fail(ctx, LMOP_ERR_UNSUPPORTED,
@@ -2276,6 +2313,23 @@ lmop_status lmop_eval_rows_noalloc(lmop_ctx* ctx, const lmop_prefix* prefix,
   return with_scratch(ctx, true, (char*)ctx->static_scratch, kNoAllocScratchBytes, true, [&] {
     return eval_rows_impl(ctx, prefix, row_prefix, tokens, offsets, n_rows, type, out, opts);
   });
+}
+
+lmop_status lmop_plan_rows(lmop_ctx* ctx, const lmop_prefix* prefix,
+                           const lmop_prefix* const* row_prefix, const int32_t* tokens,
+                           const int64_t* offsets, int32_t n_rows, const lmop_type* type,
+                           const lmop_eval_opts* opts, lmop_eval_plan* plan) {
+  LMOP_TRY(enter(ctx));
+  if (!plan) return fail(ctx, LMOP_ERR_INVALID_ARG, "plan is NULL");
+  *plan = lmop_eval_plan{};
+  ctx->plan_out = plan;
+  const lmop_status st =
+      with_scratch(ctx, ctx->user_ws_bytes > 0, ctx->user_ws, ctx->user_ws_bytes, false, [&] {
+        return eval_rows_impl(ctx, prefix, row_prefix, tokens, offsets, n_rows, type, nullptr,
+                              opts);
+      });
+  ctx->plan_out = nullptr;
+  return st;
 }
 
 lmop_status lmop_set_workspace(lmop_ctx* ctx, void* dev_ptr, size_t bytes) {

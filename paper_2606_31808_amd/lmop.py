@@ -29,7 +29,7 @@ EXPORTED = (
     "lmop_create", "lmop_destroy", "lmop_last_error", "lmop_status_string", "lmop_load_weights",
     "lmop_set_prefix", "lmop_set_prefixes", "lmop_release_prefix", "lmop_prefix_length", "lmop_eval_rows",
     "lmop_dedup_rows", "lmop_set_profiling", "lmop_get_kernel_stats", "lmop_set_workspace",
-    "lmop_get_memory", "lmop_eval_rows_noalloc",
+    "lmop_get_memory", "lmop_eval_rows_noalloc", "lmop_plan_rows",
 )
 # size of the static device array lmop_eval_rows_noalloc carves its scratch from
 LMOP_NOALLOC_SCRATCH_BYTES = 256 << 20
@@ -87,6 +87,13 @@ class lmop_memory_stats(C.Structure):
                 ("workspace_bytes", C.c_uint64), ("workspace_peak", C.c_uint64)]
 
 
+class lmop_eval_plan(C.Structure):
+    _fields_ = [("unique_rows", C.c_int32), ("batches", C.c_int32), ("batch_tokens", C.c_int32),
+                ("max_batch_tokens", C.c_int32), ("decode_groups", C.c_int32),
+                ("pad_", C.c_int32), ("scratch_bytes", C.c_uint64), ("own_kv_bytes", C.c_uint64),
+                ("min_workspace_bytes", C.c_uint64)]
+
+
 class lmop_kernel_stat(C.Structure):
     _fields_ = [("name", C.c_char * 48), ("launches", C.c_int64), ("timed_launches", C.c_int64),
                 ("total_ms", C.c_double), ("flops", C.c_double), ("bytes", C.c_double)]
@@ -124,6 +131,9 @@ def _load():
         "lmop_eval_rows_noalloc": (st, [vp, vp, C.POINTER(vp), C.POINTER(C.c_int32),
                                         C.POINTER(C.c_int64), i32, C.POINTER(lmop_type), vp,
                                         C.POINTER(lmop_eval_opts)]),
+        "lmop_plan_rows": (st, [vp, vp, C.POINTER(vp), C.POINTER(C.c_int32),
+                                C.POINTER(C.c_int64), i32, C.POINTER(lmop_type),
+                                C.POINTER(lmop_eval_opts), C.POINTER(lmop_eval_plan)]),
         "lmop_set_workspace": (st, [vp, vp, C.c_size_t]),
         "lmop_get_memory": (st, [vp, C.POINTER(lmop_memory_stats)]),
         "lmop_dedup_rows": (st, [C.POINTER(C.c_int32), C.POINTER(C.c_int64), i32,
@@ -260,6 +270,51 @@ def lmop_eval_rows(ctx, tokens, offsets, kind: int, allowed: Sequence[int], eos:
     For LMOP_AUTOMATON, `allowed` is an object with n_states, edge_offset,
     edge_token, edge_next and accepting arrays.  no_alloc calls
     lmop_eval_rows_noalloc (scratch in the library's static array) instead."""
+    toks, offs, n, ty, opts, rp, keep = _call_args(tokens, offsets, kind, allowed, eos, max_tokens,
+                                                   row_prefix, flags, max_batch_tokens, limit,
+                                                   limit_value, row_mask)
+    out = np.zeros(max(n, 0), dtype=RESULT_DTYPE)
+    steps = max_tokens if kind in (LMOP_INT, LMOP_AUTOMATON) else 1
+    dbg = None
+    if debug_logits:
+        if vocab <= 0:
+            raise ValueError("debug_logits needs vocab")
+        dbg = np.empty((n, steps, vocab), dtype=np.float32)
+        opts.debug_logits = _ptr(dbg, C.c_float)
+    fn = _lib.lmop_eval_rows_noalloc if no_alloc else _lib.lmop_eval_rows
+    _check(fn(ctx, prefix, rp, _ptr(toks, C.c_int32), _ptr(offs, C.c_int64), n, C.byref(ty),
+              out.ctypes.data, C.byref(opts)), ctx)
+    del keep
+    return out, dbg
+
+
+def lmop_plan_rows(ctx, tokens, offsets, kind: int, allowed: Sequence[int], eos: int = -1,
+                   max_tokens: int = 1, prefix=None, row_prefix=None, flags: int = 0,
+                   max_batch_tokens: int = 0, limit: int = 0, limit_value: int = 1,
+                   row_mask=None, debug_logits: bool = False) -> dict:
+    """lmop_plan_rows: the plan lmop_eval_rows would use for these arguments
+    (a dict of lmop_eval_plan's fields); runs nothing on the device.
+    debug_logits plans the logit dump's scratch (the library writes nothing)."""
+    toks, offs, n, ty, opts, rp, keep = _call_args(tokens, offsets, kind, allowed, eos, max_tokens,
+                                                   row_prefix, flags, max_batch_tokens, limit,
+                                                   limit_value, row_mask)
+    if debug_logits:
+        dummy = np.zeros(1, dtype=np.float32)
+        keep.append(dummy)
+        opts.debug_logits = _ptr(dummy, C.c_float)
+    pl = lmop_eval_plan()
+    _check(_lib.lmop_plan_rows(ctx, prefix, rp, _ptr(toks, C.c_int32), _ptr(offs, C.c_int64), n,
+                               C.byref(ty), C.byref(opts), C.byref(pl)), ctx)
+    del keep
+    return {k: int(getattr(pl, k)) for k, _ in lmop_eval_plan._fields_ if k != "pad_"}
+
+
+def _call_args(tokens, offsets, kind, allowed, eos, max_tokens, row_prefix, flags,
+               max_batch_tokens, limit, limit_value, row_mask):
+    """The marshalled arguments shared by lmop_eval_rows and lmop_plan_rows:
+    token and offset arrays, row count, lmop_type, lmop_eval_opts, the row
+    prefix array, and the arrays those structs point into (kept alive by the
+    caller until the call returns)."""
     toks = _i32(tokens)
     offs = _i64(offsets)
     n = len(offs) - 1
@@ -275,9 +330,7 @@ def lmop_eval_rows(ctx, tokens, offsets, kind: int, allowed: Sequence[int], eos:
         al = _i32(allowed)
         keep = [al]
         ty = lmop_type(kind, _ptr(al, C.c_int32), len(al), int(eos), int(max_tokens), None)
-    out = np.zeros(max(n, 0), dtype=RESULT_DTYPE)
-    steps = max_tokens if kind in (LMOP_INT, LMOP_AUTOMATON) else 1
-    dbg = None
+    keep.append(ty)
     opts = lmop_eval_opts(flags, max_batch_tokens, None, int(limit), int(limit_value), None)
     if row_mask is not None:
         mk = np.ascontiguousarray(np.asarray(row_mask, dtype=bool).astype(np.uint8))
@@ -285,20 +338,11 @@ def lmop_eval_rows(ctx, tokens, offsets, kind: int, allowed: Sequence[int], eos:
             raise ValueError("row_mask needs one entry per row")
         keep.append(mk)
         opts.row_mask = _ptr(mk, C.c_uint8)
-    if debug_logits:
-        if vocab <= 0:
-            raise ValueError("debug_logits needs vocab")
-        dbg = np.empty((n, steps, vocab), dtype=np.float32)
-        opts.debug_logits = _ptr(dbg, C.c_float)
     rp = None
     if row_prefix is not None:
         rp = (C.c_void_p * max(n, 1))(*[r.value if isinstance(r, C.c_void_p) else r
                                         for r in row_prefix])
-    fn = _lib.lmop_eval_rows_noalloc if no_alloc else _lib.lmop_eval_rows
-    _check(fn(ctx, prefix, rp, _ptr(toks, C.c_int32), _ptr(offs, C.c_int64), n, C.byref(ty),
-              out.ctypes.data, C.byref(opts)), ctx)
-    del keep
-    return out, dbg
+    return toks, offs, n, ty, opts, rp, keep
 
 
 def lmop_dedup_rows(tokens, offsets, keys=None):
@@ -399,6 +443,14 @@ class Context:
         return lmop_eval_rows(self.ctx, tokens, offsets, kind, allowed, eos, max_tokens, prefix,
                               row_prefix, flags, max_batch_tokens, debug_logits, self.vocab,
                               limit, limit_value, row_mask, no_alloc)
+
+    def plan_rows(self, tokens, offsets, kind, allowed, eos=-1, max_tokens=1, prefix=None,
+                  row_prefix=None, no_dedup=False, max_batch_tokens=0, head_restricted=False,
+                  limit=0, limit_value=1, row_mask=None, debug_logits=False) -> dict:
+        flags = (LMOP_NO_DEDUP if no_dedup else 0) | (LMOP_HEAD_RESTRICTED if head_restricted else 0)
+        return lmop_plan_rows(self.ctx, tokens, offsets, kind, allowed, eos, max_tokens, prefix,
+                              row_prefix, flags, max_batch_tokens, limit, limit_value, row_mask,
+                              debug_logits)
 
     def set_workspace(self, ptr: int, nbytes: int):
         lmop_set_workspace(self.ctx, ptr, nbytes)

@@ -1012,3 +1012,45 @@ def test_tiny_device_error_is_sticky(tiny, L, monkeypatch):
     got = fresh.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, prefix=pre)
     assert got[0].tobytes() == want[0].tobytes()
     fresh.close()
+
+
+@pytest.mark.gpu
+def test_tiny_min_workspace_runs(tiny, L):
+    """A workspace of exactly the size lmop_plan_rows names as the minimum
+    runs the call on the GPU (one row per pass at this size), with results
+    equal bit for bit to library-allocated scratch, for a yes/no and an
+    integer type; the plan of a single-step call on a device ctx equals the
+    host-only ctx's."""
+    w, orc, ref_ctx = tiny
+    wl = make_workload("filter_tiny")
+    digits = np.random.default_rng(3).choice(TINY.vocab, 10, replace=False).astype(np.int32)
+    eos = int(next(t for t in range(TINY.vocab) if t not in digits))
+    cases = [((wl.tokens, wl.offsets, wl.kind, wl.allowed), {}),
+             ((wl.tokens, wl.offsets, KIND_INT, digits), dict(eos=eos, max_tokens=4))]
+    pre_ref = ref_ctx.set_prefix(wl.prefix)
+    wants = [ref_ctx.eval_rows(*a, prefix=pre_ref, debug_logits=True, **k) for a, k in cases]
+    ref_ctx.release_prefix(pre_ref)
+    host = L.Context(TINY, device=-1)
+    host.load_weights(w)
+    ctx = L.Context(TINY, device=0, stream=torch.cuda.current_stream().cuda_stream)
+    ctx.load_weights(w)
+    a0, k0 = cases[0]
+    assert ctx.plan_rows(*a0, **k0) == host.plan_rows(*a0, **k0)
+    pre = ctx.set_prefix(wl.prefix)
+    for (a, k), (want, dwant) in zip(cases, wants):
+        plan = ctx.plan_rows(*a, prefix=pre, debug_logits=True, **k)
+        need = plan["min_workspace_bytes"]
+        buf = torch.full((need // 4 + 64,), float("nan"), dtype=torch.float32, device="cuda")
+        torch.cuda.synchronize()
+        ctx.set_workspace(buf.data_ptr(), need)
+        small = ctx.plan_rows(*a, prefix=pre, debug_logits=True, **k)
+        got, dgot = ctx.eval_rows(*a, prefix=pre, debug_logits=True, **k)
+        ctx.set_workspace(0, 0)
+        del buf
+        _log(f"minimum workspace {need} bytes: {small['batches']} passes "
+             f"(library scratch: {plan['batches']} passes, {plan['scratch_bytes']} bytes)")
+        assert small["batches"] > plan["batches"]
+        assert got.tobytes() == want.tobytes()
+        assert np.array_equal(dgot, dwant, equal_nan=True)
+    ctx.close()
+    host.close()

@@ -339,3 +339,61 @@ def test_workspace_validation_and_plan(tiny_w):
     msg = _expect(L.LMOP_ERR_OOM, big.eval_rows, np.ones(100000, np.int32), [0, 100000],
                   L.LMOP_BOOL, [1, 2], no_alloc=True)
     assert "no-allocation" in msg
+
+
+def test_plan_rows_host(tiny_w):
+    """lmop_plan_rows on a host-only ctx: the batch plan of the call without
+    running it.  Checked against what the plan must satisfy: rows counted
+    after deduplication and the row mask; every pass within the token budget
+    unless one row alone exceeds it; passes at least total / budget; one
+    decode group per pass for single-step types; min_workspace_bytes is the
+    exact threshold of lmop_eval_rows in a workspace (one byte less is
+    LMOP_ERR_OOM, that size plans)."""
+    from synth import make_workload
+    ctx = _host_ctx()
+    ctx.load_weights(tiny_w)
+    wl = make_workload("filter_tiny")
+    lens = np.diff(wl.offsets)
+    args = (wl.tokens, wl.offsets, wl.kind, wl.allowed)
+    pl = ctx.plan_rows(*args)
+    assert pl["unique_rows"] == wl.n_rows and pl["batches"] == 1
+    assert pl["max_batch_tokens"] == lens.sum() <= pl["batch_tokens"]
+    assert pl["decode_groups"] == 1
+    assert 0 < pl["own_kv_bytes"] < pl["scratch_bytes"]
+    assert 0 < pl["min_workspace_bytes"] <= pl["scratch_bytes"] + 256
+    for budget in (50, 200, 777):
+        p = ctx.plan_rows(*args, max_batch_tokens=budget)
+        assert p["batch_tokens"] == budget
+        assert p["max_batch_tokens"] <= max(budget, lens.max())
+        assert p["batches"] >= -(-lens.sum() // budget)
+        assert p["decode_groups"] == p["batches"]
+        assert p["min_workspace_bytes"] == pl["min_workspace_bytes"]
+    # duplicates and the row mask shrink the evaluated rows
+    toks = np.concatenate([wl.tokens, wl.tokens])
+    offs = np.concatenate([wl.offsets, wl.offsets[1:] + wl.offsets[-1]])
+    assert ctx.plan_rows(toks, offs, wl.kind, wl.allowed)["unique_rows"] == wl.n_rows
+    assert ctx.plan_rows(toks, offs, wl.kind, wl.allowed, no_dedup=True)["unique_rows"] == 2 * wl.n_rows
+    mask = np.arange(wl.n_rows) % 3 == 0
+    assert ctx.plan_rows(*args, row_mask=mask)["unique_rows"] == mask.sum()
+    # integer outputs keep KV for the decode steps: a larger own-KV store
+    digits = np.arange(10, 20, dtype=np.int32)
+    pi = ctx.plan_rows(wl.tokens, wl.offsets, L.LMOP_INT, digits, eos=5, max_tokens=4)
+    assert pi["own_kv_bytes"] > pl["own_kv_bytes"] and pi["decode_groups"] >= 1
+    # the workspace threshold, for both types
+    for a, k in ((args, {}), ((wl.tokens, wl.offsets, L.LMOP_INT, digits), dict(eos=5, max_tokens=4))):
+        need = ctx.plan_rows(*a, **k)["min_workspace_bytes"]
+        ctx.set_workspace(1 << 20, need - 1)
+        _expect(L.LMOP_ERR_OOM, ctx.eval_rows, *a, **k)
+        _expect(L.LMOP_ERR_OOM, ctx.plan_rows, *a, **k)
+        ctx.set_workspace(1 << 20, need)
+        _expect(L.LMOP_ERR_UNSUPPORTED, ctx.eval_rows, *a, **k)
+        small = ctx.plan_rows(*a, **k)
+        assert small["scratch_bytes"] <= need and small["batches"] >= ctx.plan_rows(*a, **k)["batches"]
+        ctx.set_workspace(0, 0)
+    # argument errors are the call's own
+    _expect(L.LMOP_ERR_INVALID_ARG, ctx.plan_rows, [1, TINY.vocab], [0, 2], L.LMOP_BOOL, [1, 2])
+    assert ctx.plan_rows([], [0], L.LMOP_BOOL, [1, 2])["batches"] == 0
+    # the logit dump's scratch is planned when asked for
+    dump = ctx.plan_rows(*args, debug_logits=True)
+    assert dump["scratch_bytes"] >= pl["scratch_bytes"] + wl.n_rows * TINY.vocab * 4
+    assert dump["min_workspace_bytes"] > pl["min_workspace_bytes"]
