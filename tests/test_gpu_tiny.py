@@ -1054,3 +1054,38 @@ def test_tiny_min_workspace_runs(tiny, L):
         assert np.array_equal(dgot, dwant, equal_nan=True)
     ctx.close()
     host.close()
+
+
+@pytest.mark.gpu
+def test_tiny_plan_matches_run(tiny, L):
+    """lmop_plan_rows describes what the call then does: every forward pass
+    launches the embedding once, so a single-step call launches it once per
+    planned pass; an integer call adds, per decode group, between one and
+    max_tokens - 1 decode passes."""
+    w, orc, ctx = tiny
+    wl = make_workload("filter_tiny")
+    pre = ctx.set_prefix(wl.prefix)
+    digits = np.random.default_rng(3).choice(TINY.vocab, 10, replace=False).astype(np.int32)
+    eos = int(next(t for t in range(TINY.vocab) if t not in digits))
+    for budget in (97, 300, 0):
+        plan = ctx.plan_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, prefix=pre,
+                             max_batch_tokens=budget)
+        ctx.set_profiling(1)
+        ctx.eval_rows(wl.tokens, wl.offsets, wl.kind, wl.allowed, prefix=pre,
+                      max_batch_tokens=budget)
+        st = ctx.kernel_stats()
+        ctx.set_profiling(0)
+        assert st["embed"]["launches"] == plan["batches"], (budget, plan)
+        plan_i = ctx.plan_rows(wl.tokens, wl.offsets, KIND_INT, digits, eos=eos, max_tokens=4,
+                               prefix=pre, max_batch_tokens=budget)
+        ctx.set_profiling(1)
+        ctx.eval_rows(wl.tokens, wl.offsets, KIND_INT, digits, eos=eos, max_tokens=4, prefix=pre,
+                      max_batch_tokens=budget)
+        st = ctx.kernel_stats()
+        ctx.set_profiling(0)
+        n = st["embed"]["launches"]
+        g = plan_i["decode_groups"]
+        assert plan_i["batches"] + g <= n <= plan_i["batches"] + 3 * g, (budget, plan_i, n)
+        _log(f"budget {budget}: {plan['batches']} passes; integer: {plan_i['batches']} passes, "
+             f"{g} decode groups, {n} forward passes run")
+    ctx.release_prefix(pre)
