@@ -610,7 +610,8 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": f"f16 ({wdesc} weights, fp32 accum)",
         "data": f"synthetic (seeded uniform token ids, random-init N(0,0.02) {wdesc} weights)",
         "config": {"workload": wl.name, "model_shape": shape.name, "rows": rows,
-                   "unique_rows": n_unique, "prefix_tokens": len(wl.prefix),
+                   "unique_rows": n_unique, "unique_rows_per_s": n_unique / (ms_step * 1e-3),
+                   "prefix_tokens": len(wl.prefix),
                    "suffix_tokens": n_tok, "suffix_tokens_per_s": n_tok / (ms_step * 1e-3),
                    "batch_tokens": args.batch_tokens or 16384, "parallelism": "single GPU",
                    "head": "restricted" if args.head_restricted else "full vocabulary",
