@@ -471,9 +471,10 @@ hipError_t launch_cfg(hipStream_t s, const GemmArgs& a) {
 
 template <int WF, int EPI>
 hipError_t launch_epi(hipStream_t s, const GemmArgs& a) {
-  // the head's epilogue does not fit the register file next to a 256-token tile
-  if (a.M > 256) return launch_cfg<8, WF, EPI>(s, a);
-  if (a.M > 64) return launch_cfg<4, WF, EPI>(s, a);
+  // the largest token tile that still gives every CU a workgroup
+  const long ntn = a.N / 256;
+  if ((long)((a.M + 127) / 128) * ntn >= 256) return launch_cfg<8, WF, EPI>(s, a);
+  if ((long)((a.M + 63) / 64) * ntn >= 256) return launch_cfg<4, WF, EPI>(s, a);
   return launch_cfg<2, WF, EPI>(s, a);
 }
 
